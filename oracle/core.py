@@ -1,0 +1,187 @@
+"""ctypes wrapper of the C oracle (test infrastructure; see ipk_oracle.c).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg use
+this module.  It loads ``libipk_oracle.so`` (building it with gcc if it is
+missing or older than its source) and exposes each step of the block on numpy
+arrays.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import threading
+from typing import Dict, Optional
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+_lock = threading.Lock()
+
+i8p = C.POINTER(C.c_int8)
+u8p = C.POINTER(C.c_uint8)
+i32p = C.POINTER(C.c_int32)
+i64p = C.POINTER(C.c_int64)
+
+
+class OracleDesc(C.Structure):
+    _fields_ = [
+        ("d_model", C.c_int32), ("n_heads", C.c_int32), ("d_k", C.c_int32),
+        ("w_q", i8p), ("w_k", i8p), ("w_v", i8p), ("w_pos", i8p), ("w_out", i8p),
+        ("pos_bias_u", i8p), ("pos_bias_v", i8p),
+        ("mult_q", i32p), ("mult_k", i32p), ("mult_v", i32p), ("mult_pos", i32p), ("mult_out", i32p),
+        ("shift_q", C.c_int32), ("shift_k", C.c_int32), ("shift_v", C.c_int32),
+        ("shift_pos", C.c_int32), ("shift_out", C.c_int32),
+        ("m_c", C.c_int32), ("m_p", C.c_int32), ("shift_s", C.c_int32),
+        ("m_o", C.c_int32), ("shift_o", C.c_int32),
+        ("q_ln2", C.c_int32), ("q_b", C.c_int32), ("q_c", C.c_int32),
+    ]
+
+
+class OracleTrace(C.Structure):
+    _fields_ = [("q", i8p), ("k", i8p), ("v", i8p), ("p", i8p), ("s", i8p), ("a", u8p), ("ctx", i8p)]
+
+
+def lib():
+    global _lib
+    with _lock:
+        if _lib is None:
+            path = _build.build(force=False)
+            L = C.CDLL(path)
+            L.ipk_oracle_rs.restype = C.c_int64
+            L.ipk_oracle_rs.argtypes = [C.c_int64, C.c_int64, C.c_int32]
+            L.ipk_oracle_clamp8.restype = C.c_int64
+            L.ipk_oracle_clamp8.argtypes = [C.c_int64]
+            L.ipk_oracle_linear.restype = None
+            L.ipk_oracle_linear.argtypes = [i8p, C.c_int64, C.c_int32, i8p, C.c_int32, i32p, C.c_int32, i8p]
+            L.ipk_oracle_rel_shift.restype = None
+            L.ipk_oracle_rel_shift.argtypes = [i64p, C.c_int32, i64p]
+            L.ipk_oracle_fused_score.restype = C.c_int64
+            L.ipk_oracle_fused_score.argtypes = [C.c_int64, C.c_int64, C.c_int64, C.c_int64, C.c_int32]
+            L.ipk_oracle_iexp.restype = C.c_int64
+            L.ipk_oracle_iexp.argtypes = [C.c_int64, C.c_int64, C.c_int64, C.c_int64]
+            L.ipk_oracle_softmax_row.restype = None
+            L.ipk_oracle_softmax_row.argtypes = [i64p, C.c_int32, C.c_int64, C.c_int64, C.c_int64, u8p]
+            L.ipk_oracle_relpos_attn.restype = C.c_int
+            L.ipk_oracle_relpos_attn.argtypes = [C.POINTER(OracleDesc), i8p, i8p, i32p, C.c_int32, C.c_int32,
+                                                 i8p, C.POINTER(OracleTrace)]
+            _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray, t):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(t)
+
+
+def rs(a: int, m: int, n: int) -> int:
+    return int(lib().ipk_oracle_rs(int(a), int(m), int(n)))
+
+
+def clamp8(v: int) -> int:
+    return int(lib().ipk_oracle_clamp8(int(v)))
+
+
+def fused_score(c: int, p: int, m_c: int, m_p: int, shift_s: int) -> int:
+    return int(lib().ipk_oracle_fused_score(int(c), int(p), int(m_c), int(m_p), int(shift_s)))
+
+
+def iexp(d: int, q_ln2: int, q_b: int, q_c: int) -> int:
+    return int(lib().ipk_oracle_iexp(int(d), int(q_ln2), int(q_b), int(q_c)))
+
+
+def linear(x: np.ndarray, w: np.ndarray, mult: np.ndarray, shift: int) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    mult = np.ascontiguousarray(mult, dtype=np.int32)
+    rows, d_in = x.reshape(-1, x.shape[-1]).shape
+    d_out = w.shape[0]
+    assert w.shape[1] == d_in and mult.shape == (d_out,)
+    y = np.empty((rows, d_out), dtype=np.int8)
+    lib().ipk_oracle_linear(_p(x, i8p), rows, d_in, _p(w, i8p), d_out, _p(mult, i32p), int(shift), _p(y, i8p))
+    return y.reshape(x.shape[:-1] + (d_out,))
+
+
+def rel_shift(p: np.ndarray) -> np.ndarray:
+    """Phi on a [T][2T-1] matrix of position scores."""
+    p = np.ascontiguousarray(p, dtype=np.int64)
+    T = p.shape[0]
+    assert p.shape == (T, 2 * T - 1)
+    out = np.empty((T, T), dtype=np.int64)
+    lib().ipk_oracle_rel_shift(_p(p, i64p), T, _p(out, i64p))
+    return out
+
+
+def softmax_row(s: np.ndarray, q_ln2: int, q_b: int, q_c: int) -> np.ndarray:
+    s = np.ascontiguousarray(s, dtype=np.int64)
+    a = np.empty(s.shape[0], dtype=np.uint8)
+    lib().ipk_oracle_softmax_row(_p(s, i64p), s.shape[0], int(q_ln2), int(q_b), int(q_c), _p(a, u8p))
+    return a
+
+
+def make_desc(blk) -> (OracleDesc, list):
+    """Descriptor over a workloads.Block; returns it with the arrays it points into."""
+    c = blk.consts
+    keep = []
+
+    def arr(a, dt, t):
+        a = np.ascontiguousarray(a, dtype=dt)
+        keep.append(a)
+        return _p(a, t)
+
+    sh = blk.shape
+    D = OracleDesc()
+    D.d_model, D.n_heads, D.d_k = sh.d_model, sh.n_heads, sh.d_k
+    D.w_q, D.w_k, D.w_v = arr(blk.w_q, np.int8, i8p), arr(blk.w_k, np.int8, i8p), arr(blk.w_v, np.int8, i8p)
+    D.w_pos, D.w_out = arr(blk.w_pos, np.int8, i8p), arr(blk.w_out, np.int8, i8p)
+    D.pos_bias_u, D.pos_bias_v = arr(blk.pos_bias_u, np.int8, i8p), arr(blk.pos_bias_v, np.int8, i8p)
+    for w in ("q", "k", "v", "pos", "out"):
+        setattr(D, "mult_" + w, arr(c["mult_" + w], np.int32, i32p))
+        setattr(D, "shift_" + w, int(c["shift_" + w]))
+    for k in ("m_c", "m_p", "shift_s", "m_o", "shift_o", "q_ln2", "q_b", "q_c"):
+        setattr(D, k, int(c[k]))
+    return D, keep
+
+
+def relpos_attn(blk, x: Optional[np.ndarray] = None, lengths: Optional[np.ndarray] = None,
+                trace: bool = False, trace_scores: bool = False):
+    """Runs the whole block on host memory; returns y [B][T][d] (and a trace dict)."""
+    x = blk.x if x is None else x
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    B, T, d = x.shape
+    H = blk.shape.n_heads
+    lengths = blk.lengths if lengths is None else lengths
+    lens = np.ascontiguousarray(lengths, dtype=np.int32)
+    pe = np.ascontiguousarray(blk.pos_table, dtype=np.int8)
+    assert pe.shape == (2 * T - 1, d)
+    D, keep = make_desc(blk)
+    y = np.empty_like(x)
+    tr = None
+    out: Dict[str, np.ndarray] = {}
+    if trace or trace_scores:
+        tr = OracleTrace()
+        if trace:
+            for k in ("q", "k", "v", "ctx"):
+                out[k] = np.zeros((B, T, d), dtype=np.int8)
+                setattr(tr, k, _p(out[k], i8p))
+            out["p"] = np.zeros((2 * T - 1, d), dtype=np.int8)
+            tr.p = _p(out["p"], i8p)
+        if trace_scores:
+            out["s"] = np.zeros((B, H, T, T), dtype=np.int8)
+            out["a"] = np.zeros((B, H, T, T), dtype=np.uint8)
+            tr.s, tr.a = _p(out["s"], i8p), _p(out["a"], u8p)
+    rc = lib().ipk_oracle_relpos_attn(C.byref(D), _p(x, i8p), _p(pe, i8p), _p(lens, i32p), B, T, _p(y, i8p),
+                                      C.byref(tr) if tr is not None else None)
+    del keep
+    if rc != 0:
+        raise ValueError(f"oracle rejected its arguments (status {rc})")
+    return (y, out) if (trace or trace_scores) else y
+
+
+def stack(wl, layers: Optional[int] = None) -> np.ndarray:
+    """Chains the blocks of a workload: layer l+1 consumes layer l's int8 output."""
+    x = wl.blocks[0].x
+    for blk in wl.blocks[: (layers or len(wl.blocks))]:
+        x = relpos_attn(blk, x=x)
+    return x

@@ -1,0 +1,218 @@
+/*
+ * CPU oracle for the integer-only relative-positional multi-head self-attention
+ * block (Sec. 3.1 of "I-Parakeet: Integer-Only Conformer ASR on Mobile NPU").
+ *
+ * TEST INFRASTRUCTURE.  This file is the slow, plain reference the GPU library is
+ * checked against.  Only the test suite, the package's smoke check and the
+ * benchmark's CPU-baseline leg may load it; the product never does.  It shares no
+ * code, header or constant with the GPU path: its descriptor is declared here.
+ *
+ * Every quantity is an exact integer held in int64; there is no blocking, fusion
+ * or reordering beyond the definitions.  OpenMP only splits independent outer
+ * loops (output rows, attention rows) across threads.
+ *
+ * Readings of points the paper leaves open (the same list is kept with the
+ * design notes):
+ *  - round-to-nearest in Eq. 7 and Eq. 11 breaks ties upward:
+ *      RS(a, m, n) = floor((a*m + 2^(n-1)) / 2^n);
+ *  - int8 grids saturate to [-127, 127] (Eq. 6 clips to +-alpha, S = alpha/127);
+ *  - the fused score q_s lives on an int8 grid (one INT8 grid per tensor);
+ *  - the softmax follows I-BERT: integer exp with a second-order polynomial on
+ *    [-ln2, 0] and a right shift by the ln2 quotient, then F = floor(2^32 / sum)
+ *    and a = floor(e * F / 2^24), an 8-bit output on the 2^-8 grid; the single
+ *    value 256 that this can reach is clamped to 255;
+ *  - row r of the position table holds relative position T-1-r, so the relative
+ *    shift Phi reads column j-i+T-1 of row i (relative position i-j);
+ *  - keys j >= L_b are left out of the softmax; rows i >= L_b output zeros.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+  int32_t d_model, n_heads, d_k;
+  const int8_t *w_q, *w_k, *w_v, *w_pos, *w_out; /* [d_out][d_in] */
+  const int8_t *pos_bias_u, *pos_bias_v;         /* [H][d_k], on Q's grid */
+  const int32_t *mult_q, *mult_k, *mult_v, *mult_pos, *mult_out; /* [d] */
+  int32_t shift_q, shift_k, shift_v, shift_pos, shift_out;
+  int32_t m_c, m_p, shift_s;
+  int32_t m_o, shift_o;
+  int32_t q_ln2, q_b, q_c;
+} oracle_desc;
+
+/* Optional intermediates; every pointer may be NULL. */
+typedef struct {
+  int8_t *q, *k, *v; /* [B][T][d] */
+  int8_t *p;         /* [2T-1][d] */
+  int8_t *s;         /* [B][H][T][T]: fused scores of valid (row, key) pairs */
+  uint8_t *a;        /* [B][H][T][T]: softmax output of valid pairs */
+  int8_t *ctx;       /* [B][T][d] */
+} oracle_trace;
+
+/* floor(v / 2^n) for n >= 0, written without relying on signed shifts. */
+static int64_t floor_div_pow2(int64_t v, int32_t n) {
+  int64_t d = (int64_t)1 << n;
+  int64_t q = v / d; /* truncates toward zero */
+  if ((v % d) != 0 && v < 0) q -= 1;
+  return q;
+}
+
+/* Eq. 7: round(2^-n * m * a) with ties toward +infinity. */
+int64_t ipk_oracle_rs(int64_t a, int64_t m, int32_t n) {
+  int64_t half = n > 0 ? ((int64_t)1 << (n - 1)) : 0;
+  return floor_div_pow2(a * m + half, n);
+}
+
+/* Eq. 6 with b = 8: the symmetric int8 grid stops at +-127. */
+int64_t ipk_oracle_clamp8(int64_t v) { return v < -127 ? -127 : (v > 127 ? 127 : v); }
+
+/* Eq. 7: integer linear layer y = W x with INT32-range accumulation and one
+ * fixed-point multiplier per output channel (weights are per-channel, Sec. 2.2). */
+void ipk_oracle_linear(const int8_t* x, int64_t rows, int32_t d_in, const int8_t* w, int32_t d_out,
+                       const int32_t* mult, int32_t shift, int8_t* y) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < rows; ++t) {
+    for (int32_t c = 0; c < d_out; ++c) {
+      int64_t acc = 0;
+      for (int32_t i = 0; i < d_in; ++i) acc += (int64_t)x[t * d_in + i] * (int64_t)w[(int64_t)c * d_in + i];
+      y[t * d_out + c] = (int8_t)ipk_oracle_clamp8(ipk_oracle_rs(acc, mult[c], shift));
+    }
+  }
+}
+
+/* Phi for one query row i: out[j] = p[j - i + T - 1], j < T (Sec. 3.1: a pure
+ * index map; nothing is computed). */
+void ipk_oracle_rel_shift_row(const int64_t* p_row, int32_t i, int32_t T, int64_t* out_row) {
+  for (int32_t j = 0; j < T; ++j) out_row[j] = p_row[j - i + T - 1];
+}
+
+/* Phi on a whole [T][2T-1] position-score matrix, giving [T][T]. */
+void ipk_oracle_rel_shift(const int64_t* p, int32_t T, int64_t* out) {
+  for (int32_t i = 0; i < T; ++i) ipk_oracle_rel_shift_row(p + (int64_t)i * (2 * T - 1), i, T, out + (int64_t)i * T);
+}
+
+/* Eq. 11: fused content + position requantization of one score. */
+int64_t ipk_oracle_fused_score(int64_t c, int64_t p_shifted, int64_t m_c, int64_t m_p, int32_t shift_s) {
+  return ipk_oracle_clamp8(ipk_oracle_rs(m_c * c + m_p * p_shifted, 1, shift_s));
+}
+
+/* I-BERT integer exp of the non-positive integer -d (real value -d * S):
+ * split -d = -z*q_ln2 + r with r in (-q_ln2, 0], evaluate the polynomial
+ * (r + q_b)^2 + q_c (on grid a*S^2) and divide by 2^z. */
+int64_t ipk_oracle_iexp(int64_t d, int64_t q_ln2, int64_t q_b, int64_t q_c) {
+  int64_t z = d / q_ln2; /* d >= 0, q_ln2 >= 1 */
+  int64_t r = z * q_ln2 - d;
+  int64_t L = (r + q_b) * (r + q_b) + q_c;
+  if (z >= 62) return 0;
+  return L >> z; /* L >= 0 here, so the shift is a floor division */
+}
+
+/* I-BERT integer softmax over n integer scores: max, exp, sum, then the 8-bit
+ * normalization a = floor(e * floor(2^32 / sum) / 2^24), clamped to 255. */
+void ipk_oracle_softmax_row(const int64_t* s, int32_t n, int64_t q_ln2, int64_t q_b, int64_t q_c, uint8_t* a) {
+  int64_t M = s[0];
+  for (int32_t j = 1; j < n; ++j) if (s[j] > M) M = s[j];
+  int64_t* e = (int64_t*)malloc(sizeof(int64_t) * (size_t)n);
+  int64_t sum = 0;
+  for (int32_t j = 0; j < n; ++j) { e[j] = ipk_oracle_iexp(M - s[j], q_ln2, q_b, q_c); sum += e[j]; }
+  uint64_t F = sum > 0 ? ((uint64_t)1 << 32) / (uint64_t)sum : 0;
+  for (int32_t j = 0; j < n; ++j) {
+    uint64_t v = ((uint64_t)e[j] * F) >> 24;
+    a[j] = (uint8_t)(v > 255 ? 255 : v);
+  }
+  free(e);
+}
+
+/* The whole block: projections (Eq. 7), content and position scores (Eq. 8),
+ * Phi, fused requantization (Eq. 11), integer softmax, A V with Eq. 7's requant,
+ * and the output projection.  Returns 0, or -1 on an invalid argument. */
+int ipk_oracle_relpos_attn(const oracle_desc* D, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
+                           int32_t B, int32_t T, int8_t* y, oracle_trace* tr) {
+  if (!D || !x || !pos_table || !y || B < 1 || T < 1) return -1;
+  const int32_t d = D->d_model, H = D->n_heads, dk = D->d_k;
+  if (d != H * dk || D->q_ln2 < 1 || D->q_b < 0 || D->q_c < 0) return -1;
+  if ((int64_t)D->q_b * D->q_b + D->q_c == 0) return -1; /* e(0) must be positive */
+  for (int32_t b = 0; b < B; ++b)
+    if (lengths && (lengths[b] < 1 || lengths[b] > T)) return -1;
+  const int64_t rows = (int64_t)B * T, R = 2 * (int64_t)T - 1;
+
+  int8_t* Q = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* K = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* V = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* P = (int8_t*)malloc((size_t)(R * d));
+  int8_t* ctx = (int8_t*)calloc((size_t)(rows * d), 1);
+  if (!Q || !K || !V || !P || !ctx) { free(Q); free(K); free(V); free(P); free(ctx); return -2; }
+
+  /* Step 1: projections of every row, padded ones included. */
+  ipk_oracle_linear(x, rows, d, D->w_q, d, D->mult_q, D->shift_q, Q);
+  ipk_oracle_linear(x, rows, d, D->w_k, d, D->mult_k, D->shift_k, K);
+  ipk_oracle_linear(x, rows, d, D->w_v, d, D->mult_v, D->shift_v, V);
+  ipk_oracle_linear(pos_table, R, d, D->w_pos, d, D->mult_pos, D->shift_pos, P);
+
+  /* Steps 2-7, one (utterance, head, query row) at a time. */
+#pragma omp parallel
+  {
+    int64_t* c = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
+    int64_t* p = (int64_t*)malloc(sizeof(int64_t) * (size_t)R);
+    int64_t* pt = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
+    int64_t* s = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
+    uint8_t* a = (uint8_t*)malloc((size_t)T);
+#pragma omp for collapse(3) schedule(dynamic, 4)
+    for (int32_t b = 0; b < B; ++b)
+      for (int32_t h = 0; h < H; ++h)
+        for (int32_t i = 0; i < T; ++i) {
+          const int32_t L = lengths ? lengths[b] : T;
+          if (i >= L) continue; /* padded query rows stay zero */
+          const int8_t* q = Q + ((int64_t)b * T + i) * d + (int64_t)h * dk;
+          const int8_t* u = D->pos_bias_u + (int64_t)h * dk;
+          const int8_t* v = D->pos_bias_v + (int64_t)h * dk;
+          /* Eq. 8, content branch: (q + u) . k_j */
+          for (int32_t j = 0; j < T; ++j) {
+            const int8_t* kr = K + ((int64_t)b * T + j) * d + (int64_t)h * dk;
+            int64_t acc = 0;
+            for (int32_t k = 0; k < dk; ++k) acc += ((int64_t)q[k] + u[k]) * (int64_t)kr[k];
+            c[j] = acc;
+          }
+          /* Eq. 8, position branch before Phi: (q + v) . p_r for every relative position */
+          for (int64_t r = 0; r < R; ++r) {
+            const int8_t* pr = P + r * d + (int64_t)h * dk;
+            int64_t acc = 0;
+            for (int32_t k = 0; k < dk; ++k) acc += ((int64_t)q[k] + v[k]) * (int64_t)pr[k];
+            p[r] = acc;
+          }
+          ipk_oracle_rel_shift_row(p, i, T, pt);
+          /* Eq. 11 on the valid keys, then the integer softmax */
+          for (int32_t j = 0; j < L; ++j) s[j] = ipk_oracle_fused_score(c[j], pt[j], D->m_c, D->m_p, D->shift_s);
+          ipk_oracle_softmax_row(s, L, D->q_ln2, D->q_b, D->q_c, a);
+          if (tr && tr->s)
+            for (int32_t j = 0; j < L; ++j) tr->s[(((int64_t)b * H + h) * T + i) * T + j] = (int8_t)s[j];
+          if (tr && tr->a)
+            for (int32_t j = 0; j < L; ++j) tr->a[(((int64_t)b * H + h) * T + i) * T + j] = a[j];
+          /* A V, requantized to the context grid (Eq. 7 with the scalar m_o) */
+          for (int32_t k = 0; k < dk; ++k) {
+            int64_t acc = 0;
+            for (int32_t j = 0; j < L; ++j) acc += (int64_t)a[j] * (int64_t)V[((int64_t)b * T + j) * d + (int64_t)h * dk + k];
+            ctx[((int64_t)b * T + i) * d + (int64_t)h * dk + k] =
+                (int8_t)ipk_oracle_clamp8(ipk_oracle_rs(acc, D->m_o, D->shift_o));
+          }
+        }
+    free(c); free(p); free(pt); free(s); free(a);
+  }
+
+  /* Step 8: output projection of the valid rows; padded rows are zero. */
+  memset(y, 0, (size_t)(rows * d));
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t L = lengths ? lengths[b] : T;
+    ipk_oracle_linear(ctx + (int64_t)b * T * d, L, d, D->w_out, d, D->mult_out, D->shift_out, y + (int64_t)b * T * d);
+  }
+
+  if (tr) {
+    if (tr->q) memcpy(tr->q, Q, (size_t)(rows * d));
+    if (tr->k) memcpy(tr->k, K, (size_t)(rows * d));
+    if (tr->v) memcpy(tr->v, V, (size_t)(rows * d));
+    if (tr->p) memcpy(tr->p, P, (size_t)(R * d));
+    if (tr->ctx) memcpy(tr->ctx, ctx, (size_t)(rows * d));
+  }
+  free(Q); free(K); free(V); free(P); free(ctx);
+  return 0;
+}

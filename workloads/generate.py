@@ -1,0 +1,294 @@
+"""Seeded synthetic workloads for the integer relative-position attention block.
+
+The paper evaluates a trained Parakeet-CTC-0.6B on LibriSpeech and Common Voice;
+neither the weights nor the audio are available, so these generators stand in for
+them with inputs of the same shapes, value ranges and length mix:
+
+* frames come at 80 ms after the 8x subsampling of the pre-encoder (Sec. 2.1),
+  so T = 125 is 10 s, T = 375 is 30 s and T = 2500 is 200 s of audio;
+* every tensor is symmetric int8, clipped to +-127 (Eq. 6, b = 8);
+* weights carry one scale per output channel, activations one per tensor
+  (Sec. 2.2);
+* the relative-position table is the sinusoidal embedding of the 2T-1 relative
+  positions (Sec. 3.1), quantized with S_pe = 1/127;
+* fixed-point multipliers use n = 16 (Eq. 7).
+
+Two scale regimes exist.  ``literal`` draws every per-tensor scale (and every
+per-channel weight scale) uniformly from [2^-8, 2^-4].  ``calibrated`` gives the
+real-valued activations unit variance and the weights Xavier scale, and then sets
+each grid to cover +-4 standard deviations of the tensor it quantizes, estimated
+from the known input distributions (no data pass); this gives non-saturated
+integer ranges.  Draw order is fixed: x, W_q, W_k, W_v, W_pos, W_out, u, v,
+scales, lengths.
+
+The conversion of real scales to integers (the multiplier m of Eq. 7, m_c and
+m_p of Eq. 11, and the integer softmax constants of I-BERT) is done here, once,
+with exact decimal arithmetic: the block itself only ever sees the integers.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+from decimal import Decimal, ROUND_FLOOR, getcontext
+from typing import Dict, List, Optional
+
+import numpy as np
+
+getcontext().prec = 80
+
+SHIFT_N = 16  # the paper's fixed-point shift n (Eq. 7)
+S_PE = 1.0 / 127.0  # grid of the quantized sinusoid table
+S_A = 2.0 ** -8  # grid of the 8-bit softmax output (I-BERT)
+SCALE_LO, SCALE_HI = 2.0 ** -8, 2.0 ** -4
+# I-BERT's second-order polynomial for exp on [-ln 2, 0]: a (p + b)^2 + c
+IEXP_A, IEXP_B, IEXP_C = 0.3585, 1.353, 0.344
+LN2 = Decimal(2).ln()
+
+
+@dataclasses.dataclass(frozen=True)
+class ConfigShape:
+    name: str
+    B: int
+    T: int
+    d_model: int
+    n_heads: int
+    layers: int = 1
+    x_dist: str = "gauss"  # "gauss": N(0, 32); "student_t3": 16 * t(df=3)
+    len_lo: Optional[int] = None  # per-utterance lengths ~ U{len_lo..T}
+
+    @property
+    def d_k(self) -> int:
+        return self.d_model // self.n_heads
+
+
+# The five workloads: a tiny block; one Parakeet-scale block on 10 s of audio;
+# 16 utterances of up to 30 s with a key padding mask; 200 s of long-form audio
+# with heavy-tailed input; and a 24-block encoder stack.
+CONFIGS: List[ConfigShape] = [
+    ConfigShape("tiny", B=1, T=64, d_model=256, n_heads=4),
+    ConfigShape("parakeet", B=1, T=125, d_model=1024, n_heads=8),
+    ConfigShape("batched", B=16, T=375, d_model=1024, n_heads=8, len_lo=200),
+    ConfigShape("longform", B=1, T=2500, d_model=1024, n_heads=8, x_dist="student_t3"),
+    ConfigShape("stack", B=8, T=500, d_model=1024, n_heads=8, layers=24),
+]
+BASE_SEED = 20260
+
+
+def config_by_name(name_or_idx) -> ConfigShape:
+    if isinstance(name_or_idx, int):
+        return CONFIGS[name_or_idx]
+    for c in CONFIGS:
+        if c.name == name_or_idx:
+            return c
+    raise KeyError(name_or_idx)
+
+
+@dataclasses.dataclass
+class Block:
+    """One block's integer inputs (numpy, host) plus the scales they came from.
+
+    Layouts: x [B][T][d]; weights [d_out][d_in] (y = x W^T); pos_bias_u/v [H][d_k]
+    on Q's grid; pos_table [2T-1][d] with row r holding relative position T-1-r;
+    lengths [B].
+    """
+
+    shape: ConfigShape
+    T: int
+    x: Optional[np.ndarray]
+    w_q: np.ndarray
+    w_k: np.ndarray
+    w_v: np.ndarray
+    w_pos: np.ndarray
+    w_out: np.ndarray
+    pos_bias_u: np.ndarray
+    pos_bias_v: np.ndarray
+    pos_table: np.ndarray
+    lengths: np.ndarray
+    scales: Dict[str, object]
+    consts: Dict[str, object]
+
+
+@dataclasses.dataclass
+class Workload:
+    shape: ConfigShape
+    regime: str
+    seed: int
+    blocks: List[Block]
+
+
+def sinusoid_table(T: int, d: int) -> np.ndarray:
+    """int8 [2T-1][d] sinusoidal relative-position table, row r = position T-1-r.
+
+    Even columns hold sin(rel * 10000^(-2k/d)), odd columns the matching cos
+    (Transformer-XL's embedding, used by the Conformer MHSA of Sec. 3.1),
+    quantized as round(127 * value).
+    """
+    rel = (T - 1 - np.arange(2 * T - 1, dtype=np.float64))[:, None]
+    k = np.arange(d // 2, dtype=np.float64)[None, :]
+    ang = rel * np.power(10000.0, -2.0 * k / d)
+    pe = np.empty((2 * T - 1, d), dtype=np.float64)
+    pe[:, 0::2] = np.sin(ang)
+    pe[:, 1::2] = np.cos(ang)
+    return np.clip(np.rint(127.0 * pe), -127, 127).astype(np.int8)
+
+
+def _dec(v) -> Decimal:
+    return v if isinstance(v, Decimal) else Decimal(float(v))
+
+
+def fixed_point(ratio, n: int = SHIFT_N) -> int:
+    """m = round(2^n * ratio), ties upward (the offline multiplier of Eq. 7)."""
+    v = _dec(ratio) * (Decimal(2) ** n) + Decimal("0.5")
+    m = int(v.to_integral_value(rounding=ROUND_FLOOR))
+    if not 0 <= m < (1 << 23):
+        raise ValueError(f"fixed-point multiplier {m} outside [0, 2^23)")
+    return m
+
+
+def softmax_constants(S_s: float):
+    """I-BERT integer-exp constants for a score grid S_s (floors of real ratios)."""
+    S = _dec(S_s)
+    q_ln2 = int((LN2 / S).to_integral_value(rounding=ROUND_FLOOR))
+    q_b = int((Decimal(str(IEXP_B)) / S).to_integral_value(rounding=ROUND_FLOOR))
+    q_c = int((Decimal(str(IEXP_C)) / (Decimal(str(IEXP_A)) * S * S)).to_integral_value(rounding=ROUND_FLOOR))
+    return q_ln2, q_b, q_c
+
+
+def _draw_x(rng, shape: ConfigShape, T: int) -> np.ndarray:
+    size = (shape.B, T, shape.d_model)
+    if shape.x_dist == "gauss":
+        v = rng.normal(0.0, 32.0, size=size)
+    elif shape.x_dist == "student_t3":
+        v = 16.0 * rng.standard_t(3, size=size)
+    else:
+        raise ValueError(shape.x_dist)
+    return np.clip(np.rint(v), -127, 127).astype(np.int8)
+
+
+def _uniform_i8(rng, size) -> np.ndarray:
+    return rng.integers(-127, 128, size=size, dtype=np.int64).astype(np.int8)
+
+
+SIGMA_W = math.sqrt((255.0 ** 2 - 1.0) / 12.0)  # std of U{-127..127}
+SIGMA_PE = 127.0 / math.sqrt(2.0)  # rms of round(127 sin)
+
+
+def _sigma_x(shape: ConfigShape) -> float:
+    return 32.0 if shape.x_dist == "gauss" else 16.0 * math.sqrt(3.0)
+
+
+def _scales_literal(rng, shape: ConfigShape, S_x: Optional[float]):
+    d = shape.d_model
+    u = lambda size=None: rng.uniform(SCALE_LO, SCALE_HI, size=size)  # noqa: E731
+    sc = {}
+    sc["S_x"] = float(u()) if S_x is None else float(S_x)
+    for w in ("q", "k", "v", "pos", "out"):
+        sc["S_W" + w] = u(d)
+    for t in ("S_Q", "S_K", "S_V", "S_P", "S_s", "S_O", "S_y"):
+        sc[t] = float(u())
+    return sc
+
+
+def _scales_calibrated(rng, shape: ConfigShape, S_x: Optional[float], logit_gain: float):
+    d, dk = shape.d_model, shape.d_k
+    kcov = 4.0  # grids cover +-4 standard deviations
+    sc = {}
+    sc["S_x"] = (1.0 / _sigma_x(shape)) if S_x is None else float(S_x)
+    sx_real = sc["S_x"] * _sigma_x(shape)
+    w_base = 1.0 / (SIGMA_W * math.sqrt(d))  # Xavier-scaled weights
+    for w in ("q", "k", "v", "pos", "out"):
+        sc["S_W" + w] = w_base * rng.uniform(0.75, 1.0, size=d)
+    sc["S_Wq"] = sc["S_Wq"] * logit_gain
+    rms = lambda a: float(np.sqrt(np.mean(np.square(a))))  # noqa: E731
+    sq = sx_real * rms(sc["S_Wq"]) * SIGMA_W * math.sqrt(d)
+    sk = sx_real * rms(sc["S_Wk"]) * SIGMA_W * math.sqrt(d)
+    sv = sx_real * rms(sc["S_Wv"]) * SIGMA_W * math.sqrt(d)
+    sp = (S_PE * SIGMA_PE) * rms(sc["S_Wpos"]) * SIGMA_W * math.sqrt(d)
+    sc["S_Q"], sc["S_K"], sc["S_V"], sc["S_P"] = (kcov * s / 127.0 for s in (sq, sk, sv, sp))
+    su = sc["S_Q"] * SIGMA_W  # u, v are int8 on Q's grid
+    logit = math.sqrt((sq * sq + su * su) * (sk * sk + sp * sp))
+    sc["S_s"] = float(np.clip(kcov * logit / 127.0, SCALE_LO, SCALE_HI))
+    sc["S_O"] = sc["S_V"]  # a convex combination of V rows stays on V's range
+    sy = 0.5 * sv * rms(sc["S_Wout"]) * SIGMA_W * math.sqrt(d)
+    sc["S_y"] = kcov * sy / 127.0
+    return sc
+
+
+def _consts_from_scales(sc, shape: ConfigShape):
+    """Integer descriptor constants from real scales (Eq. 7, Eq. 11, I-BERT)."""
+    n = SHIFT_N
+    c = {}
+    srcs = {"q": ("S_x", "S_Q"), "k": ("S_x", "S_K"), "v": ("S_x", "S_V"),
+            "pos": (None, "S_P"), "out": ("S_O", "S_y")}
+    for w, (sin, sout) in srcs.items():
+        s_in = _dec(S_PE) if sin is None else _dec(sc[sin])
+        s_out = _dec(sc[sout])
+        c["mult_" + w] = np.array([fixed_point(s_in * _dec(sw) / s_out, n) for sw in sc["S_W" + w]],
+                                  dtype=np.int32)
+        c["shift_" + w] = n
+    sqrt_dk = _dec(shape.d_k).sqrt()
+    S_Q, S_K, S_P, S_s = (_dec(sc[k]) for k in ("S_Q", "S_K", "S_P", "S_s"))
+    c["m_c"] = fixed_point(S_Q * S_K / (S_s * sqrt_dk), n)
+    c["m_p"] = fixed_point(S_Q * S_P / (S_s * sqrt_dk), n)
+    c["shift_s"] = n
+    c["m_o"] = fixed_point(_dec(S_A) * _dec(sc["S_V"]) / _dec(sc["S_O"]), n)
+    c["shift_o"] = n
+    c["q_ln2"], c["q_b"], c["q_c"] = softmax_constants(sc["S_s"])
+    return c
+
+
+def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str = "literal",
+               with_x: bool = True, S_x: Optional[float] = None, lengths=None,
+               logit_gain: float = 1.0) -> Block:
+    d, H, dk = shape.d_model, shape.n_heads, shape.d_k
+    x = _draw_x(rng, shape, T) if with_x else None
+    ws = [_uniform_i8(rng, (d, d)) for _ in range(5)]
+    u = _uniform_i8(rng, (H, dk))
+    v = _uniform_i8(rng, (H, dk))
+    if regime == "literal":
+        sc = _scales_literal(rng, shape, S_x)
+    elif regime == "calibrated":
+        sc = _scales_calibrated(rng, shape, S_x, logit_gain)
+    else:
+        raise ValueError(regime)
+    sc["S_pe"], sc["S_A"] = S_PE, S_A
+    if lengths is None:
+        if shape.len_lo is not None:
+            lengths = rng.integers(shape.len_lo, T + 1, size=shape.B)
+        else:
+            lengths = np.full(shape.B, T)
+    lengths = np.asarray(lengths, dtype=np.int32)
+    return Block(shape=shape, T=T, x=x, w_q=ws[0], w_k=ws[1], w_v=ws[2], w_pos=ws[3], w_out=ws[4],
+                 pos_bias_u=u, pos_bias_v=v, pos_table=sinusoid_table(T, d), lengths=lengths,
+                 scales=sc, consts=_consts_from_scales(sc, shape))
+
+
+def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = None,
+                  layers: Optional[int] = None, T: Optional[int] = None, B: Optional[int] = None,
+                  logit_gain: float = 1.0) -> Workload:
+    """All blocks of one named workload; the stack seeds layer l with seed + l.
+
+    ``T``, ``B`` and ``layers`` override the configured sizes (smaller cases of
+    the same recipe for tests).
+    """
+    shape = config_by_name(name_or_idx)
+    if B is not None:
+        shape = dataclasses.replace(shape, B=B)
+    idx = [c.name for c in CONFIGS].index(shape.name)
+    seed = BASE_SEED + idx if seed is None else seed
+    T = shape.T if T is None else T
+    if shape.len_lo is not None and T < shape.len_lo:
+        shape = dataclasses.replace(shape, len_lo=max(1, T // 2))
+    nl = shape.layers if layers is None else layers
+    blocks: List[Block] = []
+    S_x = None
+    lengths = None
+    for layer in range(nl):
+        rng = np.random.default_rng(seed + layer)
+        blk = make_block(shape, T, rng, regime, with_x=(layer == 0), S_x=S_x, lengths=lengths,
+                         logit_gain=logit_gain)
+        blocks.append(blk)
+        S_x = blk.scales["S_y"]
+        lengths = blk.lengths
+    return Workload(shape=shape, regime=regime, seed=seed, blocks=blocks)
