@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""Throughput of the integer relative-position MHSA block on one MI355X.
+
+A step is one call of the whole block (Q|K|V and position projections, rank-1
+bias terms, the attention core with the integer softmax, A.V and the output
+projection) on the long-form workload: B=1, T=2500 frames (200 s of audio at
+80 ms per frame), d_model=1024, H=8, d_k=128, int8 inputs with heavy-tailed x.
+Inputs are resident in HBM before the timed region.
+
+Prints one JSON line.  ``value`` is algorithmic int8 tera-operations per second
+(2 x the multiply-accumulates the method needs: projections of the valid rows,
+the position projection once, and content + position + A.V over the valid
+(query, key) pairs).  ``roofline`` reports the attention core against the dense
+INT8 MFMA peak, its duration measured with HIP events on the launch stream over
+the timed region.  ``cpu_baseline`` is the CPU oracle on the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "int8 rel-pos attention TOPS & encoder frames/sec (T=2500, d=1024, H=8), % INT8 peak"
+INT8_PEAK_TOPS = 5000.0  # MI355X dense INT8 MFMA, 5.0 POP/s
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_macs(B, T, d, H, dk, lengths):
+    """MACs the method needs for one call: Eq. 7 projections of the valid rows (Q, K,
+    V and output), the position projection of the 2T-1 table rows, and the content,
+    position and A.V contractions over the valid (query, key) pairs."""
+    sl = int(np.sum(lengths))
+    sl2 = int(np.sum(np.asarray(lengths, dtype=np.int64) ** 2))
+    proj = 4 * sl * d * d
+    pos = (2 * T - 1) * d * d
+    attn = 3 * H * dk * sl2
+    return proj, pos, attn
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="longform")
+    ap.add_argument("--regime", default="literal", choices=["literal", "calibrated"])
+    ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
+    ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(utterances and heads would shard without exchange; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_30846_amd import ipk
+    from workloads import make_workload
+
+    ipk.load()  # fails loudly when the HIP library is missing
+    wl = make_workload(args.workload, args.regime)
+    blk = wl.blocks[0]
+    sh = blk.shape
+    B, T, d, H, dk = blk.x.shape[0], blk.T, sh.d_model, sh.n_heads, sh.d_k
+    lengths = blk.lengths
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    mod = ipk.RelPosAttn.from_block(blk, device=dev)
+    x = torch.from_numpy(blk.x).to(dev)
+    pe = torch.from_numpy(blk.pos_table).to(dev)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        mod(x, pe, lengths=lengths, y=y, stream=stream)
+    torch.cuda.synchronize()
+
+    # per-step stage events, recorded by the library on the launch stream
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for row in evs:
+        for e in row:
+            e.record(stream)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        ipk.ipk_relpos_attn_record_stages(mod.handle, evs[k])
+        mod(x, pe, lengths=lengths, y=y, stream=stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+
+    stage_names = ["projections", "bias_terms", "attention", "out_projection"]
+    stage_ms = np.zeros(4)
+    for row in evs:
+        for i in range(4):
+            stage_ms[i] += row[i].elapsed_time(row[i + 1])
+    stage_ms /= args.steps
+
+    proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
+    ops = 2 * (proj + pos + attn)
+    tops = ops / (ms_step * 1e-3) / 1e12
+    frames = float(np.sum(lengths)) / (ms_step * 1e-3)
+    attn_tops = 2 * attn / (stage_ms[2] * 1e-3) / 1e12
+
+    rec = {
+        "metric": METRIC,
+        "value": round(tops, 3),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: B={B} T={T} d_model={d} H={H} d_k={dk}, int8 block, "
+                        f"{args.regime} scales, seed {wl.seed}",
+            "global_batch": B,
+            "seq_len": T,
+            "parallelism": "none (1 GPU)",
+        },
+        "frames_per_s": round(frames, 1),
+        "pct_int8_peak": round(100.0 * tops / INT8_PEAK_TOPS, 3),
+        "algorithmic_ops": ops,
+        "stage_ms": {n: round(float(v), 5) for n, v in zip(stage_names, stage_ms)},
+        "wall_s_timed_region": round(wall, 4),
+        "roofline": {
+            "kernel": "relpos_attn_core",
+            "bound": "mfma",
+            "achieved": round(attn_tops, 3),
+            "peak": INT8_PEAK_TOPS,
+            "unit": "TOP/s",
+            "frac": round(attn_tops / INT8_PEAK_TOPS, 5),
+            "traffic": None,
+        },
+    }
+
+    if args.cpu_baseline:
+        from oracle import core
+
+        ncores = len(os.sched_getaffinity(0))
+        os.environ.setdefault("OMP_NUM_THREADS", str(ncores))
+        t1 = time.perf_counter()
+        y_ref = core.relpos_attn(blk)
+        cpu_s = time.perf_counter() - t1
+        exact = bool(np.array_equal(y_ref, y.cpu().numpy()))
+        rec["cpu_baseline"] = {
+            "value": round(ops / cpu_s / 1e12, 6),
+            "unit": "TOPS",
+            "cores": core.num_threads(),
+            "kind": "oracle",
+            "sample": f"one whole call of the same workload ({args.workload}, B={B}, T={T}); "
+                      f"{cpu_s:.2f} s; output bit-exact vs GPU: {exact}",
+        }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,169 @@
+/*
+ * ipk: integer-only relative-positional multi-head self-attention on MI355X (gfx950).
+ *
+ * The block is the MHSA term of the Conformer block (Eq. 2) of "I-Parakeet:
+ * Integer-Only Conformer ASR on Mobile NPU", computed entirely in integers as in
+ * Sec. 3.1:
+ *
+ *   Q, K, V  = clamp8(RS(x W^T, mult[c], shift))            (Eq. 7, per channel)
+ *   P        = clamp8(RS(pe W_pos^T, mult_pos[c], shift))    (Eq. 7)
+ *   c_ij     = (Q_i + u) . K_j                                (Eq. 8, content)
+ *   p_ij     = (Q_i + v) . P_{j-i+T-1}                        (Eq. 8 with Phi as
+ *                                                              an index map)
+ *   s_ij     = clamp8(RS(m_c c_ij + m_p p_ij, 1, shift_s))    (Eq. 11)
+ *   a_ij     = I-BERT integer softmax of s_i. (8-bit, grid 2^-8)
+ *   ctx_i    = clamp8(RS(sum_j a_ij V_j, m_o, shift_o))       (Eq. 7)
+ *   y        = clamp8(RS(ctx W_out^T, mult_out[c], shift))    (Eq. 7)
+ *
+ * with RS(a, m, n) = floor((a m + 2^(n-1)) / 2^n) (round to nearest, ties up) and
+ * clamp8(v) = min(max(v, -127), 127) (symmetric int8 grid, Eq. 6 with b = 8).
+ * The I-BERT softmax over the valid keys j < L_b of row i is: M = max_j s_ij;
+ * d = M - s_ij; z = floor(d / q_ln2); r = z q_ln2 - d; e_ij = ((r + q_b)^2 + q_c) >> z;
+ * F = floor(2^32 / sum_j e_ij); a_ij = min(floor(e_ij F / 2^24), 255).
+ * Rows i >= L_b of y are zero.
+ *
+ * All run-time arguments are integers; real scales never reach the library.
+ * Every entry point returns an ipk_status and never throws.  The text of the
+ * last error on the calling thread is available from ipk_last_error().
+ */
+#ifndef IPK_H
+#define IPK_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define IPK_ABI_VERSION 1
+
+/* Status codes. */
+typedef enum ipk_status {
+  IPK_OK = 0,
+  IPK_ERR_INVALID_ARG = -1,   /* a pointer, size or constant outside its documented range */
+  IPK_ERR_UNSUPPORTED = -2,   /* valid per the method but outside this implementation's limits */
+  IPK_ERR_OUT_OF_MEMORY = -3, /* a device or host allocation failed */
+  IPK_ERR_HIP = -4            /* the HIP runtime reported an error (launch, copy, device) */
+} ipk_status;
+
+/* Implementation limits (checked by ipk_relpos_attn_create / _run). */
+#define IPK_MAX_BATCH 256 /* utterances per call */
+#define IPK_MAX_T 8192    /* frames per utterance */
+
+/*
+ * Block descriptor, read only during ipk_relpos_attn_create.
+ *
+ * Shapes: d_model = n_heads * d_k, d_k in {64, 128}; max_batch in [1, IPK_MAX_BATCH]
+ * and max_T in [1, IPK_MAX_T] size the handle's workspace.
+ *
+ * Weights (DEVICE pointers, int8, [d_out = d_model][d_in = d_model], row-major,
+ * nn.Linear convention y = x W^T): w_q, w_k, w_v (the three projections of
+ * Eq. 8's Q, K, V), w_pos (projection of the sinusoidal relative-position
+ * embeddings, Sec. 3.1), w_out (output projection).
+ * pos_bias_u, pos_bias_v (DEVICE, int8, [n_heads][d_k]): the learned biases u, v of
+ * Eq. 8, on the grid of Q.
+ *
+ * Requantization (HOST pointers, int32, [d_model]): mult_{q,k,v,pos,out}[c] is
+ * the fixed-point multiplier m of Eq. 7 for output channel c (per-channel weight
+ * scales, Sec. 2.2; per-tensor scales are the case of equal entries), with the
+ * shared shift shift_{q,k,v,pos,out} (the paper's n = 16).
+ * Fused score (Eq. 11): m_c, m_p, shift_s.  Context requant (A V, Eq. 7): m_o, shift_o.
+ * Ranges: 0 <= mult < 2^23 for every multiplier; 1 <= shift <= 40.
+ *
+ * Softmax constants (I-BERT integer exp for the score grid S_s):
+ * q_ln2 = floor(ln2 / S_s) >= 1, q_b = floor(b / S_s) >= 0,
+ * q_c = floor(c / (a S_s^2)) >= 0 with (a, b, c) = (0.3585, 1.353, 0.344).
+ * Implementation limits: the polynomial (r + q_b)^2 + q_c must stay below 2^24
+ * for r in (-q_ln2, 0], must be at least 2^8 at r = 0, and max_T times its maximum
+ * must stay below 2^32 (IPK_ERR_UNSUPPORTED otherwise).
+ *
+ * Zero points zp_x, zp_y must be 0: quantization is symmetric (Eq. 6).
+ */
+typedef struct ipk_relpos_attn_desc {
+  int32_t d_model, n_heads, d_k;
+  int32_t max_batch, max_T;
+  const int8_t *w_q, *w_k, *w_v, *w_pos, *w_out;
+  const int8_t *pos_bias_u, *pos_bias_v;
+  const int32_t *mult_q, *mult_k, *mult_v, *mult_pos, *mult_out;
+  int32_t shift_q, shift_k, shift_v, shift_pos, shift_out;
+  int32_t m_c, m_p, shift_s;
+  int32_t m_o, shift_o;
+  int32_t q_ln2, q_b, q_c;
+  int32_t zp_x, zp_y;
+} ipk_relpos_attn_desc;
+
+typedef struct ipk_relpos_attn ipk_relpos_attn_t;
+
+/*
+ * Validates the descriptor, allocates the handle and its device workspace for
+ * (max_batch, max_T), and copies the weights, biases and multipliers into it on
+ * the current HIP device.  Synchronizes its own copies, so the caller may free its
+ * buffers when it returns.
+ * Returns IPK_OK and sets *out, or a negative status with *out = NULL and nothing
+ * leaked (IPK_ERR_INVALID_ARG, IPK_ERR_UNSUPPORTED, IPK_ERR_OUT_OF_MEMORY, IPK_ERR_HIP).
+ */
+int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t** out);
+
+/*
+ * Runs the block on `stream` (a hipStream_t; NULL is the default stream).
+ * x        DEVICE int8 [B][T][d_model]   block input
+ * pos_table DEVICE int8 [2T-1][d_model]  sinusoidal relative-position table; row r
+ *                                        holds relative position T-1-r
+ * lengths  HOST int32 [B] valid frames L_b in [1, T], or NULL for all T; the values
+ *          are captured when the call returns (the array may be reused at once)
+ * y        DEVICE int8 [B][T][d_model]   block output; rows t >= L_b are zero
+ * x, pos_table and y must be 16-byte aligned.
+ * The call is asynchronous: it enqueues kernels and returns.  Pointers are borrowed
+ * until the stream work completes.  The handle's workspace is shared by all calls:
+ * calls on one handle must be ordered on one stream (calls on different streams
+ * race).  x and y may not overlap.
+ * Errors: IPK_ERR_INVALID_ARG (null handle/x/pos_table/y, B < 1, T < 1,
+ * B > max_batch, T > max_T, a length outside [1, T]); IPK_ERR_HIP (launch failure).
+ * On an error nothing is enqueued.
+ */
+int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
+                        int32_t B, int32_t T, int8_t* y, void* stream);
+
+/* Frees the handle and its workspace after synchronizing the device; NULL is a no-op.
+ * Returns IPK_OK (or IPK_ERR_HIP if the device reported an error). */
+int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h);
+
+/*
+ * Copies one intermediate of the last run from the handle's workspace into a
+ * caller buffer (DEVICE pointer `dst` of `bytes` bytes), on `stream`, for tests and
+ * debugging.  Layouts for the last run's (B, T):
+ *   IPK_INTER_Q, IPK_INTER_K:  int8 [B][T][d_model]
+ *   IPK_INTER_V:               int8 [B][T][d_model]
+ *   IPK_INTER_P:               int8 [2T-1][d_model]
+ *   IPK_INTER_CTX:             int8 [B][T][d_model] (attention output before W_out)
+ * Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`, bytes too small, null),
+ * IPK_ERR_HIP.
+ */
+enum { IPK_INTER_Q = 0, IPK_INTER_K = 1, IPK_INTER_V = 2, IPK_INTER_P = 3, IPK_INTER_CTX = 4 };
+int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
+
+/*
+ * Stage timing for profiling: the NEXT run on `h` records the five caller-created
+ * HIP events events[0..4] (hipEvent_t, created with timing enabled) on its stream
+ * before the Q|K|V and position projections, before the bias/prefix-sum kernel,
+ * before the attention core, before the output projection, and after it.  The
+ * events are used once; later runs record nothing until this is called again.
+ * events = NULL clears a pending request.  Errors: IPK_ERR_INVALID_ARG (null
+ * handle, or a null entry in events).
+ */
+int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
+
+/* Human-readable name of a status code (static storage). */
+const char* ipk_status_string(int status);
+
+/* Text of the last error reported on the calling thread ("" if none). */
+const char* ipk_last_error(void);
+
+/* IPK_ABI_VERSION of the loaded library. */
+int ipk_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IPK_H */

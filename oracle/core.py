@@ -49,6 +49,8 @@ def lib():
         if _lib is None:
             path = _build.build(force=False)
             L = C.CDLL(path)
+            L.ipk_oracle_num_threads.restype = C.c_int
+            L.ipk_oracle_num_threads.argtypes = []
             L.ipk_oracle_rs.restype = C.c_int64
             L.ipk_oracle_rs.argtypes = [C.c_int64, C.c_int64, C.c_int32]
             L.ipk_oracle_clamp8.restype = C.c_int64
@@ -73,6 +75,10 @@ def lib():
 def _p(a: np.ndarray, t):
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data_as(t)
+
+
+def num_threads() -> int:
+    return int(lib().ipk_oracle_num_threads())
 
 
 def rs(a: int, m: int, n: int) -> int:

@@ -25,6 +25,7 @@
  *    shift Phi reads column j-i+T-1 of row i (relative position i-j);
  *  - keys j >= L_b are left out of the softmax; rows i >= L_b output zeros.
  */
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -48,6 +49,9 @@ typedef struct {
   uint8_t *a;        /* [B][H][T][T]: softmax output of valid pairs */
   int8_t *ctx;       /* [B][T][d] */
 } oracle_trace;
+
+/* Threads the parallel loops will use. */
+int ipk_oracle_num_threads(void) { return omp_get_max_threads(); }
 
 /* floor(v / 2^n) for n >= 0, written without relying on signed shifts. */
 static int64_t floor_div_pow2(int64_t v, int32_t n) {

@@ -1,0 +1,289 @@
+// C-ABI entry points of the ipk library: descriptor validation, the handle and its
+// workspace, and the per-run launch sequence
+//   projections (Q|K|V and the position table) -> rank-1 bias terms and V prefix
+//   sums -> attention core -> output projection.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "../../include/ipk.h"
+#include "ipk_internal.h"
+
+namespace ipk {
+int attn_rows_per_block(int T_al);
+}
+
+using namespace ipk;
+
+struct ipk_relpos_attn {
+  int device;
+  int d, H, DK, max_B, max_T;
+  Weights w;
+  Scalars sc;
+  Workspace ws;
+  std::vector<void*> allocs;
+  RunShape last;
+  bool has_run;
+  hipEvent_t stage_ev[5];
+  bool stages_pending;
+};
+
+static thread_local char g_last_error[512];
+
+static int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+static bool mult_ok(int64_t m) { return m >= 0 && m < (1 << 23); }
+static bool shift_ok(int32_t s) { return s >= 1 && s <= 40; }
+
+static int validate_desc(const ipk_relpos_attn_desc* d) {
+  if (!d) return fail(IPK_ERR_INVALID_ARG, "desc is NULL");
+  if (d->d_k != 64 && d->d_k != 128) return fail(IPK_ERR_UNSUPPORTED, "d_k=%d: only 64 and 128 are built", d->d_k);
+  if (d->n_heads < 1 || d->d_model != d->n_heads * d->d_k)
+    return fail(IPK_ERR_INVALID_ARG, "d_model=%d must equal n_heads=%d * d_k=%d", d->d_model, d->n_heads, d->d_k);
+  if (d->d_model > 16384) return fail(IPK_ERR_UNSUPPORTED, "d_model=%d above 16384", d->d_model);
+  if (d->max_batch < 1 || d->max_batch > IPK_MAX_BATCH)
+    return fail(IPK_ERR_INVALID_ARG, "max_batch=%d outside [1, %d]", d->max_batch, IPK_MAX_BATCH);
+  if (d->max_T < 1 || d->max_T > IPK_MAX_T)
+    return fail(IPK_ERR_INVALID_ARG, "max_T=%d outside [1, %d]", d->max_T, IPK_MAX_T);
+  const void* ptrs[] = {d->w_q, d->w_k, d->w_v, d->w_pos, d->w_out, d->pos_bias_u, d->pos_bias_v,
+                        d->mult_q, d->mult_k, d->mult_v, d->mult_pos, d->mult_out};
+  for (const void* p : ptrs)
+    if (!p) return fail(IPK_ERR_INVALID_ARG, "a weight, bias or multiplier pointer is NULL");
+  const int32_t* mults[] = {d->mult_q, d->mult_k, d->mult_v, d->mult_pos, d->mult_out};
+  const char* names[] = {"mult_q", "mult_k", "mult_v", "mult_pos", "mult_out"};
+  for (int t = 0; t < 5; ++t)
+    for (int c = 0; c < d->d_model; ++c)
+      if (!mult_ok(mults[t][c])) return fail(IPK_ERR_INVALID_ARG, "%s[%d]=%d outside [0, 2^23)", names[t], c, mults[t][c]);
+  const int32_t shifts[] = {d->shift_q, d->shift_k, d->shift_v, d->shift_pos, d->shift_out, d->shift_s, d->shift_o};
+  for (int32_t s : shifts)
+    if (!shift_ok(s)) return fail(IPK_ERR_INVALID_ARG, "a shift (%d) is outside [1, 40]", s);
+  if (!mult_ok(d->m_c) || !mult_ok(d->m_p) || !mult_ok(d->m_o))
+    return fail(IPK_ERR_INVALID_ARG, "m_c=%d, m_p=%d, m_o=%d must be in [0, 2^23)", d->m_c, d->m_p, d->m_o);
+  if (d->q_ln2 < 1 || d->q_b < 0 || d->q_c < 0)
+    return fail(IPK_ERR_INVALID_ARG, "softmax constants need q_ln2 >= 1, q_b >= 0, q_c >= 0");
+  // the integer-exp polynomial over r in (-q_ln2, 0]
+  const int64_t qb = d->q_b, lo = qb - (d->q_ln2 - 1);
+  const int64_t sq_max = qb * qb > lo * lo ? qb * qb : lo * lo;
+  const int64_t poly_max = sq_max + d->q_c, poly0 = qb * qb + d->q_c;
+  if (poly_max >= ((int64_t)1 << 24))
+    return fail(IPK_ERR_UNSUPPORTED, "integer-exp polynomial reaches %lld >= 2^24", (long long)poly_max);
+  if (poly0 < 256) return fail(IPK_ERR_UNSUPPORTED, "integer exp of 0 is %lld < 2^8", (long long)poly0);
+  if ((int64_t)d->max_T * poly_max >= ((int64_t)1 << 32))
+    return fail(IPK_ERR_UNSUPPORTED, "max_T * max exp = %lld reaches 2^32", (long long)d->max_T * poly_max);
+  if (d->zp_x != 0 || d->zp_y != 0) return fail(IPK_ERR_INVALID_ARG, "zero points must be 0 (symmetric grids)");
+  return IPK_OK;
+}
+
+static void free_handle(ipk_relpos_attn* h) {
+  if (!h) return;
+  for (void* p : h->allocs) (void)hipFree(p);
+  delete h;
+}
+
+template <typename T>
+static hipError_t dev_alloc(ipk_relpos_attn* h, T** p, size_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
+  if (e != hipSuccess) return e;
+  h->allocs.push_back(q);
+  *p = (T*)q;
+  return hipSuccess;
+}
+
+extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t** out) {
+  g_last_error[0] = 0;
+  if (!out) return fail(IPK_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int st = validate_desc(desc);
+  if (st != IPK_OK) return st;
+  if (attn_rows_per_block(t_aligned(desc->max_T)) == 0)
+    return fail(IPK_ERR_UNSUPPORTED, "max_T=%d does not fit the on-chip score rows", desc->max_T);
+
+  ipk_relpos_attn* h = new (std::nothrow) ipk_relpos_attn();
+  if (!h) return fail(IPK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    free_handle(h);
+    return fail(IPK_ERR_HIP, "hipGetDevice failed");
+  }
+  h->d = desc->d_model;
+  h->H = desc->n_heads;
+  h->DK = desc->d_k;
+  h->max_B = desc->max_batch;
+  h->max_T = desc->max_T;
+  h->sc = Scalars{desc->m_c, desc->m_p, desc->shift_s, desc->m_o, desc->shift_o, desc->q_ln2, desc->q_b, desc->q_c};
+  h->has_run = false;
+  h->stages_pending = false;
+
+  const size_t d = h->d, H = h->H, DK = h->DK, Bm = h->max_B;
+  const size_t T_al = t_aligned(h->max_T), PR = p_rows((int)T_al);
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+  };
+  chk(dev_alloc(h, &h->w.w_qkv, 3 * d * d));
+  chk(dev_alloc(h, &h->w.w_pos, d * d));
+  chk(dev_alloc(h, &h->w.w_out, d * d));
+  chk(dev_alloc(h, &h->w.u, H * DK));
+  chk(dev_alloc(h, &h->w.v, H * DK));
+  chk(dev_alloc(h, &h->w.mult_qkv, 3 * d));
+  chk(dev_alloc(h, &h->w.shift_qkv, 3 * d));
+  chk(dev_alloc(h, &h->w.mult_pos, d));
+  chk(dev_alloc(h, &h->w.shift_pos, d));
+  chk(dev_alloc(h, &h->w.mult_out, d));
+  chk(dev_alloc(h, &h->w.shift_out, d));
+  chk(dev_alloc(h, &h->ws.q, Bm * H * T_al * DK));
+  chk(dev_alloc(h, &h->ws.k, Bm * H * T_al * DK));
+  chk(dev_alloc(h, &h->ws.vt, Bm * H * DK * T_al));
+  chk(dev_alloc(h, &h->ws.p, H * PR * DK));
+  chk(dev_alloc(h, &h->ws.ctx, Bm * (size_t)h->max_T * d));
+  chk(dev_alloc(h, &h->ws.bu, Bm * H * T_al));
+  chk(dev_alloc(h, &h->ws.bv, H * PR));
+  chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK + 1) * DK));
+  if (e != hipSuccess) {
+    free_handle(h);
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
+                hipGetErrorString(e));
+  }
+  // weights (device to device), multipliers (host to device)
+  chk(hipMemcpy(h->w.w_qkv, desc->w_q, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.w_qkv + d * d, desc->w_k, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.w_qkv + 2 * d * d, desc->w_v, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.w_pos, desc->w_pos, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.w_out, desc->w_out, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
+  chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
+  std::vector<int32_t> mq(3 * d), sq(3 * d), sp(d, desc->shift_pos), so(d, desc->shift_out);
+  for (size_t c = 0; c < d; ++c) {
+    mq[c] = desc->mult_q[c];
+    mq[d + c] = desc->mult_k[c];
+    mq[2 * d + c] = desc->mult_v[c];
+    sq[c] = desc->shift_q;
+    sq[d + c] = desc->shift_k;
+    sq[2 * d + c] = desc->shift_v;
+  }
+  chk(hipMemcpy(h->w.mult_qkv, mq.data(), 3 * d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.shift_qkv, sq.data(), 3 * d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.mult_pos, desc->mult_pos, d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.shift_pos, sp.data(), d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.mult_out, desc->mult_out, d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.shift_out, so.data(), d * 4, hipMemcpyHostToDevice));
+  // deterministic contents for the padding rows of the workspace
+  chk(hipMemset(h->ws.p, 0, H * PR * DK));
+  chk(hipMemset(h->ws.vt, 0, Bm * H * DK * T_al));
+  chk(hipMemset(h->ws.k, 0, Bm * H * T_al * DK));
+  chk(hipMemset(h->ws.q, 0, Bm * H * T_al * DK));
+  chk(hipDeviceSynchronize());
+  if (e != hipSuccess) {
+    free_handle(h);
+    (void)hipGetLastError();
+    return fail(IPK_ERR_HIP, "copying the weights failed: %s", hipGetErrorString(e));
+  }
+  *out = h;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
+                                   const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!x || !pos_table || !y) return fail(IPK_ERR_INVALID_ARG, "x, pos_table and y must be non-NULL");
+  if (((uintptr_t)x | (uintptr_t)pos_table | (uintptr_t)y) & 15)
+    return fail(IPK_ERR_INVALID_ARG, "x, pos_table and y must be 16-byte aligned");
+  if (B < 1 || B > h->max_B) return fail(IPK_ERR_INVALID_ARG, "B=%d outside [1, max_batch=%d]", B, h->max_B);
+  if (T < 1 || T > h->max_T) return fail(IPK_ERR_INVALID_ARG, "T=%d outside [1, max_T=%d]", T, h->max_T);
+  Lengths lens;
+  for (int b = 0; b < B; ++b) {
+    const int L = lengths ? lengths[b] : T;
+    if (L < 1 || L > T) return fail(IPK_ERR_INVALID_ARG, "lengths[%d]=%d outside [1, T=%d]", b, L, T);
+    lens.len[b] = L;
+  }
+  for (int b = B; b < IPK_MAX_BATCH; ++b) lens.len[b] = 0;
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d};
+  hipStream_t st = (hipStream_t)stream;
+  const bool rec = h->stages_pending;
+  h->stages_pending = false;
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (rec && e == hipSuccess) e = hipEventRecord(h->stage_ev[i], st);
+  };
+  mark(0);
+  if (e == hipSuccess) e = launch_projections(rs, h->w, h->ws, x, pos_table, st);
+  mark(1);
+  if (e == hipSuccess) e = launch_bias_terms(rs, h->w, h->ws, lens, st);
+  mark(2);
+  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st);
+  mark(3);
+  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st);
+  mark(4);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  h->last = rs;
+  h->has_run = true;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst, int64_t bytes,
+                                            void* stream) {
+  if (!h || !dst) return fail(IPK_ERR_INVALID_ARG, "handle and dst must be non-NULL");
+  if (!h->has_run) return fail(IPK_ERR_INVALID_ARG, "no run yet");
+  if (which < IPK_INTER_Q || which > IPK_INTER_CTX) return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
+  const RunShape& rs = h->last;
+  const int64_t need = (which == IPK_INTER_P ? (int64_t)(2 * rs.T - 1) : (int64_t)rs.B * rs.T) * rs.d;
+  if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
+  hipError_t e = launch_gather_intermediate(rs, h->ws, which, (int8_t*)dst, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "gather failed: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!events) {
+    h->stages_pending = false;
+    return IPK_OK;
+  }
+  for (int i = 0; i < 5; ++i)
+    if (!events[i]) return fail(IPK_ERR_INVALID_ARG, "events[%d] is NULL", i);
+  for (int i = 0; i < 5; ++i) h->stage_ev[i] = (hipEvent_t)events[i];
+  h->stages_pending = true;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h) {
+  if (!h) return IPK_OK;
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(h->device);
+  hipError_t e = hipDeviceSynchronize();
+  free_handle(h);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+extern "C" const char* ipk_status_string(int status) {
+  switch (status) {
+    case IPK_OK: return "IPK_OK";
+    case IPK_ERR_INVALID_ARG: return "IPK_ERR_INVALID_ARG";
+    case IPK_ERR_UNSUPPORTED: return "IPK_ERR_UNSUPPORTED";
+    case IPK_ERR_OUT_OF_MEMORY: return "IPK_ERR_OUT_OF_MEMORY";
+    case IPK_ERR_HIP: return "IPK_ERR_HIP";
+    default: return "IPK_ERR_UNKNOWN";
+  }
+}
+
+extern "C" const char* ipk_last_error(void) { return g_last_error; }
+
+extern "C" int ipk_abi_version(void) { return IPK_ABI_VERSION; }

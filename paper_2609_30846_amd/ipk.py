@@ -1,0 +1,223 @@
+"""Python binding of the ipk C ABI (include/ipk.h): argument marshalling only.
+
+Every step of the block runs in the HIP kernels of ``libipk.so``.  There is no
+fallback: ``load()`` raises if the library is not built, and every entry point
+raises ``IpkError`` when the library returns a non-zero status.  Device buffers
+are torch tensors on the current HIP device; streams are torch streams.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libipk.so")
+
+IPK_OK = 0
+IPK_ERR_INVALID_ARG = -1
+IPK_ERR_UNSUPPORTED = -2
+IPK_ERR_OUT_OF_MEMORY = -3
+IPK_ERR_HIP = -4
+IPK_MAX_BATCH = 256
+IPK_MAX_T = 8192
+IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX = range(5)
+
+# Every function the header declares, as (name, restype, argtypes).
+_vp = C.c_void_p
+SIGNATURES = [
+    ("ipk_relpos_attn_create", C.c_int, [_vp, C.POINTER(_vp)]),
+    ("ipk_relpos_attn_run", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
+    ("ipk_relpos_attn_destroy", C.c_int, [_vp]),
+    ("ipk_relpos_attn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
+    ("ipk_relpos_attn_record_stages", C.c_int, [_vp, _vp]),
+    ("ipk_status_string", C.c_char_p, [C.c_int]),
+    ("ipk_last_error", C.c_char_p, []),
+    ("ipk_abi_version", C.c_int, []),
+]
+
+
+class IpkError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_name(status)}: {msg}")
+        self.status = status
+
+
+class Desc(C.Structure):
+    """Mirror of ipk_relpos_attn_desc."""
+
+    _fields_ = [
+        ("d_model", C.c_int32), ("n_heads", C.c_int32), ("d_k", C.c_int32),
+        ("max_batch", C.c_int32), ("max_T", C.c_int32),
+        ("w_q", _vp), ("w_k", _vp), ("w_v", _vp), ("w_pos", _vp), ("w_out", _vp),
+        ("pos_bias_u", _vp), ("pos_bias_v", _vp),
+        ("mult_q", _vp), ("mult_k", _vp), ("mult_v", _vp), ("mult_pos", _vp), ("mult_out", _vp),
+        ("shift_q", C.c_int32), ("shift_k", C.c_int32), ("shift_v", C.c_int32),
+        ("shift_pos", C.c_int32), ("shift_out", C.c_int32),
+        ("m_c", C.c_int32), ("m_p", C.c_int32), ("shift_s", C.c_int32),
+        ("m_o", C.c_int32), ("shift_o", C.c_int32),
+        ("q_ln2", C.c_int32), ("q_b", C.c_int32), ("q_c", C.c_int32),
+        ("zp_x", C.c_int32), ("zp_y", C.c_int32),
+    ]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load():
+    """Loads libipk.so (raises FileNotFoundError if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise FileNotFoundError(
+                    f"{LIB_PATH} is not built; run python -m paper_2609_30846_amd.build (no CPU fallback exists)")
+            lib = C.CDLL(LIB_PATH)
+            for name, res, args in SIGNATURES:
+                f = getattr(lib, name)
+                f.restype = res
+                f.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def status_name(status: int) -> str:
+    try:
+        return load().ipk_status_string(int(status)).decode()
+    except FileNotFoundError:
+        return str(status)
+
+
+def last_error() -> str:
+    return load().ipk_last_error().decode()
+
+
+def abi_version() -> int:
+    return int(load().ipk_abi_version())
+
+
+def _check(status: int):
+    if status != IPK_OK:
+        raise IpkError(status, last_error())
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def ipk_relpos_attn_create(desc: Desc) -> int:
+    h = _vp()
+    _check(load().ipk_relpos_attn_create(C.byref(desc), C.byref(h)))
+    return h.value
+
+
+def ipk_relpos_attn_run(h: int, x, pos_table, lengths: Optional[Sequence[int]], B: int, T: int, y,
+                        stream=None) -> None:
+    lens = None
+    if lengths is not None:
+        lens = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    lp = lens.ctypes.data if lens is not None else None
+    _check(load().ipk_relpos_attn_run(h, _ptr(x), _ptr(pos_table), lp, int(B), int(T), _ptr(y),
+                                      _stream_ptr(stream)))
+
+
+def ipk_relpos_attn_destroy(h: Optional[int]) -> None:
+    _check(load().ipk_relpos_attn_destroy(h))
+
+
+def ipk_relpos_attn_intermediate(h: int, which: int, dst, stream=None) -> None:
+    _check(load().ipk_relpos_attn_intermediate(h, int(which), _ptr(dst), int(dst.numel() * dst.element_size()),
+                                               _stream_ptr(stream)))
+
+
+def ipk_relpos_attn_record_stages(h: int, events) -> None:
+    """``events``: five torch.cuda.Event(enable_timing=True), already recorded once."""
+    if events is None:
+        _check(load().ipk_relpos_attn_record_stages(h, None))
+        return
+    arr = (_vp * 5)(*[int(e.cuda_event) for e in events])
+    _check(load().ipk_relpos_attn_record_stages(h, arr))
+
+
+class RelPosAttn:
+    """Owns one handle: device copies of a block's weights, built from host arrays.
+
+    ``weights`` maps w_q, w_k, w_v, w_pos, w_out ([d][d] int8), pos_bias_u/v
+    ([H][d_k] int8); ``consts`` maps mult_{q,k,v,pos,out} ([d] int32) and the
+    integer scalars of the descriptor.  Host arrays are copied to the device only
+    for the duration of create.
+    """
+
+    def __init__(self, d_model: int, n_heads: int, weights: dict, consts: dict, max_batch: int, max_T: int,
+                 device=None):
+        import torch
+
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        keep = {}
+        desc = Desc()
+        desc.d_model, desc.n_heads, desc.d_k = d_model, n_heads, d_model // n_heads
+        desc.max_batch, desc.max_T = max_batch, max_T
+        for k in ("w_q", "w_k", "w_v", "w_pos", "w_out", "pos_bias_u", "pos_bias_v"):
+            t = torch.as_tensor(np.ascontiguousarray(weights[k], dtype=np.int8)).to(dev)
+            keep[k] = t
+            setattr(desc, k, t.data_ptr())
+        for w in ("q", "k", "v", "pos", "out"):
+            m = np.ascontiguousarray(consts["mult_" + w], dtype=np.int32)
+            keep["mult_" + w] = m
+            setattr(desc, "mult_" + w, m.ctypes.data)
+            setattr(desc, "shift_" + w, int(consts["shift_" + w]))
+        for k in ("m_c", "m_p", "shift_s", "m_o", "shift_o", "q_ln2", "q_b", "q_c"):
+            setattr(desc, k, int(consts[k]))
+        desc.zp_x = int(consts.get("zp_x", 0))
+        desc.zp_y = int(consts.get("zp_y", 0))
+        with torch.cuda.device(dev):
+            self.handle = ipk_relpos_attn_create(desc)
+        self.device = dev
+        self.d_model, self.n_heads = d_model, n_heads
+        self.max_batch, self.max_T = max_batch, max_T
+
+    @classmethod
+    def from_block(cls, blk, max_batch: Optional[int] = None, max_T: Optional[int] = None, device=None):
+        weights = {k: getattr(blk, k) for k in ("w_q", "w_k", "w_v", "w_pos", "w_out", "pos_bias_u", "pos_bias_v")}
+        return cls(blk.shape.d_model, blk.shape.n_heads, weights, blk.consts,
+                   max_batch or blk.shape.B, max_T or blk.T, device)
+
+    def __call__(self, x, pos_table, lengths=None, y=None, stream=None):
+        import torch
+
+        B, T, d = x.shape
+        if y is None:
+            y = torch.empty_like(x)
+        ipk_relpos_attn_run(self.handle, x, pos_table, lengths, B, T, y, stream)
+        return y
+
+    def intermediate(self, which: int, shape, stream=None):
+        import torch
+
+        dst = torch.empty(shape, dtype=torch.int8, device=self.device)
+        ipk_relpos_attn_intermediate(self.handle, which, dst, stream)
+        return dst
+
+    def close(self):
+        if getattr(self, "handle", None):
+            ipk_relpos_attn_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

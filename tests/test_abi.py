@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: exported symbols, header/binding agreement and the
+validation errors create/run return before any HIP call."""
+
+import ctypes as C
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2609_30846_amd import ipk
+from workloads import make_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ipk.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ipk_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ipk.load()
+    declared = _declared_functions()
+    assert declared, "no declarations parsed"
+    for name in declared:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", ipk.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(re.findall(r" T (ipk_\w+)", out.stdout))
+    assert set(declared) <= exported
+    # the binding declares exactly the header's functions
+    assert sorted(n for n, _, _ in ipk.SIGNATURES) == declared
+
+
+def test_status_strings_and_version():
+    assert ipk.abi_version() == 1
+    assert ipk.status_name(0) == "IPK_OK"
+    assert ipk.status_name(-1) == "IPK_ERR_INVALID_ARG"
+    assert ipk.status_name(-2) == "IPK_ERR_UNSUPPORTED"
+    assert ipk.status_name(-3) == "IPK_ERR_OUT_OF_MEMORY"
+    assert ipk.status_name(-4) == "IPK_ERR_HIP"
+    assert ipk.status_name(7) == "IPK_ERR_UNKNOWN"
+
+
+def test_descriptor_struct_matches_header_field_order():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct ipk_relpos_attn_desc \{(.*?)\}", text, flags=re.S).group(1)
+    names = re.findall(r"\*?(\w+)\s*[,;]", body)
+    assert names == [f[0] for f in ipk.Desc._fields_]
+
+
+def _valid_desc():
+    """A descriptor that passes validation (weights point to dummy host memory)."""
+    blk = make_workload("tiny", "calibrated").blocks[0]
+    keep = []
+    d = ipk.Desc()
+    d.d_model, d.n_heads, d.d_k = 256, 4, 64
+    d.max_batch, d.max_T = 1, 64
+    dummy = np.zeros(16, dtype=np.int8)
+    keep.append(dummy)
+    for k in ("w_q", "w_k", "w_v", "w_pos", "w_out", "pos_bias_u", "pos_bias_v"):
+        setattr(d, k, dummy.ctypes.data)
+    for w in ("q", "k", "v", "pos", "out"):
+        m = np.ascontiguousarray(blk.consts["mult_" + w], dtype=np.int32)
+        keep.append(m)
+        setattr(d, "mult_" + w, m.ctypes.data)
+        setattr(d, "shift_" + w, 16)
+    for k in ("m_c", "m_p", "shift_s", "m_o", "shift_o", "q_ln2", "q_b", "q_c"):
+        setattr(d, k, int(blk.consts[k]))
+    return d, keep
+
+
+def _create_status(desc):
+    h = C.c_void_p()
+    st = ipk.load().ipk_relpos_attn_create(C.byref(desc), C.byref(h))
+    assert h.value is None  # never a handle on failure
+    return st
+
+
+BAD = [
+    ("d_k", 96, ipk.IPK_ERR_UNSUPPORTED),
+    ("d_model", 250, ipk.IPK_ERR_INVALID_ARG),
+    ("n_heads", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("max_batch", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("max_batch", 257, ipk.IPK_ERR_INVALID_ARG),
+    ("max_T", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("max_T", 8193, ipk.IPK_ERR_INVALID_ARG),
+    ("w_pos", None, ipk.IPK_ERR_INVALID_ARG),
+    ("mult_out", None, ipk.IPK_ERR_INVALID_ARG),
+    ("shift_q", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("shift_s", 41, ipk.IPK_ERR_INVALID_ARG),
+    ("m_c", -1, ipk.IPK_ERR_INVALID_ARG),
+    ("m_p", 1 << 23, ipk.IPK_ERR_INVALID_ARG),
+    ("m_o", -5, ipk.IPK_ERR_INVALID_ARG),
+    ("q_ln2", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("q_b", -1, ipk.IPK_ERR_INVALID_ARG),
+    ("q_c", -1, ipk.IPK_ERR_INVALID_ARG),
+    ("q_b", 5000, ipk.IPK_ERR_UNSUPPORTED),  # polynomial above 2^24
+    ("zp_x", 3, ipk.IPK_ERR_INVALID_ARG),
+    ("zp_y", -1, ipk.IPK_ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("field,value,want", BAD)
+def test_create_rejects_invalid_descriptor(field, value, want):
+    d, keep = _valid_desc()
+    setattr(d, field, value)
+    assert _create_status(d) == want
+    assert ipk.last_error() != ""
+
+
+def test_create_rejects_small_exp_and_long_sum():
+    d, keep = _valid_desc()
+    d.q_b, d.q_c = 10, 100  # exp(0) = 200 < 2^8
+    assert _create_status(d) == ipk.IPK_ERR_UNSUPPORTED
+    d, keep = _valid_desc()
+    d.q_ln2, d.q_b, d.q_c, d.max_T = 2, 4000, 0, 8192  # 8192 * 16e6 >= 2^32
+    assert _create_status(d) == ipk.IPK_ERR_UNSUPPORTED
+
+
+def test_create_rejects_out_of_range_multiplier_entry():
+    d, keep = _valid_desc()
+    bad = np.full(256, 7, dtype=np.int32)
+    bad[100] = 1 << 23
+    keep.append(bad)
+    d.mult_v = bad.ctypes.data
+    assert _create_status(d) == ipk.IPK_ERR_INVALID_ARG
+    assert "mult_v[100]" in ipk.last_error()
+
+
+def test_null_arguments_rejected():
+    lib = ipk.load()
+    assert lib.ipk_relpos_attn_create(None, None) == ipk.IPK_ERR_INVALID_ARG
+    h = C.c_void_p(1234)
+    assert lib.ipk_relpos_attn_create(None, C.byref(h)) == ipk.IPK_ERR_INVALID_ARG
+    assert h.value is None
+    assert lib.ipk_relpos_attn_run(None, None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_relpos_attn_intermediate(None, 0, None, 0, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_relpos_attn_destroy(None) == ipk.IPK_OK
+
+
+def test_generated_constants_pass_validation_ranges():
+    # every workload's integers sit inside the ranges create() accepts
+    for name in ("tiny", "parakeet", "batched", "longform"):
+        for regime in ("literal", "calibrated"):
+            c = make_workload(name, regime, layers=1).blocks[0].consts
+            for w in ("q", "k", "v", "pos", "out"):
+                assert c["mult_" + w].min() >= 0 and c["mult_" + w].max() < (1 << 23)
+            q_ln2, q_b, q_c = c["q_ln2"], c["q_b"], c["q_c"]
+            poly_max = max(q_b * q_b, (q_b - q_ln2 + 1) ** 2) + q_c
+            assert q_ln2 >= 1 and 256 <= q_b * q_b + q_c and poly_max < (1 << 24)
+            assert 8192 * poly_max < (1 << 32)
