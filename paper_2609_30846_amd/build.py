@@ -23,6 +23,9 @@ FLAGS = [
     "-Wall",
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the attention core post-processes every
+    # score tile with VALU code, which would otherwise copy them out of AGPRs
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

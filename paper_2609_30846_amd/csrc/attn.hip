@@ -1,27 +1,36 @@
 // Relative-position attention core of the integer MHSA block (Sec. 3.1).
 //
-// One 256-thread workgroup owns (utterance b, head h, a block of 16*NRT query
-// rows).  Each wave owns one 16-row tile and a contiguous range of 64-key chunks
-// (4/NRT waves split the keys of a tile).  Per 16x16 score tile:
+// Work split: a 256-thread workgroup owns (utterance b, head h, WGQ consecutive
+// queries).  Each wave owns 32 queries (two 16-query MFMA tiles, so every K, P
+// and V fragment it loads feeds two MFMAs) and a contiguous range of 64-key
+// chunks; KSPLIT waves share one set of 32 queries and split its keys.
 //
-//  * content score   c = Q K^T + (u.K_j)    -- v_mfma_i32_16x16x64_i8; the rank-1
-//                                              term seeds the accumulator
-//  * position score  G = Q P_win^T + (v.P_r) for the two 16-row windows of the
-//                    table that the tile's relative positions j-i+T-1 touch;
-//                    Phi is then a per-row rotation inside each 16-lane row
-//                    group: every source lane picks the window its value belongs
-//                    to and ds_bpermute moves it to the lane of its key
-//  * fused requant   s = clamp8(RS(m_c c + m_p p, 1, shift_s))  (Eq. 11), exact
-//                    in 64-bit
-//  * masked keys (j >= L_b) are stored as -128, a code below every valid score
-//
-// The int8 scores of the workgroup's rows stay in LDS (never in HBM).  Then:
-// row max (wave shuffles + LDS across the waves of a tile), I-BERT integer exp
-// and row sum, F = floor(2^32 / sum), and a = min(floor(e F / 2^24), 255).
-// The A.V contraction runs on v_mfma_i32_16x16x64_i8 with a - 128 as the signed
-// operand; the exact correction 128 * sum_j V_j over the same keys comes from
-// per-chunk prefix sums of V.  Partial contexts of the waves sharing a tile are
-// added in LDS (int32, exact) and requantized with (m_o, shift_o).
+// Phase 1, per 16-key step, with v_mfma_i32_16x16x64_i8 (queries on MFMA rows):
+//  * content   c = Q K^T, accumulator seeded with the rank-1 term u.K_j
+//  * position  G = Q P_win^T, seeded with v.P_r, for the 16 table rows that
+//              start at relative position j0-i0+T-1 ("hi" window).  The rows
+//              just before it ("lo") are the previous step's hi window, and the
+//              second query tile reuses the first tile's previous P fragment,
+//              so each step loads one new P fragment and runs one new position
+//              MFMA pair per tile.
+//  * Phi       p_ij = G_i(j-i+T-1) is a rotation by the row index inside each
+//              16-lane row group: every source lane picks the window its value
+//              belongs to and ds_bpermute moves it to the lane of its key.
+//  * Eq. 11    s = clamp8(RS(m_c c + m_p p, 1, n)), exact: in 32-bit
+//              integers when the descriptor bounds |m_c c + m_p p| below 2^31,
+//              otherwise in float64 (every intermediate is an integer below 2^53).
+//              Scores are kept as biased codes s + 128 in [1, 255].
+//  * the four scores a lane holds (four queries, one key) are packed into a
+//    dword and transposed inside each lane quad with DPP, so every lane stores
+//    four keys of one query with one ds_write_b32: the int8 score rows of the
+//    workgroup stay in LDS, never in HBM.
+// Phase 2: row max (shuffles + LDS across the KSPLIT waves), I-BERT integer exp
+// from a 255-entry table, row sums, F = floor(2^32 / sum).
+// Phase 3: per-row tables of the softmax code a = min(floor(e F / 2^24), 255),
+// stored as a - 128; A.V on MFMA with that signed operand plus the exact
+// correction 128 * sum_j V_j over the same keys (per-chunk sums of V); partial
+// contexts of the KSPLIT waves are added in LDS (exact int32) and requantized
+// with (m_o, shift_o).
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -33,263 +42,566 @@ struct AttnArgs {
   const int32_t *bu, *bv, *vsum;
   int8_t* ctx;
   Lengths lens;
-  int T, T_al, H, d, p_rows;
-  int32_t m_c, m_p, shift_s, m_o, shift_o, q_ln2, q_b, q_c;
+  int T, T_al, H, d, p_rows, p_base;
+  int nqb;        // query blocks per (utterance, head)
+  int xcd_group;  // keep each (utterance, head) on one XCD
+  // fused score: narrow path
+  int32_t mc24, mp24, bias32, post_shift;
+  // fused score: wide path (multipliers scaled by 2^-shift_s)
+  double mcd, mpd;
+  int32_t m_o, shift_o, q_ln2, q_b, q_c;
 };
 
 constexpr int SCORE_PAD = 16;  // bytes added to each LDS score row
+constexpr int ATAB_STRIDE = 260;  // bytes per softmax-code table row (bank spread)
 
 __device__ __forceinline__ uint32_t iexp_int(int d, int q_ln2, int q_b, int q_c) {
-  // I-BERT integer exp of -d: d = z q_ln2 - r, r in (-q_ln2, 0]
+  // I-BERT integer exp of -d: d = z q_ln2 - r with r in (-q_ln2, 0]
   const int z = d / q_ln2;
   const int r = z * q_ln2 - d;
   const int poly = (r + q_b) * (r + q_b) + q_c;  // < 2^24 (checked at create)
   return z >= 32 ? 0u : ((uint32_t)poly >> z);
 }
 
-template <int DK, int NRT>
-__global__ __launch_bounds__(256) void relpos_attn_core(AttnArgs a) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int WPT = 4 / NRT;   // waves per 16-row tile
-  constexpr int NKS = DK / 64;   // MFMA K-steps over d_k
-  constexpr int NT = DK / 16;    // 16-wide output tiles of the context
+// 4x4 byte transpose inside each lane quad: lane p of a quad holds bytes
+// m(0..3, p) and ends with m(p, 0..3).
+__device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t x, uint32_t sel1, uint32_t sel2) {
+  const uint32_t o1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  const uint32_t z = __builtin_amdgcn_perm(o1, x, sel1);
+  const uint32_t o2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)z, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  return __builtin_amdgcn_perm(o2, z, sel2);
+}
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int rt = w % NRT, ks = w / NRT;
-  const int b = blockIdx.z, h = blockIdx.y;
-  const int i_base = blockIdx.x * 16 * NRT;
-  const int i0 = i_base + 16 * rt;
+// Low 32 bits of a * b + c for 24-bit signed a, b (v_mad_i32_i24); the addition
+// wraps modulo 2^32.
+__device__ __forceinline__ int mad_i24(int a, int b, int c) {
+  return (int)((uint32_t)__mul24(a, b) + (uint32_t)c);
+}
+
+constexpr int ATTN_WAVES = 8;  // waves per workgroup (two per SIMD)
+
+template <int DK, int KSPLIT, bool WIDE>
+__global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets of 32 per workgroup
+  constexpr int WGQ = 32 * NQS;              // queries per workgroup
+  constexpr int NKS = DK / 64;          // MFMA K-steps over d_k
+  constexpr int NT = DK / 16;           // 16-channel output tiles of the context
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in SGPRs
+  const int col = lane & 15, g = lane >> 4;
+  const int qset = w / KSPLIT, kpart = w % KSPLIT;
+  // Workgroups go round-robin to the 8 XCDs (id % 8); when the (utterance, head)
+  // pairs divide evenly, every workgroup of one pair is placed on the same XCD so that
+  // its K, P and V stay in that XCD's L2.
+  int qb, bhi;
+  {
+    const int lin = blockIdx.x;
+    if (a.xcd_group) {
+      const int x = lin & 7, k = lin >> 3, slot = k / a.nqb;
+      qb = k - slot * a.nqb;
+      bhi = x + 8 * slot;
+    } else {
+      qb = lin % a.nqb;
+      bhi = lin / a.nqb;
+    }
+  }
+  const int b = bhi / a.H, h = bhi - (bhi / a.H) * a.H;
+  const int wg_q0 = qb * WGQ;
+  const int q0 = wg_q0 + 32 * qset;  // first query of this wave
   const int L = a.lens.len[b];
   const int T = a.T, T_al = a.T_al;
   const int srow = T_al + SCORE_PAD;
-  const int sbuf_bytes = 16 * NRT * srow;
-  const int red_bytes = 4 * 16 * DK * 4;
-  int8_t* sbuf = (int8_t*)smem;
-  int32_t* red = (int32_t*)smem;  // reused after the scores are consumed
-  int32_t* smax = (int32_t*)(smem + (sbuf_bytes > red_bytes ? sbuf_bytes : red_bytes));
-  uint32_t* ssum = (uint32_t*)(smax + 64);
-
-  const int col = lane & 15, g = lane >> 4;
   const int nkc = (L + KCHUNK - 1) / KCHUNK;
-  const int c_begin = ks * nkc / WPT, c_end = (ks + 1) * nkc / WPT;
-  const bool active = i0 < L;
+  const int c_begin = kpart * nkc / KSPLIT, c_end = (kpart + 1) * nkc / KSPLIT;
+  const int c_full = min(c_end, L / KCHUNK);  // chunks below this hold only valid keys
+  const bool active = q0 < L;
+
+  // LDS carve-up (the host computes the same sizes)
+  const int s_bytes = WGQ * srow;
+  const int red_bytes = KSPLIT > 1 ? (KSPLIT / 2) * NQS * 32 * DK * 4 : 0;
+  const int big = s_bytes > red_bytes ? s_bytes : red_bytes;
+  uint8_t* sbuf = smem;
+  int32_t* red = (int32_t*)smem;  // reused once the scores are consumed
+  uint32_t* etab = (uint32_t*)(smem + big);
+  uint8_t* atab = smem + big + 1024;
+  int32_t* smax = (int32_t*)(atab + WGQ * ATAB_STRIDE + 12);
+  uint32_t* ssum = (uint32_t*)(smax + 32 * ATTN_WAVES);
+  uint32_t* sF = ssum + 32 * ATTN_WAVES;
+
   const size_t bh = (size_t)b * a.H + h;
   const int8_t* Qh = a.q + bh * T_al * DK;
   const int8_t* Kh = a.k + bh * T_al * DK;
   const int8_t* VTh = a.vt + bh * DK * T_al;
   const int8_t* Ph = a.p + (size_t)h * a.p_rows * DK;
   const int32_t* bu = a.bu + bh * T_al;
-  const int32_t* bv = a.bv + (size_t)h * a.p_rows;
-  const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK + 1) * DK;
-  int8_t* srows = sbuf + (size_t)(16 * rt) * srow;
+  const v4i* bv4 = (const v4i*)(a.bv + (size_t)h * a.p_rows * 4);
+  const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
+  uint8_t* my_rows = sbuf + (size_t)(32 * qset) * srow;
+  // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
+  const int frag_off = col * 64 + g * 16;
+
+  // I-BERT integer exp of every score distance d = M - s in [0, 254]
+  if (tid < 256) etab[tid] = tid < 255 ? iexp_int(tid, a.q_ln2, a.q_b, a.q_c) : 0u;
+
+  constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
+  constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
 
   // ---------------- phase 1: fused scores into LDS, running row max
-  int mx[4] = {-128, -128, -128, -128};
-  if (active) {
-    v4i qa[NKS];
+  int mx[2][4];
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) qa[s] = *(const v4i*)(Qh + (size_t)(i0 + col) * DK + s * 64 + g * 16);
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx[t][i] = LOCODE;
+
+  const int j_begin = c_begin * KCHUNK;
+  const int j_stop = min(c_end * KCHUNK, (L + 15) & ~15);  // steps wholly past L are skipped
+  const int j_full = max(j_begin, min(j_stop, L & ~15));   // steps below this are unmasked
+  if (active && j_begin < j_stop) {
+    const uint32_t frag = (uint32_t)frag_off;
+    v4i qf[2][NKS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) qf[t][s] = *(const v4i*)(Qh + (size_t)(q0 + 16 * t) * DK + frag + s * 1024);
     bool take_hi[4];
     int src_addr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int arow = 4 * g + i;
-      take_hi[i] = (col + arow) < 16;                           // as a source lane
-      src_addr[i] = (g * 16 + ((col - arow) & 15)) * 4;         // as a destination lane
+      take_hi[i] = (col + arow) < 16;                    // as a source lane
+      src_addr[i] = (g * 16 + ((col - arow) & 15)) * 4;  // as a destination lane
     }
-    const int64_t half = (int64_t)1 << (a.shift_s - 1);
-    for (int c = c_begin; c < c_end; ++c) {
-      for (int sub = 0; sub < 4; ++sub) {
-        const int j0 = c * KCHUNK + sub * 16;
-        const int bu_j = bu[j0 + col];
-        v4i cs = {bu_j, bu_j, bu_j, bu_j};
+    const int p = col & 3;
+    const uint32_t sel1 = (p & 1) ? 0x03070105u : 0x06020400u;
+    const uint32_t sel2 = (p & 2) ? 0x03020706u : 0x05040100u;
+    // after the transpose a lane stores query 4g+p of a tile, keys 4*(col/4) .. +3
+    uint8_t* sdst0 = my_rows + (size_t)(4 * g + p) * srow + (col >> 2) * 4;
+    uint8_t* sdst1 = sdst0 + (size_t)16 * srow;
+
+    // table row of (query q0, key j0) is j0 - q0 + T - 1; tile 1 sits 16 rows lower
+    const int8_t* kptr = Kh + (size_t)j_begin * DK;
+    const int8_t* pptr = Ph + (size_t)(a.p_base + j_begin - q0 + T - 1) * DK;
+    const int32_t* buptr = bu + j_begin;
+    const v4i* bvptr = bv4 + (a.p_base + j_begin - q0 + T - 1);
+
+    // ping-pong register sets: "A" is the current step, "B" the other one
+    v4i kA[NKS], kB[NKS], pA[NKS], pB[NKS], gA[2], gB[2], bvA, bvB;
+    int buA, buB;
+    // rows just below the first step: tile 0's lo window and tile 1's lo window
+    {
+      v4i pm2[NKS];
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) {
-          const v4i kf = *(const v4i*)(Kh + (size_t)(j0 + col) * DK + s * 64 + g * 16);
-          cs = __builtin_amdgcn_mfma_i32_16x16x64_i8(qa[s], kf, cs, 0, 0, 0);
-        }
-        // relative position of (row i0, key j0) is table row j0 - i0 + T - 1
-        const int rlo = P_PADLO + j0 - i0 + T - 1 - 16, rhi = rlo + 16;
-        const int bvl = bv[rlo + col], bvh = bv[rhi + col];
-        v4i glo = {bvl, bvl, bvl, bvl}, ghi = {bvh, bvh, bvh, bvh};
+      for (int s = 0; s < NKS; ++s) {
+        pB[s] = *(const v4i*)(pptr - 16 * DK + frag + s * 1024);
+        pm2[s] = *(const v4i*)(pptr - 32 * DK + frag + s * 1024);
+      }
+      bvB = bvptr[(int)col - 16];
+      const v4i bvm2 = bvptr[(int)col - 32];
+      gB[0] = bvB;
+      gB[1] = bvm2;
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) {
-          const v4i pl = *(const v4i*)(Ph + (size_t)(rlo + col) * DK + s * 64 + g * 16);
-          const v4i ph = *(const v4i*)(Ph + (size_t)(rhi + col) * DK + s * 64 + g * 16);
-          glo = __builtin_amdgcn_mfma_i32_16x16x64_i8(qa[s], pl, glo, 0, 0, 0);
-          ghi = __builtin_amdgcn_mfma_i32_16x16x64_i8(qa[s], ph, ghi, 0, 0, 0);
-        }
-        const int j = j0 + col;
+      for (int s = 0; s < NKS; ++s) {
+        gB[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], pB[s], gB[0], 0, 0, 0);
+        gB[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], pm2[s], gB[1], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
+      kA[s] = *(const v4i*)(kptr + frag + s * 1024);
+      pA[s] = *(const v4i*)(pptr + frag + s * 1024);
+    }
+    buA = buptr[col];
+    bvA = bvptr[col];
+
+    int j0 = j_begin;
+    // One 16-key step.  Inputs: kc (K rows j0..), pc (table rows of tile 0's hi
+    // window) with its bias tuple bvc, po / bvo (tile 1's hi window = tile 0's
+    // previous one) and gl (the lo windows).  Writes the hi windows to gh and fetches
+    // the next step's K, P and biases into kn, po, bvo, bun (the last step re-reads
+    // its own rows, in bounds).
+    auto step = [&](const bool masked, v4i* kc, v4i* pc, const v4i bvc, const int buc, v4i* po, v4i& bvo,
+                    v4i* gl, v4i* gh, v4i* kn, int& bun) {
+      const int adv = j0 + 16 < j_stop ? 16 : 0;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) kn[s] = *(const v4i*)(kptr + adv * DK + frag + s * 1024);
+      bun = buptr[adv + col];
+      v4i cs[2];
+      cs[0] = cs[1] = (v4i){0, 0, 0, 0};
+      gh[0] = bvc;
+      gh[1] = bvo;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        cs[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], kc[s], cs[0], 0, 0, 0);
+        cs[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], kc[s], cs[1], 0, 0, 0);
+        gh[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], pc[s], gh[0], 0, 0, 0);
+        gh[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], po[s], gh[1], 0, 0, 0);
+      }
+      // tile 1's window of the next step is this step's tile-0 window: po is free now
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) po[s] = *(const v4i*)(pptr + adv * DK + frag + s * 1024);
+      bvo = bvptr[adv + col];
+      // rank-1 content term u.K_j folded into the addend: m_c (c0 + u.K_j) + rounding + code bias
+      int k1 = 0;
+      double k1d = 0.0;
+      if (WIDE)
+        k1d = __builtin_fma(a.mcd, (double)buc, 128.5);
+      else
+        k1 = __mul24(a.mc24, buc) + a.bias32;
+      const bool key_ok = j0 + col < L;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        int code[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int sel = take_hi[i] ? ghi[i] : glo[i];
+          const int sel = take_hi[i] ? gh[t][i] : gl[t][i];
           const int pt = __builtin_amdgcn_ds_bpermute(src_addr[i], sel);
-          const int64_t t = (int64_t)a.m_c * cs[i] + (int64_t)a.m_p * pt + half;
-          const int64_t r = t >> a.shift_s;
-          int sv = r < -127 ? -127 : (r > 127 ? 127 : (int)r);
-          if (j >= L) sv = -128;
-          mx[i] = sv > mx[i] ? sv : mx[i];
-          srows[(4 * g + i) * srow + j] = (int8_t)sv;
+          int v;
+          if (WIDE) {
+            // truncation equals the floor here: every negative value clamps to code 1
+            v = (int)__builtin_fma(a.mcd, (double)cs[t][i], __builtin_fma(a.mpd, (double)pt, k1d));
+          } else {
+            int x = mad_i24(a.mp24, pt, k1);
+            asm volatile("" : "+v"(x));  // keep the two multiply-adds from being re-associated
+            v = mad_i24(a.mc24, cs[t][i], x);
+          }
+          v = min(max(v, LOCODE), HICODE);
+          if (masked && !key_ok) v = LOCODE;
+          mx[t][i] = max(mx[t][i], v);
+          code[i] = v;
         }
+        // four queries of one key -> one dword, then four keys of one query
+        uint32_t packed;
+        if (WIDE) {
+          packed = __builtin_amdgcn_perm((uint32_t)code[1], (uint32_t)code[0], 0x0c0c0400u) |
+                   __builtin_amdgcn_perm((uint32_t)code[3], (uint32_t)code[2], 0x04000c0cu);
+        } else {
+          packed = __builtin_amdgcn_perm((uint32_t)code[1], (uint32_t)code[0], 0x0c0c0602u) |
+                   __builtin_amdgcn_perm((uint32_t)code[3], (uint32_t)code[2], 0x06020c0cu);
+        }
+        *(uint32_t*)((t ? sdst1 : sdst0) + j0) = quad_transpose_bytes(packed, sel1, sel2);
       }
+      kptr += 16 * DK;
+      pptr += 16 * DK;
+      buptr += 16;
+      bvptr += 16;
+      j0 += 16;
+    };
+    // steps alternate register sets: A = (kA, pA, bvA) current with tile 1 on (pB, bvB)
+    while (j0 + 32 <= j_full) {
+      step(false, kA, pA, bvA, buA, pB, bvB, gB, gA, kB, buB);
+      step(false, kB, pB, bvB, buB, pA, bvA, gA, gB, kA, buA);
+    }
+    bool in_a = true;
+    while (j0 < j_stop) {
+      const bool m = j0 + 16 > j_full;
+      if (in_a)
+        step(m, kA, pA, bvA, buA, pB, bvB, gB, gA, kB, buB);
+      else
+        step(m, kB, pB, bvB, buB, pA, bvA, gA, gB, kA, buA);
+      in_a = !in_a;
     }
   }
   // row max over the 16 key lanes of each row group
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int v = mx[i];
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      const int u = __shfl_xor(v, o);
-      v = u > v ? u : v;
+    for (int i = 0; i < 4; ++i) {
+      int v = mx[t][i];
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) v = max(v, __shfl_xor(v, o));
+      mx[t][i] = v;
     }
-    mx[i] = v;
-  }
   if (col == 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) smax[w * 16 + 4 * g + i] = mx[i];
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) smax[w * 32 + 16 * t + 4 * g + i] = WIDE ? mx[t][i] : (mx[t][i] >> 16);
   }
   __syncthreads();
 
-  // from here on lane (g, col) works on row `col` of its tile and keys g*16.. of a chunk
-  int M = -128;
+  // phases 2 and 3: lane (g, col) works on query row `col` of each tile and keys
+  // g*16 .. g*16+15 of a chunk
+  int Mrow[2];
 #pragma unroll
-  for (int k2 = 0; k2 < WPT; ++k2) {
-    const int v = smax[(rt + NRT * k2) * 16 + col];
-    M = v > M ? v : M;
+  for (int t = 0; t < 2; ++t) {
+    int m = 1;
+#pragma unroll
+    for (int k2 = 0; k2 < KSPLIT; ++k2) m = max(m, smax[(qset * KSPLIT + k2) * 32 + 16 * t + col]);
+    Mrow[t] = m;
   }
+  const uint8_t* srd0 = my_rows + (size_t)col * srow + g * 16;
+  const uint8_t* srd1 = srd0 + (size_t)16 * srow;
 
   // ---------------- phase 2: row sums of the integer exp
-  uint32_t sum = 0;
+  uint32_t sum[2] = {0u, 0u};
   if (active) {
-    for (int c = c_begin; c < c_end; ++c) {
-      const v4i sv16 = *(const v4i*)(srows + col * srow + c * KCHUNK + g * 16);
+    for (int c = c_begin; c < c_full; ++c) {
 #pragma unroll
-      for (int wd = 0; wd < 4; ++wd)
+      for (int t = 0; t < 2; ++t) {
+        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+        const uint32_t* erow = etab + Mrow[t];
 #pragma unroll
-        for (int by = 0; by < 4; ++by) {
-          const int s = (int)(int8_t)((uint32_t)sv16[wd] >> (8 * by));
-          if (s != -128) sum += iexp_int(M - s, a.q_ln2, a.q_b, a.q_c);
+        for (int wd = 0; wd < 4; ++wd) {
+          const uint32_t x = (uint32_t)sv[wd];
+          const uint32_t e0 = erow[-(int)(x & 0xff)], e1 = erow[-(int)((x >> 8) & 0xff)];
+          const uint32_t e2 = erow[-(int)((x >> 16) & 0xff)], e3 = erow[-(int)(x >> 24)];
+          sum[t] += e0 + e1 + e2 + e3;
         }
+      }
+    }
+    if (c_full < c_end) {  // the chunk that holds the utterance's last key
+      const int c = c_full;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+#pragma unroll
+        for (int by = 0; by < 16; ++by) {
+          const bool ok = c * KCHUNK + g * 16 + by < L;
+          const int code = ok ? (int)(((uint32_t)sv[by >> 2] >> (8 * (by & 3))) & 0xff) : Mrow[t];
+          const uint32_t e = etab[Mrow[t] - code];
+          sum[t] += ok ? e : 0u;
+        }
+      }
     }
   }
-  sum += __shfl_xor(sum, 16);
-  sum += __shfl_xor(sum, 32);
-  if (g == 0) ssum[w * 16 + col] = sum;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    sum[t] += __shfl_xor(sum[t], 16);
+    sum[t] += __shfl_xor(sum[t], 32);
+  }
+  if (g == 0) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) ssum[w * 32 + 16 * t + col] = sum[t];
+  }
   __syncthreads();
-  uint32_t tot = 0;
+  if (kpart == 0 && g == 0) {
 #pragma unroll
-  for (int k2 = 0; k2 < WPT; ++k2) tot += ssum[(rt + NRT * k2) * 16 + col];
-  const uint64_t F = tot ? ((uint64_t)1 << 32) / tot : 0;
+    for (int t = 0; t < 2; ++t) {
+      uint32_t tot = 0;
+#pragma unroll
+      for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qset * KSPLIT + k2) * 32 + 16 * t + col];
+      sF[32 * qset + 16 * t + col] = tot ? (uint32_t)(((uint64_t)1 << 32) / tot) : 0u;
+    }
+  }
+  __syncthreads();
+  // softmax code tables: atab[row][d] = (min(floor(e(d) F_row / 2^24), 255)) ^ 0x80
+  {
+    const int dd = tid & 255;
+    const uint32_t e = etab[dd];
+    for (int r = tid >> 8; r < WGQ; r += ATTN_WAVES / 4) {
+      const uint64_t v = ((uint64_t)e * sF[r]) >> 24;
+      const uint32_t av = v > 255 ? 255u : (uint32_t)v;
+      atab[r * ATAB_STRIDE + dd] = (uint8_t)(av ^ 0x80u);
+    }
+  }
+  __syncthreads();
 
-  // ---------------- phase 3: a = softmax codes, A.V on MFMA
-  v4i acc[NT];
+  // ---------------- phase 3: A.V on MFMA
+  v4i acc[2][NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) acc[nt] = (v4i){0, 0, 0, 0};
-  if (active) {
-    for (int c = c_begin; c < c_end; ++c) {
-      const v4i sv16 = *(const v4i*)(srows + col * srow + c * KCHUNK + g * 16);
-      v4i af;
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int wd = 0; wd < 4; ++wd) {
-        uint32_t packed = 0;
+    for (int nt = 0; nt < NT; ++nt) acc[t][nt] = (v4i){0, 0, 0, 0};
+  if (active && c_begin < c_end) {
+    const uint8_t* arow0 = atab + (32 * qset + col) * ATAB_STRIDE + Mrow[0];
+    const uint8_t* arow1 = atab + (32 * qset + 16 + col) * ATAB_STRIDE + Mrow[1];
+    const int vt_off = col * 64 + g * 16;       // lane's bytes of a 16-channel x 64-key block
+    constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
+    const int8_t* vptr = VTh + (size_t)c_begin * CH;
+    // softmax codes (as a - 128) of one chunk of keys for both query tiles
+    auto codes_full = [&](int c, v4i* af) {
 #pragma unroll
-        for (int by = 0; by < 4; ++by) {
-          const int s = (int)(int8_t)((uint32_t)sv16[wd] >> (8 * by));
-          uint32_t av = 0;
-          if (s != -128) {
-            const uint64_t e = iexp_int(M - s, a.q_ln2, a.q_b, a.q_c);
-            const uint64_t v = (e * F) >> 24;
-            av = v > 255 ? 255u : (uint32_t)v;
-          }
-          packed |= ((av ^ 0x80u) & 0xffu) << (8 * by);  // a - 128 as a signed byte
+      for (int t = 0; t < 2; ++t) {
+        const uint8_t* arow = t ? arow1 : arow0;
+        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          const uint32_t x = (uint32_t)sv[wd];
+          const uint32_t a0 = arow[-(int)(x & 0xff)], a1 = arow[-(int)((x >> 8) & 0xff)];
+          const uint32_t a2 = arow[-(int)((x >> 16) & 0xff)], a3 = arow[-(int)(x >> 24)];
+          af[t][wd] = (int)(a0 | (a1 << 8) | (a2 << 16) | (a3 << 24));
         }
-        af[wd] = (int)packed;
       }
+    };
+    auto codes_tail = [&](int c, v4i* af) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const uint8_t* arow = t ? arow1 : arow0;
+        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          uint32_t packed = 0;
+#pragma unroll
+          for (int by = 0; by < 4; ++by) {
+            const bool ok = c * KCHUNK + g * 16 + wd * 4 + by < L;
+            const int code = ok ? (int)(((uint32_t)sv[wd] >> (8 * by)) & 0xff) : Mrow[t];
+            const uint32_t av = arow[-code];
+            packed |= (ok ? av : 0x80u) << (8 * by);  // a = 0 for padded keys
+          }
+          af[t][wd] = (int)packed;
+        }
+      }
+    };
+    auto load_v = [&](const int8_t* src, v4i* dst) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) dst[nt] = *(const v4i*)(src + nt * 1024 + vt_off);
+    };
+    auto mma = [&](const v4i* af, const v4i* vf) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const v4i vf = *(const v4i*)(VTh + (size_t)(nt * 16 + col) * T_al + c * KCHUNK + g * 16);
-        acc[nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, vf, acc[nt], 0, 0, 0);
+        acc[0][nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0], vf[nt], acc[0][nt], 0, 0, 0);
+        acc[1][nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1], vf[nt], acc[1][nt], 0, 0, 0);
+      }
+    };
+    v4i vb0[NT], vb1[NT];
+    load_v(vptr, vb0);
+    int c = c_begin;
+    // two chunks per iteration with ping-pong V buffers; the next chunk is fetched ahead
+    for (; c + 2 <= c_full; c += 2) {
+      v4i af[2];
+      load_v(vptr + CH, vb1);
+      codes_full(c, af);
+      mma(af, vb0);
+      const int adv = c + 2 < c_end ? 2 * CH : CH;
+      load_v(vptr + adv, vb0);
+      codes_full(c + 1, af);
+      mma(af, vb1);
+      vptr += 2 * CH;
+    }
+    for (; c < c_end; ++c) {
+      v4i af[2];
+      if (c < c_full)
+        codes_full(c, af);
+      else
+        codes_tail(c, af);
+      mma(af, vb0);
+      if (c + 1 < c_end) {
+        vptr += CH;
+        load_v(vptr, vb0);
       }
     }
+    // exact correction for the -128 offset: + 128 * sum of V over the same keys
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int n = nt * 16 + col;
-      const int corr = 128 * (vs[(size_t)c_end * DK + n] - vs[(size_t)c_begin * DK + n]);
+      int vsum = 0;
+      for (int c = c_begin; c < c_end; ++c) vsum += vs[(size_t)c * DK + n];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[nt][i] += corr;
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[t][nt][i] += 128 * vsum;
     }
   }
-  __syncthreads();  // all waves are done with the scores; reuse LDS for the partials
-  // lane holds context channel n = nt*16 + col of rows 4g + i
+
+  // ---------------- combine the key splits, requantize, store
+  if (KSPLIT > 1) {
+    // tree over the key splits: in each round the upper half writes, the lower half adds
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
+    for (int cnt = KSPLIT; cnt > 1; cnt >>= 1) {
+      const int half = cnt >> 1;
+      __syncthreads();  // the scores (first round) or the previous partials are consumed
+      if (kpart >= half && kpart < cnt) {
+        int32_t* dst = red + (size_t)((kpart - half) * NQS + qset) * 32 * DK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) red[(w * 16 + 4 * g + i) * DK + nt * 16 + col] = acc[nt][i];
-  __syncthreads();
-  const int half_o = 1 << (a.shift_o - 1);
-  for (int idx = threadIdx.x; idx < 16 * NRT * DK; idx += 256) {
-    const int row = idx / DK, n = idx - row * DK;
-    const int rt2 = row >> 4, ar = row & 15;
-    const int i = i_base + row;
-    if (i >= T) continue;
-    int v = 0;
-    if (i < L) {
-      int tot2 = 0;
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int k2 = 0; k2 < WPT; ++k2) tot2 += red[((rt2 + NRT * k2) * 16 + ar) * DK + n];
-      const int64_t r = ((int64_t)tot2 * a.m_o + half_o) >> a.shift_o;
-      v = r < -127 ? -127 : (r > 127 ? 127 : (int)r);
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dst[(16 * t + 4 * g + i) * DK + nt * 16 + col] = acc[t][nt][i];
+      }
+      __syncthreads();
+      if (kpart < half) {
+        const int32_t* src = red + (size_t)(kpart * NQS + qset) * 32 * DK;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[t][nt][i] += src[(16 * t + 4 * g + i) * DK + nt * 16 + col];
+      }
     }
-    a.ctx[((size_t)b * T + i) * a.d + (size_t)h * DK + n] = (int8_t)v;
+  }
+  if (kpart == 0) {
+    const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int qi = q0 + 16 * t + 4 * g + i;
+        if (qi >= T) continue;
+        int8_t* out = a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + col;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          int v = 0;
+          if (qi < L) {
+            const int64_t r = ((int64_t)acc[t][nt][i] * a.m_o + half_o) >> a.shift_o;
+            v = r < -127 ? -127 : (r > 127 ? 127 : (int)r);
+          }
+          out[nt * 16] = (int8_t)v;
+        }
+      }
   }
 }
 
 // ---------------------------------------------------------------------------
-// Rank-1 bias terms and prefix sums of V over 64-key chunks.
+// Rank-1 bias terms u.K_j and v.P_r, and sums of V over each 64-key chunk.
 struct BiasArgs {
   const int8_t *k, *vt, *p, *u, *v;
   int32_t *bu, *bv, *vsum;
   int BH, H, T_al, DK, p_rows;
 };
 
+// u . row for a row stored fragment-major: DK/64 slabs of 64 contiguous bytes, 1 KB apart
+__device__ __forceinline__ int dot_frag_row(const int8_t* u, const int8_t* row, int DK) {
+  int acc = 0;
+  for (int s = 0; s < DK / 64; ++s)
+    for (int i = 0; i < 64; i += 16) {
+      const v4i xa = *(const v4i*)(u + s * 64 + i), ya = *(const v4i*)(row + s * 1024 + i);
+#pragma unroll
+      for (int wd = 0; wd < 4; ++wd) acc = __builtin_amdgcn_sdot4(xa[wd], ya[wd], acc, false);
+    }
+  return acc;
+}
+
 __global__ __launch_bounds__(256) void bias_terms(BiasArgs a) {
   const long n_bu = (long)a.BH * a.T_al;
   const long n_bv = (long)a.H * a.p_rows;
-  const long n_vs = (long)a.BH * a.DK;
+  const long nch = a.T_al / KCHUNK;
+  const long n_vs = (long)a.BH * a.DK * nch;
   long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx < n_bu) {
     const long bh = idx / a.T_al;
+    const int t = (int)(idx - bh * a.T_al);
     const int h = (int)(bh % a.H);
-    const int8_t* kr = a.k + idx * a.DK;
-    const int8_t* ur = a.u + (size_t)h * a.DK;
-    int acc = 0;
-    for (int kk = 0; kk < a.DK; ++kk) acc += (int)ur[kk] * (int)kr[kk];
-    a.bu[idx] = acc;
+    a.bu[idx] = dot_frag_row(a.u + (size_t)h * a.DK, a.k + bh * a.T_al * a.DK + frag_index(t, 0, a.DK), a.DK);
     return;
   }
   idx -= n_bu;
   if (idx < n_bv) {
     const int h = (int)(idx / a.p_rows);
-    const int8_t* pr = a.p + idx * a.DK;
-    const int8_t* vr = a.v + (size_t)h * a.DK;
-    int acc = 0;
-    for (int kk = 0; kk < a.DK; ++kk) acc += (int)vr[kk] * (int)pr[kk];
-    a.bv[idx] = acc;
+    const int r = (int)(idx - (long)h * a.p_rows);
+    const int val = dot_frag_row(a.v + (size_t)h * a.DK, a.p + (size_t)h * a.p_rows * a.DK + frag_index(r, 0, a.DK), a.DK);
+    *(v4i*)(a.bv + idx * 4) = (v4i){val, val, val, val};
     return;
   }
   idx -= n_bv;
   if (idx < n_vs) {
-    const long bh = idx / a.DK;
-    const int n = (int)(idx % a.DK);
-    const int8_t* row = a.vt + idx * a.T_al;
-    int32_t* out = a.vsum + bh * (long)(a.T_al / KCHUNK + 1) * a.DK + n;
-    int run = 0;
-    out[0] = 0;
-    for (int c = 0; c < a.T_al / KCHUNK; ++c) {
-      for (int t = 0; t < KCHUNK; ++t) run += (int)row[c * KCHUNK + t];
-      out[(size_t)(c + 1) * a.DK] = run;
+    // thread per (bh, chunk, channel): channel fastest so stores coalesce
+    const long n = idx % a.DK;
+    const long c = (idx / a.DK) % nch;
+    const long bh = idx / (a.DK * nch);
+    const int8_t* row = a.vt + bh * a.T_al * a.DK + vt_index((int)c * KCHUNK, (int)n, a.DK);
+    const int ones = 0x01010101;
+    int acc = 0;
+#pragma unroll
+    for (int i = 0; i < KCHUNK; i += 16) {
+      const v4i x = *(const v4i*)(row + i);
+#pragma unroll
+      for (int wd = 0; wd < 4; ++wd) acc = __builtin_amdgcn_sdot4(x[wd], ones, acc, false);
     }
+    a.vsum[(bh * nch + c) * a.DK + n] = acc;
   }
 }
 
@@ -298,7 +610,7 @@ __global__ __launch_bounds__(256) void bias_terms(BiasArgs a) {
 struct GatherArgs {
   const int8_t* src;
   int8_t* dst;
-  int which, B, T, T_al, H, DK, d, p_rows;
+  int which, B, T, T_al, H, DK, d, p_rows, p_base;
 };
 
 __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
@@ -310,41 +622,64 @@ __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
   const int h = c / a.DK, kk = c % a.DK;
   int8_t v;
   if (a.which == 3) {
-    v = a.src[((size_t)h * a.p_rows + P_PADLO + m) * a.DK + kk];
+    v = a.src[(size_t)h * a.p_rows * a.DK + frag_index(a.p_base + (int)m, kk, a.DK)];
   } else if (a.which == 4) {
     v = a.src[idx];
   } else {
     const long b = m / a.T, t = m % a.T;
-    const size_t bh = (size_t)b * a.H + h;
-    if (a.which == 2)
-      v = a.src[(bh * a.DK + kk) * a.T_al + t];
-    else
-      v = a.src[(bh * a.T_al + t) * a.DK + kk];
+    const size_t base = ((size_t)b * a.H + h) * a.T_al * a.DK;
+    v = a.src[base + (a.which == 2 ? vt_index((int)t, kk, a.DK) : frag_index((int)t, kk, a.DK))];
   }
   a.dst[idx] = v;
 }
 
 // ---------------------------------------------------------------------------
-template <int DK, int NRT>
+size_t attn_lds_bytes(int DK, int ksplit, int T_al) {
+  const int wgq = 32 * ATTN_WAVES / ksplit;
+  const size_t s_bytes = (size_t)wgq * (T_al + SCORE_PAD);
+  const size_t red = ksplit > 1 ? (size_t)(ksplit / 2) * (ATTN_WAVES / ksplit) * 32 * DK * 4 : 0;
+  return (s_bytes > red ? s_bytes : red) + 1024 + (size_t)wgq * ATAB_STRIDE + 12 + 3 * 32 * ATTN_WAVES * 4;
+}
+
+// Key split per workgroup: the fewest splits whose workgroup fits in LDS and that
+// still gives every CU a workgroup; otherwise the largest split that fits (most
+// workgroups); 0 if none fits.
+int attn_key_split(int DK, int T_al, long bh_count, int T) {
+  const size_t budget = 160 * 1024;
+  int best = 0;
+  for (int ks = 1; ks <= ATTN_WAVES; ks <<= 1) {
+    if (attn_lds_bytes(DK, ks, T_al) > budget) continue;
+    const int wgq = 32 * ATTN_WAVES / ks;
+    const long wgs = bh_count * ((T + wgq - 1) / wgq);
+    if (wgs >= 256) return ks;
+    best = ks;
+  }
+  return best;
+}
+
+template <int DK, int KS, bool WIDE>
 static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int T_al, hipStream_t st) {
-  const int sbuf = 16 * NRT * (T_al + SCORE_PAD);
-  const int red = 4 * 16 * DK * 4;
-  const size_t shmem = (size_t)(sbuf > red ? sbuf : red) + 2 * 64 * 4;
-  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, NRT>,
+  const size_t shmem = attn_lds_bytes(DK, KS, T_al);
+  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS, WIDE>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
   if (e != hipSuccess) return e;
-  const int rows_per_wg = 16 * NRT;
-  dim3 grid((T + rows_per_wg - 1) / rows_per_wg, H, B);
-  hipLaunchKernelGGL((relpos_attn_core<DK, NRT>), grid, dim3(256), shmem, st, args);
+  const int wgq = 32 * ATTN_WAVES / KS;
+  AttnArgs a2 = args;
+  a2.nqb = (T + wgq - 1) / wgq;
+  a2.xcd_group = (B * H) % 8 == 0;
+  dim3 grid(a2.nqb * B * H);
+  hipLaunchKernelGGL((relpos_attn_core<DK, KS, WIDE>), grid, dim3(64 * ATTN_WAVES), shmem, st, a2);
   return hipGetLastError();
 }
 
-// Largest query block (16, 32 or 64 rows) whose scores fit the LDS budget.
-int attn_rows_per_block(int T_al) {
-  const int budget = 160 * 1024 - 1024;
-  for (int nrt = 4; nrt >= 1; nrt >>= 1)
-    if (16 * nrt * (T_al + SCORE_PAD) <= budget) return 16 * nrt;
-  return 0;
+template <int DK, bool WIDE>
+static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st) {
+  const int ks = attn_key_split(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
+  if (ks == 1) return launch_attn_cfg<DK, 1, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
+  if (ks == 2) return launch_attn_cfg<DK, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
+  if (ks == 4) return launch_attn_cfg<DK, 4, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
+  if (ks == 8) return launch_attn_cfg<DK, 8, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
@@ -364,24 +699,20 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
   a.H = rs.H;
   a.d = rs.d;
   a.p_rows = p_rows(rs.T_al);
-  a.m_c = sc.m_c;
-  a.m_p = sc.m_p;
-  a.shift_s = sc.shift_s;
+  a.p_base = rs.p_base;
+  a.mc24 = sc.fs_mc24;
+  a.mp24 = sc.fs_mp24;
+  a.bias32 = sc.fs_bias32;
+  a.post_shift = sc.fs_post_shift;
+  a.mcd = sc.fs_mcd;
+  a.mpd = sc.fs_mpd;
   a.m_o = sc.m_o;
   a.shift_o = sc.shift_o;
   a.q_ln2 = sc.q_ln2;
   a.q_b = sc.q_b;
   a.q_c = sc.q_c;
-  const int rows = attn_rows_per_block(rs.T_al);
-  if (rs.DK == 128) {
-    if (rows == 64) return launch_attn_cfg<128, 4>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-    if (rows == 32) return launch_attn_cfg<128, 2>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-    if (rows == 16) return launch_attn_cfg<128, 1>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-  } else if (rs.DK == 64) {
-    if (rows == 64) return launch_attn_cfg<64, 4>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-    if (rows == 32) return launch_attn_cfg<64, 2>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-    if (rows == 16) return launch_attn_cfg<64, 1>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-  }
+  if (rs.DK == 128) return sc.fs_wide ? launch_attn_dk<128, true>(a, rs, st) : launch_attn_dk<128, false>(a, rs, st);
+  if (rs.DK == 64) return sc.fs_wide ? launch_attn_dk<64, true>(a, rs, st) : launch_attn_dk<64, false>(a, rs, st);
   return hipErrorInvalidValue;
 }
 
@@ -402,7 +733,7 @@ hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspa
   a.T_al = rs.T_al;
   a.DK = rs.DK;
   a.p_rows = p_rows(rs.T_al);
-  const long total = (long)a.BH * a.T_al + (long)a.H * a.p_rows + (long)a.BH * a.DK;
+  const long total = (long)a.BH * a.T_al + (long)a.H * a.p_rows + (long)a.BH * a.DK * (a.T_al / KCHUNK);
   hipLaunchKernelGGL(bias_terms, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a);
   return hipGetLastError();
 }
@@ -420,6 +751,7 @@ hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, i
   a.DK = rs.DK;
   a.d = rs.d;
   a.p_rows = p_rows(rs.T_al);
+  a.p_base = rs.p_base;
   const long rows = which == 3 ? (long)(2 * rs.T - 1) : (long)rs.B * rs.T;
   const long total = rows * rs.d;
   hipLaunchKernelGGL(gather_intermediate, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a);

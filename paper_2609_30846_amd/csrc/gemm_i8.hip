@@ -38,7 +38,7 @@ struct GemmArgs {
   GemmProblem prob[2];
   int nprob;
   int8_t *q, *k, *vt, *p, *y;
-  int T, T_al, H, DK, d, p_rows;
+  int T, T_al, H, DK, d, p_rows, p_base;
 };
 
 constexpr int BK = 64;
@@ -154,15 +154,17 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
           const int b = m / args.T, t = m - b * args.T;
           const size_t bh = (size_t)b * args.H + h;
           if (which < 2) {
-            int8_t* base = which == 0 ? args.q : args.k;
-            *(uint32_t*)(base + (bh * args.T_al + t) * args.DK + kk) = packed;
+            int8_t* base = (which == 0 ? args.q : args.k) + bh * args.T_al * args.DK;
+            *(uint32_t*)(base + frag_index(t, kk, args.DK)) = packed;
           } else {
+            int8_t* base = args.vt + bh * args.T_al * args.DK;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) args.vt[(bh * args.DK + kk + e) * args.T_al + t] = (int8_t)qv[e];
+            for (int e = 0; e < 4; ++e) base[vt_index(t, kk + e, args.DK)] = (int8_t)qv[e];
           }
         } else if (P.mode == OUT_POS) {
           const int h = n / args.DK, kk = n - h * args.DK;
-          *(uint32_t*)(args.p + ((size_t)h * args.p_rows + P_PADLO + m) * args.DK + kk) = packed;
+          int8_t* base = args.p + (size_t)h * args.p_rows * args.DK;
+          *(uint32_t*)(base + frag_index(args.p_base + m, kk, args.DK)) = packed;
         } else {
           *(uint32_t*)(args.y + (size_t)m * P.N + n) = packed;
         }
@@ -199,6 +201,7 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.DK = rs.DK;
   a.d = rs.d;
   a.p_rows = p_rows(rs.T_al);
+  a.p_base = rs.p_base;
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,

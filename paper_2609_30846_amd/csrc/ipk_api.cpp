@@ -3,7 +3,9 @@
 //   projections (Q|K|V and the position table) -> rank-1 bias terms and V prefix
 //   sums -> attention core -> output projection.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdarg.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
@@ -13,10 +15,6 @@
 
 #include "../../include/ipk.h"
 #include "ipk_internal.h"
-
-namespace ipk {
-int attn_rows_per_block(int T_al);
-}
 
 using namespace ipk;
 
@@ -85,6 +83,34 @@ static int validate_desc(const ipk_relpos_attn_desc* d) {
   return IPK_OK;
 }
 
+// Chooses how the attention core evaluates Eq. 11.  |c|, |p| <= d_k * 254 * 127
+// (int8 keys/positions times the 9-bit q + u, q + v); the 32-bit path is used when
+// m_c |c| + m_p |p| plus the rounding and code bias stays below 2^31 for every
+// possible score, so its wrap-around arithmetic is exact.
+static void plan_fused_score(Scalars* sc, int d_k) {
+  const int64_t cmax = (int64_t)d_k * 254 * 127;
+  const int n = sc->shift_s;
+  // 32-bit path: scale the multipliers to a shift of 16 so that the biased code
+  // s + 128 = floor((m_c c + m_p p + 2^15 + 128 * 2^16) / 2^16) is byte 2 of the
+  // clamped sum; only possible for n <= 16
+  bool narrow = n <= 16;
+  int64_t mc = 0, mp = 0, bias = ((int64_t)1 << 15) + ((int64_t)128 << 16);
+  if (narrow) {
+    mc = (int64_t)sc->m_c << (16 - n);
+    mp = (int64_t)sc->m_p << (16 - n);
+    narrow = mc < (1 << 23) && mp < (1 << 23) && (mc + mp) * cmax + bias < ((int64_t)1 << 31);
+  }
+  const char* force = getenv("IPK_SCORE_PATH");  // testing aid: "wide" forces float64
+  if (force && strcmp(force, "wide") == 0) narrow = false;
+  sc->fs_wide = !narrow;
+  sc->fs_mc24 = narrow ? (int32_t)mc : 0;
+  sc->fs_mp24 = narrow ? (int32_t)mp : 0;
+  sc->fs_bias32 = (int32_t)bias;
+  sc->fs_post_shift = 0;
+  sc->fs_mcd = ldexp((double)sc->m_c, -n);
+  sc->fs_mpd = ldexp((double)sc->m_p, -n);
+}
+
 static void free_handle(ipk_relpos_attn* h) {
   if (!h) return;
   for (void* p : h->allocs) (void)hipFree(p);
@@ -107,7 +133,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   *out = nullptr;
   int st = validate_desc(desc);
   if (st != IPK_OK) return st;
-  if (attn_rows_per_block(t_aligned(desc->max_T)) == 0)
+  if (attn_key_split(desc->d_k, t_aligned(desc->max_T), 1, desc->max_T) == 0)
     return fail(IPK_ERR_UNSUPPORTED, "max_T=%d does not fit the on-chip score rows", desc->max_T);
 
   ipk_relpos_attn* h = new (std::nothrow) ipk_relpos_attn();
@@ -121,7 +147,16 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   h->DK = desc->d_k;
   h->max_B = desc->max_batch;
   h->max_T = desc->max_T;
-  h->sc = Scalars{desc->m_c, desc->m_p, desc->shift_s, desc->m_o, desc->shift_o, desc->q_ln2, desc->q_b, desc->q_c};
+  h->sc = Scalars{};
+  h->sc.m_c = desc->m_c;
+  h->sc.m_p = desc->m_p;
+  h->sc.shift_s = desc->shift_s;
+  h->sc.m_o = desc->m_o;
+  h->sc.shift_o = desc->shift_o;
+  h->sc.q_ln2 = desc->q_ln2;
+  h->sc.q_b = desc->q_b;
+  h->sc.q_c = desc->q_c;
+  plan_fused_score(&h->sc, desc->d_k);
   h->has_run = false;
   h->stages_pending = false;
 
@@ -148,8 +183,8 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->ws.p, H * PR * DK));
   chk(dev_alloc(h, &h->ws.ctx, Bm * (size_t)h->max_T * d));
   chk(dev_alloc(h, &h->ws.bu, Bm * H * T_al));
-  chk(dev_alloc(h, &h->ws.bv, H * PR));
-  chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK + 1) * DK));
+  chk(dev_alloc(h, &h->ws.bv, H * PR * 4));
+  chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK) * DK));
   if (e != hipSuccess) {
     free_handle(h);
     (void)hipGetLastError();
@@ -212,7 +247,7 @@ extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const 
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
     return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
-  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d};
+  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d, p_base_row(T)};
   hipStream_t st = (hipStream_t)stream;
   const bool rec = h->stages_pending;
   h->stages_pending = false;

@@ -1,17 +1,22 @@
 // Internal declarations of the ipk library (not part of the C ABI).
 //
 // Workspace layout in HBM for one run of (B, T), with T_al = T rounded up to the
-// 64-key chunk and H heads of width DK:
-//   q, k   int8  [B][H][T_al][DK]   head-major rows: one 128-byte (DK=128) line per token
-//   vt     int8  [B][H][DK][T_al]   V transposed, so the A.V contraction reads keys
-//                                   contiguously for each output channel
-//   p      int8  [H][P_ROWS][DK]    projected relative-position table; table row r
-//                                   is stored at row P_PADLO + r, and the rows around
-//                                   it keep the index map j-i+T-1 in bounds for every
-//                                   padded tile (their contents are never used)
+// 64-key chunk and H heads of width DK.  Every layout is chosen so that the
+// attention core's MFMA operand fragments (16 rows x 64 bytes) are contiguous 1 KB
+// blocks, which the L2 serves at about twice the rate of 16 scattered half lines.
+//   q, k   int8  [B][H] fragment-major rows: row t, channel kk sits at
+//                frag_index(t, kk) = (t/16)*16*DK + (kk/64)*1024 + (t%16)*64 + kk%64
+//   vt     int8  [B][H] V transposed, chunk-major: key t, channel kk sits at
+//                vt_index(t, kk) = (t/64)*64*DK + kk*64 + t%64
+//   p      int8  [H] fragment-major rows of the projected relative-position table;
+//                table row r is stored at row p_base + r, where p_base >= P_PADLO is
+//                chosen per run so that the table row j-i+T-1 of every 16-query by
+//                16-key tile starts a 16-row block.  The rows around the table keep
+//                every padded tile in bounds (their contents are never used).
 //   bu     int32 [B][H][T_al]       u . K_j  (rank-1 part of the content score)
-//   bv     int32 [H][P_ROWS]        v . P_r  (rank-1 part of the position score)
-//   vsum   int32 [B][H][T_al/64+1][DK] prefix sums of V over 64-key chunks
+//   bv     int32 [H][P_ROWS][4]     v . P_r  (rank-1 part of the position score), four
+//                                   copies per row: the tuple seeds an MFMA accumulator
+//   vsum   int32 [B][H][T_al/64][DK] sums of V over each 64-key chunk
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
@@ -27,6 +32,15 @@ constexpr int P_PADHI = 128;  // rows kept after the last table row
 inline int round_up(int v, int m) { return (v + m - 1) / m * m; }
 inline int t_aligned(int T) { return round_up(T, KCHUNK); }
 inline int p_rows(int T_al) { return P_PADLO + 2 * T_al + P_PADHI; }
+// Row of table row 0: the smallest value >= P_PADLO with (p_base + T - 1) % 16 == 0.
+inline int p_base_row(int T) { return P_PADLO + (16 - (T - 1) % 16) % 16; }
+
+__host__ __device__ inline size_t frag_index(int row, int kk, int DK) {
+  return (size_t)(row >> 4) * (16 * DK) + (size_t)(kk >> 6) * 1024 + (row & 15) * 64 + (kk & 63);
+}
+__host__ __device__ inline size_t vt_index(int t, int kk, int DK) {
+  return (size_t)(t >> 6) * (64 * DK) + (size_t)kk * 64 + (t & 63);
+}
 
 struct Workspace {
   int8_t *q, *k, *vt, *p, *ctx;
@@ -50,6 +64,13 @@ struct Scalars {
   int32_t m_c, m_p, shift_s;
   int32_t m_o, shift_o;
   int32_t q_ln2, q_b, q_c;
+  // Eq. 11 as evaluated by the attention core: either in 32-bit integers
+  // (t = mc24 c + mp24 p + bias32, then >> post_shift; exact when the bound on
+  // |t| proven at create holds) or, when that bound fails, in float64 with the
+  // multipliers pre-scaled by 2^-shift_s.
+  bool fs_wide;
+  int32_t fs_mc24, fs_mp24, fs_bias32, fs_post_shift;
+  double fs_mcd, fs_mpd;
 };
 
 // Per-utterance valid lengths, passed by value to the kernels that mask.
@@ -59,6 +80,7 @@ struct Lengths {
 
 struct RunShape {
   int B, T, T_al, H, DK, d;
+  int p_base;  // workspace row of relative-position table row 0
 };
 
 // Enqueue the kernels of one run; return the first HIP error.
@@ -70,6 +92,9 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
                             hipStream_t st);
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st);
+// Key split of the attention core for a run (0 when T_al does not fit LDS).
+int attn_key_split(int DK, int T_al, long bh_count, int T);
+
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st);
 

@@ -14,6 +14,18 @@ from workloads import make_workload
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(params=["auto", "wide"])
+def score_path(request, monkeypatch):
+    """The attention core evaluates Eq. 11 in 32-bit integers when the descriptor
+    bounds the fused score below 2^31 ("auto" picks it for the calibrated regime)
+    and in float64 otherwise; "wide" forces the float64 path at create time."""
+    if request.param == "wide":
+        monkeypatch.setenv("IPK_SCORE_PATH", "wide")
+    else:
+        monkeypatch.delenv("IPK_SCORE_PATH", raising=False)
+    return request.param
+
+
 def _run_gpu(ipk, blk, x=None, lengths=None, inter=False, module=None):
     import torch
 
@@ -54,7 +66,7 @@ def _check_block(ipk, blk, label):
 
 @pytest.mark.parametrize("regime", ["literal", "calibrated"])
 @pytest.mark.parametrize("name", ["tiny", "parakeet"])
-def test_small_configs(gpu_lib, name, regime):
+def test_small_configs(gpu_lib, name, regime, score_path):
     blk = make_workload(name, regime).blocks[0]
     _check_block(gpu_lib, blk, f"{name}/{regime}")
 
@@ -75,7 +87,7 @@ SHAPES = [
 
 @pytest.mark.parametrize("regime", ["literal", "calibrated"])
 @pytest.mark.parametrize("T,d,H,B,lengths", SHAPES)
-def test_ragged_shapes(gpu_lib, T, d, H, B, lengths, regime):
+def test_ragged_shapes(gpu_lib, T, d, H, B, lengths, regime, score_path):
     import dataclasses
 
     from workloads import generate
@@ -87,13 +99,13 @@ def test_ragged_shapes(gpu_lib, T, d, H, B, lengths, regime):
 
 
 @pytest.mark.parametrize("regime", ["literal", "calibrated"])
-def test_batched_masked(gpu_lib, regime):
+def test_batched_masked(gpu_lib, regime, score_path):
     blk = make_workload("batched", regime).blocks[0]
     _check_block(gpu_lib, blk, f"batched/{regime}")
 
 
 @pytest.mark.parametrize("regime", ["literal", "calibrated"])
-def test_longform(gpu_lib, regime):
+def test_longform(gpu_lib, regime, score_path):
     blk = make_workload("longform", regime).blocks[0]
     print(f"[parity] longform/{regime}", flush=True)
     g = _run_gpu(gpu_lib, blk)
