@@ -171,12 +171,9 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->w.w_out, d * d));
   chk(dev_alloc(h, &h->w.u, H * DK));
   chk(dev_alloc(h, &h->w.v, H * DK));
-  chk(dev_alloc(h, &h->w.mult_qkv, 3 * d));
-  chk(dev_alloc(h, &h->w.shift_qkv, 3 * d));
-  chk(dev_alloc(h, &h->w.mult_pos, d));
-  chk(dev_alloc(h, &h->w.shift_pos, d));
-  chk(dev_alloc(h, &h->w.mult_out, d));
-  chk(dev_alloc(h, &h->w.shift_out, d));
+  chk(dev_alloc(h, &h->w.scale_qkv, 3 * d));
+  chk(dev_alloc(h, &h->w.scale_pos, d));
+  chk(dev_alloc(h, &h->w.scale_out, d));
   chk(dev_alloc(h, &h->ws.q, Bm * H * T_al * DK));
   chk(dev_alloc(h, &h->ws.k, Bm * H * T_al * DK));
   chk(dev_alloc(h, &h->ws.vt, Bm * H * DK * T_al));
@@ -199,21 +196,18 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(hipMemcpy(h->w.w_out, desc->w_out, d * d, hipMemcpyDefault));
   chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
   chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
-  std::vector<int32_t> mq(3 * d), sq(3 * d), sp(d, desc->shift_pos), so(d, desc->shift_out);
+  // Eq. 7 scales m * 2^-n: m < 2^23 and n <= 40, so each is an exact double
+  std::vector<double> sq(3 * d), sp(d), so(d);
   for (size_t c = 0; c < d; ++c) {
-    mq[c] = desc->mult_q[c];
-    mq[d + c] = desc->mult_k[c];
-    mq[2 * d + c] = desc->mult_v[c];
-    sq[c] = desc->shift_q;
-    sq[d + c] = desc->shift_k;
-    sq[2 * d + c] = desc->shift_v;
+    sq[c] = ldexp((double)desc->mult_q[c], -desc->shift_q);
+    sq[d + c] = ldexp((double)desc->mult_k[c], -desc->shift_k);
+    sq[2 * d + c] = ldexp((double)desc->mult_v[c], -desc->shift_v);
+    sp[c] = ldexp((double)desc->mult_pos[c], -desc->shift_pos);
+    so[c] = ldexp((double)desc->mult_out[c], -desc->shift_out);
   }
-  chk(hipMemcpy(h->w.mult_qkv, mq.data(), 3 * d * 4, hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.shift_qkv, sq.data(), 3 * d * 4, hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.mult_pos, desc->mult_pos, d * 4, hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.shift_pos, sp.data(), d * 4, hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.mult_out, desc->mult_out, d * 4, hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.shift_out, so.data(), d * 4, hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.scale_qkv, sq.data(), 3 * d * sizeof(double), hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.scale_pos, sp.data(), d * sizeof(double), hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->w.scale_out, so.data(), d * sizeof(double), hipMemcpyHostToDevice));
   // deterministic contents for the padding rows of the workspace
   chk(hipMemset(h->ws.p, 0, H * PR * DK));
   chk(hipMemset(h->ws.vt, 0, Bm * H * DK * T_al));

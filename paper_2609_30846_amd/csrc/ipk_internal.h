@@ -52,12 +52,10 @@ struct Weights {
   int8_t* w_pos;       // [d][d]
   int8_t* w_out;       // [d][d]
   int8_t *u, *v;       // [H][DK]
-  int32_t* mult_qkv;   // [3d]
-  int32_t* shift_qkv;  // [3d]
-  int32_t* mult_pos;   // [d]
-  int32_t* shift_pos;  // [d]
-  int32_t* mult_out;   // [d]
-  int32_t* shift_out;  // [d]
+  // per-output-channel requantization scales m * 2^-n (exact in float64)
+  double* scale_qkv;  // [3d]
+  double* scale_pos;  // [d]
+  double* scale_out;  // [d]
 };
 
 struct Scalars {
