@@ -1,9 +1,10 @@
 // Relative-position attention core of the integer MHSA block (Sec. 3.1).
 //
-// Work split: a 256-thread workgroup owns (utterance b, head h, WGQ consecutive
-// queries).  Each wave owns 32 queries (two 16-query MFMA tiles, so every K, P
-// and V fragment it loads feeds two MFMAs) and a contiguous range of 64-key
-// chunks; KSPLIT waves share one set of 32 queries and split its keys.
+// Work split: a workgroup of ATTN_WAVES waves owns (utterance b, head h, WGQ
+// consecutive queries).  Each wave owns 32 queries (two 16-query MFMA tiles, so
+// every K, P and V fragment it loads feeds two MFMAs); KSPLIT waves share one set
+// of 32 queries and split its keys: phase 1 in 16-key steps, phases 2 and 3 in
+// 64-key chunks (scores are exchanged through LDS in between).
 //
 // Phase 1, per 16-key step, with v_mfma_i32_16x16x64_i8 (queries on MFMA rows):
 //  * content   c = Q K^T, accumulator seeded with the rank-1 term u.K_j
@@ -25,12 +26,16 @@
 //    four keys of one query with one ds_write_b32: the int8 score rows of the
 //    workgroup stay in LDS, never in HBM.
 // Phase 2: row max (shuffles + LDS across the KSPLIT waves), I-BERT integer exp
-// from a 255-entry table, row sums, F = floor(2^32 / sum).
+// of every distance d = max - s from a table, row sums, F = floor(2^32 / sum).
 // Phase 3: per-row tables of the softmax code a = min(floor(e F / 2^24), 255),
 // stored as a - 128; A.V on MFMA with that signed operand plus the exact
-// correction 128 * sum_j V_j over the same keys (per-chunk sums of V); partial
-// contexts of the KSPLIT waves are added in LDS (exact int32) and requantized
-// with (m_o, shift_o).
+// correction 128 * sum_j V_j over the same keys (per-chunk sums of V, fetched
+// with the V fragments; V is streamed in parts of four 16-channel tiles); partial
+// contexts of the KSPLIT waves are added with LDS atomics (exact int32) and
+// requantized with (m_o, shift_o) by all waves together.
+// Both lookup tables are laid out [d][32] in dwords: the exp table holds one copy
+// per LDS bank (lane l reads copy l % 32), the code table holds row r in bank
+// r % 32, so a lookup is one multiply-add and one conflict-free ds_read_b32.
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -53,7 +58,7 @@ struct AttnArgs {
 };
 
 constexpr int SCORE_PAD = 16;  // bytes added to each LDS score row
-constexpr int ATAB_STRIDE = 260;  // bytes per softmax-code table row (bank spread)
+constexpr int TAB_BLOCK = 256 * 32;  // dwords of one [d][32] lookup table
 
 __device__ __forceinline__ uint32_t iexp_int(int d, int q_ln2, int q_b, int q_c) {
   // I-BERT integer exp of -d: d = z q_ln2 - r with r in (-q_ln2, 0]
@@ -119,14 +124,18 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   const bool active = q0 < L;
 
   // LDS carve-up (the host computes the same sizes)
+  constexpr int RSTRIDE = DK + 4;  // dwords per row of the key-split partial sums
   const int s_bytes = WGQ * srow;
-  const int red_bytes = KSPLIT > 1 ? (KSPLIT / 2) * NQS * 32 * DK * 4 : 0;
-  const int big = s_bytes > red_bytes ? s_bytes : red_bytes;
+  const int red_bytes = KSPLIT > 1 ? NQS * 32 * RSTRIDE * 4 : 0;
+  const int big = ((s_bytes > red_bytes ? s_bytes : red_bytes) + 15) & ~15;
   uint8_t* sbuf = smem;
   int32_t* red = (int32_t*)smem;  // reused once the scores are consumed
-  uint32_t* etab = (uint32_t*)(smem + big);
-  uint8_t* atab = smem + big + 1024;
-  int32_t* smax = (int32_t*)(atab + WGQ * ATAB_STRIDE + 12);
+  // lookup tables: first the per-bank copies of the exp table (phase 2), then the
+  // per-row code tables, 32 rows per block (phase 3)
+  uint32_t* tab = (uint32_t*)(smem + big);
+  constexpr int TAB_DW = (WGQ / 32) * TAB_BLOCK;
+  uint32_t* etab = tab + TAB_DW;  // the 255 exp values, once
+  int32_t* smax = (int32_t*)(etab + 256);
   uint32_t* ssum = (uint32_t*)(smax + 32 * ATTN_WAVES);
   uint32_t* sF = ssum + 32 * ATTN_WAVES;
 
@@ -142,8 +151,18 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
   const int frag_off = col * 64 + g * 16;
 
-  // I-BERT integer exp of every score distance d = M - s in [0, 254]
-  if (tid < 256) etab[tid] = tid < 255 ? iexp_int(tid, a.q_ln2, a.q_b, a.q_c) : 0u;
+  // I-BERT integer exp of every score distance d = M - s in [0, 254]: once, and
+  // in 32 per-bank copies (copy (d + c) % 32 of the pass is written by lane d,
+  // which keeps the writes free of bank conflicts)
+  {
+    const int dd = tid & 255;
+    const uint32_t e = dd < 255 ? iexp_int(dd, a.q_ln2, a.q_b, a.q_c) : 0u;
+    if (tid < 256) etab[dd] = e;
+    for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e;
+    }
+  }
 
   constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
@@ -155,9 +174,11 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
 #pragma unroll
     for (int i = 0; i < 4; ++i) mx[t][i] = LOCODE;
 
-  const int j_begin = c_begin * KCHUNK;
-  const int j_stop = min(c_end * KCHUNK, (L + 15) & ~15);  // steps wholly past L are skipped
-  const int j_full = max(j_begin, min(j_stop, L & ~15));   // steps below this are unmasked
+  // phase 1 splits the 16-key steps that hold a valid key evenly over the key splits
+  const int nst = (L + 15) >> 4;
+  const int j_begin = 16 * (kpart * nst / KSPLIT);
+  const int j_stop = 16 * ((kpart + 1) * nst / KSPLIT);
+  const int j_full = max(j_begin, min(j_stop, L & ~15));  // steps below this are unmasked
   if (active && j_begin < j_stop) {
     const uint32_t frag = (uint32_t)frag_off;
     v4i qf[2][NKS];
@@ -335,18 +356,23 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   const uint8_t* srd1 = srd0 + (size_t)16 * srow;
 
   // ---------------- phase 2: row sums of the integer exp
+  // lane l reads copy l % 32 of the exp table: e(M - code) at erow[-32 code]
   uint32_t sum[2] = {0u, 0u};
   if (active) {
+    const uint32_t* erow[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) erow[t] = tab + Mrow[t] * 32 + (lane & 31);
     for (int c = c_begin; c < c_full; ++c) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
-        const uint32_t* erow = etab + Mrow[t];
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
           const uint32_t x = (uint32_t)sv[wd];
-          const uint32_t e0 = erow[-(int)(x & 0xff)], e1 = erow[-(int)((x >> 8) & 0xff)];
-          const uint32_t e2 = erow[-(int)((x >> 16) & 0xff)], e3 = erow[-(int)(x >> 24)];
+          const uint32_t e0 = erow[t][__mul24(-32, (int)(x & 0xff))];
+          const uint32_t e1 = erow[t][__mul24(-32, (int)((x >> 8) & 0xff))];
+          const uint32_t e2 = erow[t][__mul24(-32, (int)((x >> 16) & 0xff))];
+          const uint32_t e3 = erow[t][__mul24(-32, (int)(x >> 24))];
           sum[t] += e0 + e1 + e2 + e3;
         }
       }
@@ -386,15 +412,14 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     }
   }
   __syncthreads();
-  // softmax code tables: atab[row][d] = (min(floor(e(d) F_row / 2^24), 255)) ^ 0x80
-  {
-    const int dd = tid & 255;
-    const uint32_t e = etab[dd];
-    for (int r = tid >> 8; r < WGQ; r += ATTN_WAVES / 4) {
-      const uint64_t v = ((uint64_t)e * sF[r]) >> 24;
-      const uint32_t av = v > 255 ? 255u : (uint32_t)v;
-      atab[r * ATAB_STRIDE + dd] = (uint8_t)(av ^ 0x80u);
-    }
+  // softmax code tables (over the exp copies, which phase 2 has finished with):
+  // row r, distance d at dword (r / 32) * TAB_BLOCK + d * 32 + r % 32 holds
+  // min(floor(e(d) F_r / 2^24), 255) ^ 0x80, i.e. the byte a - 128
+  for (int idx = tid; idx < TAB_DW; idx += 64 * ATTN_WAVES) {
+    const int blk = idx / TAB_BLOCK, rem = idx - blk * TAB_BLOCK;
+    const int dd = rem >> 5, r = blk * 32 + (rem & 31);
+    const uint64_t v = ((uint64_t)etab[dd] * sF[r]) >> 24;
+    tab[idx] = (v > 255 ? 255u : (uint32_t)v) ^ 0x80u;
   }
   __syncthreads();
 
@@ -405,22 +430,24 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[t][nt] = (v4i){0, 0, 0, 0};
   if (active && c_begin < c_end) {
-    const uint8_t* arow0 = atab + (32 * qset + col) * ATAB_STRIDE + Mrow[0];
-    const uint8_t* arow1 = atab + (32 * qset + 16 + col) * ATAB_STRIDE + Mrow[1];
+    // code of (row, M - code) at arow[-32 code]
+    const uint32_t* arow0 = tab + qset * TAB_BLOCK + Mrow[0] * 32 + col;
+    const uint32_t* arow1 = tab + qset * TAB_BLOCK + Mrow[1] * 32 + 16 + col;
     const int vt_off = col * 64 + g * 16;       // lane's bytes of a 16-channel x 64-key block
     constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
-    const int8_t* vptr = VTh + (size_t)c_begin * CH;
     // softmax codes (as a - 128) of one chunk of keys for both query tiles
     auto codes_full = [&](int c, v4i* af) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const uint8_t* arow = t ? arow1 : arow0;
+        const uint32_t* arow = t ? arow1 : arow0;
         const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
           const uint32_t x = (uint32_t)sv[wd];
-          const uint32_t a0 = arow[-(int)(x & 0xff)], a1 = arow[-(int)((x >> 8) & 0xff)];
-          const uint32_t a2 = arow[-(int)((x >> 16) & 0xff)], a3 = arow[-(int)(x >> 24)];
+          const uint32_t a0 = arow[__mul24(-32, (int)(x & 0xff))];
+          const uint32_t a1 = arow[__mul24(-32, (int)((x >> 8) & 0xff))];
+          const uint32_t a2 = arow[__mul24(-32, (int)((x >> 16) & 0xff))];
+          const uint32_t a3 = arow[__mul24(-32, (int)(x >> 24))];
           af[t][wd] = (int)(a0 | (a1 << 8) | (a2 << 16) | (a3 << 24));
         }
       }
@@ -428,7 +455,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     auto codes_tail = [&](int c, v4i* af) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const uint8_t* arow = t ? arow1 : arow0;
+        const uint32_t* arow = t ? arow1 : arow0;
         const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
@@ -437,94 +464,86 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
           for (int by = 0; by < 4; ++by) {
             const bool ok = c * KCHUNK + g * 16 + wd * 4 + by < L;
             const int code = ok ? (int)(((uint32_t)sv[wd] >> (8 * by)) & 0xff) : Mrow[t];
-            const uint32_t av = arow[-code];
+            const uint32_t av = arow[-32 * code];
             packed |= (ok ? av : 0x80u) << (8 * by);  // a = 0 for padded keys
           }
           af[t][wd] = (int)packed;
         }
       }
     };
-    auto load_v = [&](const int8_t* src, v4i* dst) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) dst[nt] = *(const v4i*)(src + nt * 1024 + vt_off);
+    // V^T operands in parts of NP = 4 channel tiles (a d_k = 128 chunk is two parts),
+    // each with this lane's V sums over the chunk for channels (h NP + k) * 16 + col
+    constexpr int NP = 4;
+    constexpr int NSPLIT = NT / NP;
+    struct VPart {
+      v4i v[NP];
+      v4i s;
     };
-    auto mma = [&](const v4i* af, const v4i* vf) {
+    auto load_part = [&](int c, int h, VPart& dst) {
+      const int8_t* src = VTh + (size_t)c * CH + h * NP * 1024 + vt_off;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        acc[0][nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0], vf[nt], acc[0][nt], 0, 0, 0);
-        acc[1][nt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1], vf[nt], acc[1][nt], 0, 0, 0);
+      for (int k = 0; k < NP; ++k) dst.v[k] = *(const v4i*)(src + k * 1024);
+      dst.s = *(const v4i*)(vs + ((size_t)c * 16 + col) * NT + h * NP);
+    };
+    int vacc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) vacc[nt] = 0;
+    v4i af[2];
+    auto mma_part = [&](const int h, const VPart& vp) {
+#pragma unroll
+      for (int k = 0; k < NP; ++k) {
+        acc[0][h * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0], vp.v[k], acc[0][h * NP + k], 0, 0, 0);
+        acc[1][h * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1], vp.v[k], acc[1][h * NP + k], 0, 0, 0);
+        vacc[h * NP + k] += vp.s[k];
       }
     };
-    v4i vb0[NT], vb1[NT];
-    load_v(vptr, vb0);
-    int c = c_begin;
-    // two chunks per iteration with ping-pong V buffers; the next chunk is fetched ahead
-    for (; c + 2 <= c_full; c += 2) {
-      v4i af[2];
-      load_v(vptr + CH, vb1);
-      codes_full(c, af);
-      mma(af, vb0);
-      const int adv = c + 2 < c_end ? 2 * CH : CH;
-      load_v(vptr + adv, vb0);
-      codes_full(c + 1, af);
-      mma(af, vb1);
-      vptr += 2 * CH;
-    }
-    for (; c < c_end; ++c) {
-      v4i af[2];
+    auto codes = [&](int c) {
       if (c < c_full)
         codes_full(c, af);
       else
         codes_tail(c, af);
-      mma(af, vb0);
-      if (c + 1 < c_end) {
-        vptr += CH;
-        load_v(vptr, vb0);
+    };
+    // the next part is always in flight; past the last chunk the loads re-read it
+    // (in bounds, unused), which keeps the loads unconditional
+    const int c_last = c_end - 1;
+    VPart pb0, pb1;
+    load_part(c_begin, 0, pb0);
+    if (NSPLIT == 2) {
+      for (int c = c_begin; c < c_end; ++c) {
+        load_part(c, 1, pb1);
+        codes(c);
+        mma_part(0, pb0);
+        load_part(min(c + 1, c_last), 0, pb0);
+        mma_part(1, pb1);
+      }
+    } else {
+      for (int c = c_begin; c < c_end;) {
+        load_part(min(c + 1, c_last), 0, pb1);
+        codes(c);
+        mma_part(0, pb0);
+        if (++c >= c_end) break;
+        load_part(min(c + 1, c_last), 0, pb0);
+        codes(c);
+        mma_part(0, pb1);
+        ++c;
       }
     }
     // exact correction for the -128 offset: + 128 * sum of V over the same keys
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = nt * 16 + col;
-      int vsum = 0;
-      for (int c = c_begin; c < c_end; ++c) vsum += vs[(size_t)c * DK + n];
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[t][nt][i] += 128 * vsum;
-    }
+        for (int i = 0; i < 4; ++i) acc[t][nt][i] += 128 * vacc[nt];
   }
 
   // ---------------- combine the key splits, requantize, store
-  if (KSPLIT > 1) {
-    // tree over the key splits: in each round the upper half writes, the lower half adds
-#pragma unroll
-    for (int cnt = KSPLIT; cnt > 1; cnt >>= 1) {
-      const int half = cnt >> 1;
-      __syncthreads();  // the scores (first round) or the previous partials are consumed
-      if (kpart >= half && kpart < cnt) {
-        int32_t* dst = red + (size_t)((kpart - half) * NQS + qset) * 32 * DK;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) dst[(16 * t + 4 * g + i) * DK + nt * 16 + col] = acc[t][nt][i];
-      }
-      __syncthreads();
-      if (kpart < half) {
-        const int32_t* src = red + (size_t)(kpart * NQS + qset) * 32 * DK;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[t][nt][i] += src[(16 * t + 4 * g + i) * DK + nt * 16 + col];
-      }
-    }
-  }
-  if (kpart == 0) {
-    const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
+  const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
+  auto requant_o = [&](int32_t v) -> int {
+    const int64_t r = ((int64_t)v * a.m_o + half_o) >> a.shift_o;
+    return r < -127 ? -127 : (r > 127 ? 127 : (int)r);
+  };
+  if (KSPLIT == 1) {
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -533,15 +552,47 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
         if (qi >= T) continue;
         int8_t* out = a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + col;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          int v = 0;
-          if (qi < L) {
-            const int64_t r = ((int64_t)acc[t][nt][i] * a.m_o + half_o) >> a.shift_o;
-            v = r < -127 ? -127 : (r > 127 ? 127 : (int)r);
-          }
-          out[nt * 16] = (int8_t)v;
-        }
+        for (int nt = 0; nt < NT; ++nt) out[nt * 16] = (int8_t)(qi < L ? requant_o(acc[t][nt][i]) : 0);
       }
+  } else {
+    // partial sums of one query set: [32 rows][RSTRIDE] int32; the padding puts
+    // rows 4 apart into different banks.  The first key split stores, the others
+    // add with LDS atomics (exact, order-free).
+    int32_t* rq = red + (size_t)qset * 32 * RSTRIDE;
+    __syncthreads();  // every wave is done with the score rows
+    if (kpart == 0) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) rq[(16 * t + 4 * g + i) * RSTRIDE + nt * 16 + col] = acc[t][nt][i];
+    }
+    __syncthreads();
+    if (kpart != 0 && active) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) atomicAdd(&rq[(16 * t + 4 * g + i) * RSTRIDE + nt * 16 + col], acc[t][nt][i]);
+    }
+    __syncthreads();
+    // the KSPLIT waves of the set share its 32 rows: items of 4 channels, row-major
+    constexpr int IPR = DK / 4;  // items per row
+    for (int it = kpart * 64 + lane; it < 32 * IPR; it += 64 * KSPLIT) {
+      const int rr = it / IPR;
+      const int ch = (it % IPR) * 4;
+      const int qi = q0 + rr;
+      if (qi >= T) continue;
+      const v4i v = *(const v4i*)(rq + rr * RSTRIDE + ch);
+      uint32_t packed = 0;
+      if (qi < L) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) packed |= ((uint32_t)requant_o(v[e]) & 0xffu) << (8 * e);
+      }
+      *(uint32_t*)(a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + ch) = packed;
+    }
   }
 }
 
@@ -601,7 +652,9 @@ __global__ __launch_bounds__(256) void bias_terms(BiasArgs a) {
 #pragma unroll
       for (int wd = 0; wd < 4; ++wd) acc = __builtin_amdgcn_sdot4(x[wd], ones, acc, false);
     }
-    a.vsum[(bh * nch + c) * a.DK + n] = acc;
+    // [bh][chunk][n % 16][n / 16]: a lane of the attention core reads its NT
+    // channels n % 16 + 16 k of one chunk with one or two 16-byte loads
+    a.vsum[((bh * nch + c) * 16 + n % 16) * (a.DK / 16) + n / 16] = acc;
   }
 }
 
@@ -637,9 +690,14 @@ __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
 size_t attn_lds_bytes(int DK, int ksplit, int T_al) {
   const int wgq = 32 * ATTN_WAVES / ksplit;
   const size_t s_bytes = (size_t)wgq * (T_al + SCORE_PAD);
-  const size_t red = ksplit > 1 ? (size_t)(ksplit / 2) * (ATTN_WAVES / ksplit) * 32 * DK * 4 : 0;
-  return (s_bytes > red ? s_bytes : red) + 1024 + (size_t)wgq * ATAB_STRIDE + 12 + 3 * 32 * ATTN_WAVES * 4;
+  const size_t red = ksplit > 1 ? (size_t)(ATTN_WAVES / ksplit) * 32 * (DK + 4) * 4 : 0;
+  const size_t big = ((s_bytes > red ? s_bytes : red) + 15) & ~(size_t)15;
+  return big + (size_t)(wgq / 32) * TAB_BLOCK * 4 + 256 * 4 + 3 * 32 * ATTN_WAVES * 4;
 }
+
+// Key splits the kernel is built for (divisors of ATTN_WAVES; smaller splits put
+// more query rows in LDS than fit).
+static const int kKeySplits[] = {4, 8};
 
 // Key split per workgroup: the fewest splits whose workgroup fits in LDS and that
 // still gives every CU a workgroup; otherwise the largest split that fits (most
@@ -647,7 +705,7 @@ size_t attn_lds_bytes(int DK, int ksplit, int T_al) {
 int attn_key_split(int DK, int T_al, long bh_count, int T) {
   const size_t budget = 160 * 1024;
   int best = 0;
-  for (int ks = 1; ks <= ATTN_WAVES; ks <<= 1) {
+  for (int ks : kKeySplits) {
     if (attn_lds_bytes(DK, ks, T_al) > budget) continue;
     const int wgq = 32 * ATTN_WAVES / ks;
     const long wgs = bh_count * ((T + wgq - 1) / wgq);
@@ -675,8 +733,6 @@ static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int
 template <int DK, bool WIDE>
 static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st) {
   const int ks = attn_key_split(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
-  if (ks == 1) return launch_attn_cfg<DK, 1, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-  if (ks == 2) return launch_attn_cfg<DK, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
   if (ks == 4) return launch_attn_cfg<DK, 4, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
   if (ks == 8) return launch_attn_cfg<DK, 8, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
   return hipErrorInvalidValue;

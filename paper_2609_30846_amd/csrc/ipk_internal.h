@@ -16,7 +16,8 @@
 //   bu     int32 [B][H][T_al]       u . K_j  (rank-1 part of the content score)
 //   bv     int32 [H][P_ROWS][4]     v . P_r  (rank-1 part of the position score), four
 //                                   copies per row: the tuple seeds an MFMA accumulator
-//   vsum   int32 [B][H][T_al/64][DK] sums of V over each 64-key chunk
+//   vsum   int32 [B][H][T_al/64][16][DK/16] sums of V over each 64-key chunk; channel n
+//                                   at [n % 16][n / 16]
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
