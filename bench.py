@@ -10,9 +10,10 @@ Inputs are resident in HBM before the timed region.
 Prints one JSON line.  ``value`` is algorithmic int8 tera-operations per second
 (2 x the multiply-accumulates the method needs: projections of the valid rows,
 the position projection once, and content + position + A.V over the valid
-(query, key) pairs).  ``roofline`` reports the attention core against the dense
-INT8 MFMA peak, its duration measured with HIP events on the launch stream over
-the timed region.  ``cpu_baseline`` is the CPU oracle on the same workload.
+(query, key) pairs), timed over K steps with no events inside the region.
+``roofline`` reports the attention core against the dense INT8 MFMA peak, its
+average duration measured with per-kernel HIP events on the launch stream over a
+second pass of K steps.  ``cpu_baseline`` is the CPU oracle on the same workload.
 """
 
 from __future__ import annotations
@@ -46,6 +47,35 @@ def algorithmic_macs(B, T, d, H, dk, lengths):
     return proj, pos, attn
 
 
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources the library is built from."""
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_30846_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter measurement
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter on a plain copy of
+    known size), or None when the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -55,6 +85,8 @@ def main():
     ap.add_argument("--regime", default="literal", choices=["literal", "calibrated"])
     ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device (reference kernel for the HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -63,6 +95,16 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n}), flush=True)
+        return
 
     from paper_2609_30846_amd import ipk
     from workloads import make_workload
@@ -86,23 +128,32 @@ def main():
         mod(x, pe, lengths=lengths, y=y, stream=stream)
     torch.cuda.synchronize()
 
-    # per-step stage events, recorded by the library on the launch stream
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for row in evs:
-        for e in row:
-            e.record(stream)
+    # timed region: K whole steps, bracketed by synchronizations; no per-kernel
+    # events inside it (recording them costs the stream about as much as a kernel)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
-    for k in range(args.steps):
-        ipk.ipk_relpos_attn_record_stages(mod.handle, evs[k])
+    for _ in range(args.steps):
         mod(x, pe, lengths=lengths, y=y, stream=stream)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / args.steps
+
+    # stage pass: K more steps with per-kernel HIP events recorded by the library on
+    # the launch stream (event i at the start of kernel i, event 4 at the end of the
+    # last); stage_ms and the roofline's kernel duration come from it
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for row in evs:
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        ipk.ipk_relpos_attn_record_stages(mod.handle, evs[k])
+        mod(x, pe, lengths=lengths, y=y, stream=stream)
+    torch.cuda.synchronize()
 
     stage_names = ["projections", "bias_terms", "attention", "out_projection"]
     stage_ms = np.zeros(4)
@@ -141,6 +192,7 @@ def main():
         "pct_int8_peak": round(100.0 * tops / INT8_PEAK_TOPS, 3),
         "algorithmic_ops": ops,
         "stage_ms": {n: round(float(v), 5) for n, v in zip(stage_names, stage_ms)},
+        "stage_timing": "separate pass of the same K steps with per-kernel HIP events on the launch stream",
         "wall_s_timed_region": round(wall, 4),
         "roofline": {
             "kernel": "relpos_attn_core",
@@ -149,7 +201,7 @@ def main():
             "peak": INT8_PEAK_TOPS,
             "unit": "TOP/s",
             "frac": round(attn_tops / INT8_PEAK_TOPS, 5),
-            "traffic": None,
+            "traffic": measured_traffic("relpos_attn_core"),
         },
     }
 

@@ -144,12 +144,13 @@ int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst,
 
 /*
  * Stage timing for profiling: the NEXT run on `h` records the five caller-created
- * HIP events events[0..4] (hipEvent_t, created with timing enabled) on its stream
- * before the Q|K|V and position projections, before the bias/prefix-sum kernel,
- * before the attention core, before the output projection, and after it.  The
- * events are used once; later runs record nothing until this is called again.
- * events = NULL clears a pending request.  Errors: IPK_ERR_INVALID_ARG (null
- * handle, or a null entry in events).
+ * HIP events events[0..4] (hipEvent_t, created with timing enabled) on its stream:
+ * events[0..3] when the Q|K|V and position projections, the bias kernel, the
+ * attention core and the output projection start, events[4] when the output
+ * projection ends.  The events are carried by the kernel dispatches themselves,
+ * so recording them adds no work to the stream.  The events are used once; later
+ * runs record nothing until this is called again.  events = NULL clears a pending
+ * request.  Errors: IPK_ERR_INVALID_ARG (null handle, or a null entry in events).
  */
 int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
 

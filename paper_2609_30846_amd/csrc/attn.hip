@@ -716,7 +716,8 @@ int attn_key_split(int DK, int T_al, long bh_count, int T) {
 }
 
 template <int DK, int KS, bool WIDE>
-static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int T_al, hipStream_t st) {
+static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int T_al, hipStream_t st,
+                                  const LaunchEv& ev) {
   const size_t shmem = attn_lds_bytes(DK, KS, T_al);
   hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS, WIDE>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
@@ -726,20 +727,19 @@ static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int
   a2.nqb = (T + wgq - 1) / wgq;
   a2.xcd_group = (B * H) % 8 == 0;
   dim3 grid(a2.nqb * B * H);
-  hipLaunchKernelGGL((relpos_attn_core<DK, KS, WIDE>), grid, dim3(64 * ATTN_WAVES), shmem, st, a2);
-  return hipGetLastError();
+  return launch_kernel(relpos_attn_core<DK, KS, WIDE>, grid, dim3(64 * ATTN_WAVES), (uint32_t)shmem, st, ev, a2);
 }
 
 template <int DK, bool WIDE>
-static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st) {
+static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st, const LaunchEv& ev) {
   const int ks = attn_key_split(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
-  if (ks == 4) return launch_attn_cfg<DK, 4, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
-  if (ks == 8) return launch_attn_cfg<DK, 8, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st);
+  if (ks == 4) return launch_attn_cfg<DK, 4, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
+  if (ks == 8) return launch_attn_cfg<DK, 8, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
-                            hipStream_t st) {
+                            hipStream_t st, const LaunchEv& ev) {
   AttnArgs a{};
   a.q = ws.q;
   a.k = ws.k;
@@ -767,13 +767,13 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
   a.q_ln2 = sc.q_ln2;
   a.q_b = sc.q_b;
   a.q_c = sc.q_c;
-  if (rs.DK == 128) return sc.fs_wide ? launch_attn_dk<128, true>(a, rs, st) : launch_attn_dk<128, false>(a, rs, st);
-  if (rs.DK == 64) return sc.fs_wide ? launch_attn_dk<64, true>(a, rs, st) : launch_attn_dk<64, false>(a, rs, st);
+  if (rs.DK == 128) return sc.fs_wide ? launch_attn_dk<128, true>(a, rs, st, ev) : launch_attn_dk<128, false>(a, rs, st, ev);
+  if (rs.DK == 64) return sc.fs_wide ? launch_attn_dk<64, true>(a, rs, st, ev) : launch_attn_dk<64, false>(a, rs, st, ev);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspace& ws, const Lengths& lens,
-                             hipStream_t st) {
+                             hipStream_t st, const LaunchEv& ev) {
   (void)lens;
   BiasArgs a{};
   a.k = ws.k;
@@ -790,8 +790,7 @@ hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspa
   a.DK = rs.DK;
   a.p_rows = p_rows(rs.T_al);
   const long total = (long)a.BH * a.T_al + (long)a.H * a.p_rows + (long)a.BH * a.DK * (a.T_al / KCHUNK);
-  hipLaunchKernelGGL(bias_terms, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a);
-  return hipGetLastError();
+  return launch_kernel(bias_terms, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, ev, a);
 }
 
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,

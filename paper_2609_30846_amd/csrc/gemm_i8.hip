@@ -300,32 +300,31 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
 }
 
 template <int TN, int TM>
-static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st) {
+static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  hipLaunchKernelGGL((gemm_i8_requant<TN, TM>), dim3(8 * a.per_xcd), dim3(256), 0, st, a);
-  return hipGetLastError();
+  return launch_kernel(gemm_i8_requant<TN, TM>, dim3(8 * a.per_xcd), dim3(256), 0, st, ev, a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
-                              const int8_t* pos_table, hipStream_t st) {
+                              const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
   constexpr int TN = 256, TM = 128;
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
-  return launch_gemm<TN, TM>(a, tiles, st);
+  return launch_gemm<TN, TM>(a, tiles, st, ev);
 }
 
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
-                                 hipStream_t st) {
+                                 hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, y);
   constexpr int TN = 128, TM = 64;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  return launch_gemm<TN, TM>(a, tiles, st);
+  return launch_gemm<TN, TM>(a, tiles, st, ev);
 }
 
 }  // namespace ipk

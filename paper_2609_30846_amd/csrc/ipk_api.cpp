@@ -245,19 +245,17 @@ extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const 
   hipStream_t st = (hipStream_t)stream;
   const bool rec = h->stages_pending;
   h->stages_pending = false;
-  hipError_t e = hipSuccess;
-  auto mark = [&](int i) {
-    if (rec && e == hipSuccess) e = hipEventRecord(h->stage_ev[i], st);
-  };
-  mark(0);
-  if (e == hipSuccess) e = launch_projections(rs, h->w, h->ws, x, pos_table, st);
-  mark(1);
-  if (e == hipSuccess) e = launch_bias_terms(rs, h->w, h->ws, lens, st);
-  mark(2);
-  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st);
-  mark(3);
-  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st);
-  mark(4);
+  // stage events ride on the kernel dispatches: event i is stamped when kernel i
+  // starts, event 4 when the last kernel ends (no separate event packets)
+  LaunchEv ev[4];
+  if (rec) {
+    for (int i = 0; i < 4; ++i) ev[i].start = h->stage_ev[i];
+    ev[3].stop = h->stage_ev[4];
+  }
+  hipError_t e = launch_projections(rs, h->w, h->ws, x, pos_table, st, ev[0]);
+  if (e == hipSuccess) e = launch_bias_terms(rs, h->w, h->ws, lens, st, ev[1]);
+  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st, ev[2]);
+  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st, ev[3]);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;
   h->has_run = true;

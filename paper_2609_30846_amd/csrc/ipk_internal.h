@@ -21,6 +21,7 @@
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -82,15 +83,31 @@ struct RunShape {
   int p_base;  // workspace row of relative-position table row 0
 };
 
+// Optional timing events of one kernel launch, carried by the dispatch itself
+// (hipExtLaunchKernel): start is stamped when the kernel starts, stop when it ends.
+struct LaunchEv {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
+template <typename K, typename... Args>
+inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t st, const LaunchEv& ev,
+                                Args... args) {
+  if (ev.start || ev.stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, ev.start, ev.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
+  return hipGetLastError();
+}
+
 // Enqueue the kernels of one run; return the first HIP error.
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
-                              const int8_t* pos_table, hipStream_t st);
+                              const int8_t* pos_table, hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspace& ws, const Lengths& lens,
-                             hipStream_t st);
+                             hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
-                            hipStream_t st);
+                            hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
-                                 hipStream_t st);
+                                 hipStream_t st, const LaunchEv& ev = {});
 // Key split of the attention core for a run (0 when T_al does not fit LDS).
 int attn_key_split(int DK, int T_al, long bh_count, int T);
 
