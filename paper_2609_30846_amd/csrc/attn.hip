@@ -145,7 +145,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   const int8_t* VTh = a.vt + bh * DK * T_al;
   const int8_t* Ph = a.p + (size_t)h * a.p_rows * DK;
   const int32_t* bu = a.bu + bh * T_al;
-  const v4i* bv4 = (const v4i*)(a.bv + (size_t)h * a.p_rows * 4);
+  const int32_t* bvh = a.bv + (size_t)h * a.p_rows;
   const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
   uint8_t* my_rows = sbuf + (size_t)(32 * qset) * srow;
   // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
@@ -205,10 +205,13 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     const int8_t* kptr = Kh + (size_t)j_begin * DK;
     const int8_t* pptr = Ph + (size_t)(a.p_base + j_begin - q0 + T - 1) * DK;
     const int32_t* buptr = bu + j_begin;
-    const v4i* bvptr = bv4 + (a.p_base + j_begin - q0 + T - 1);
+    // v.P_r of this lane's column (one int32 per table row), splatted into the MFMA seed
+    const int32_t* bvptr = bvh + (a.p_base + j_begin - q0 + T - 1);
+    auto splat = [](int b) { return (v4i){b, b, b, b}; };
 
     // ping-pong register sets: "A" is the current step, "B" the other one
-    v4i kA[NKS], kB[NKS], pA[NKS], pB[NKS], gA[2], gB[2], bvA, bvB;
+    v4i kA[NKS], kB[NKS], pA[NKS], pB[NKS], gA[2], gB[2];
+    int bvA, bvB;
     int buA, buB;
     // rows just below the first step: tile 0's lo window and tile 1's lo window
     {
@@ -219,9 +222,9 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
         pm2[s] = *(const v4i*)(pptr - 32 * DK + frag + s * 1024);
       }
       bvB = bvptr[(int)col - 16];
-      const v4i bvm2 = bvptr[(int)col - 32];
-      gB[0] = bvB;
-      gB[1] = bvm2;
+      const int bvm2 = bvptr[(int)col - 32];
+      gB[0] = splat(bvB);
+      gB[1] = splat(bvm2);
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
         gB[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], pB[s], gB[0], 0, 0, 0);
@@ -242,7 +245,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     // previous one) and gl (the lo windows).  Writes the hi windows to gh and fetches
     // the next step's K, P and biases into kn, po, bvo, bun (the last step re-reads
     // its own rows, in bounds).
-    auto step = [&](const bool masked, v4i* kc, v4i* pc, const v4i bvc, const int buc, v4i* po, v4i& bvo,
+    auto step = [&](const bool masked, v4i* kc, v4i* pc, const int bvc, const int buc, v4i* po, int& bvo,
                     v4i* gl, v4i* gh, v4i* kn, int& bun) {
       const int adv = j0 + 16 < j_stop ? 16 : 0;
 #pragma unroll
@@ -250,8 +253,8 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
       bun = buptr[adv + col];
       v4i cs[2];
       cs[0] = cs[1] = (v4i){0, 0, 0, 0};
-      gh[0] = bvc;
-      gh[1] = bvo;
+      gh[0] = splat(bvc);
+      gh[1] = splat(bvo);
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
         cs[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], kc[s], cs[0], 0, 0, 0);
@@ -363,18 +366,23 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
 #pragma unroll
     for (int t = 0; t < 2; ++t) erow[t] = tab + Mrow[t] * 32 + (lane & 31);
     for (int c = c_begin; c < c_full; ++c) {
+      // all 32 lookups of the chunk are issued before any is summed (LDS latency
+      // overlaps instead of being paid once per four codes)
+      v4i sv[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) sv[t] = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+      uint32_t ev[2][16];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          ev[t][k] = erow[t][__mul24(-32, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+        uint32_t acc_e = 0;
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t x = (uint32_t)sv[wd];
-          const uint32_t e0 = erow[t][__mul24(-32, (int)(x & 0xff))];
-          const uint32_t e1 = erow[t][__mul24(-32, (int)((x >> 8) & 0xff))];
-          const uint32_t e2 = erow[t][__mul24(-32, (int)((x >> 16) & 0xff))];
-          const uint32_t e3 = erow[t][__mul24(-32, (int)(x >> 24))];
-          sum[t] += e0 + e1 + e2 + e3;
-        }
+        for (int k = 0; k < 16; ++k) acc_e += ev[t][k];
+        sum[t] += acc_e;
       }
     }
     if (c_full < c_end) {  // the chunk that holds the utterance's last key
@@ -436,21 +444,26 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     const int vt_off = col * 64 + g * 16;       // lane's bytes of a 16-channel x 64-key block
     constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
     // softmax codes (as a - 128) of one chunk of keys for both query tiles
+    // all 32 lookups of a chunk are issued before any is packed
     auto codes_full = [&](int c, v4i* af) {
+      v4i sv[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) sv[t] = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+      uint32_t av[2][16];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const uint32_t* arow = t ? arow1 : arow0;
-        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          av[t][k] = arow[__mul24(-32, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t x = (uint32_t)sv[wd];
-          const uint32_t a0 = arow[__mul24(-32, (int)(x & 0xff))];
-          const uint32_t a1 = arow[__mul24(-32, (int)((x >> 8) & 0xff))];
-          const uint32_t a2 = arow[__mul24(-32, (int)((x >> 16) & 0xff))];
-          const uint32_t a3 = arow[__mul24(-32, (int)(x >> 24))];
-          af[t][wd] = (int)(a0 | (a1 << 8) | (a2 << 16) | (a3 << 24));
+          const uint32_t* e = av[t] + 4 * wd;
+          af[t][wd] = (int)(e[0] | (e[1] << 8) | (e[2] << 16) | (e[3] << 24));
         }
-      }
     };
     auto codes_tail = [&](int c, v4i* af) {
 #pragma unroll
@@ -634,7 +647,7 @@ __global__ __launch_bounds__(256) void bias_terms(BiasArgs a) {
     const int h = (int)(idx / a.p_rows);
     const int r = (int)(idx - (long)h * a.p_rows);
     const int val = dot_frag_row(a.v + (size_t)h * a.DK, a.p + (size_t)h * a.p_rows * a.DK + frag_index(r, 0, a.DK), a.DK);
-    *(v4i*)(a.bv + idx * 4) = (v4i){val, val, val, val};
+    a.bv[idx] = val;
     return;
   }
   idx -= n_bv;

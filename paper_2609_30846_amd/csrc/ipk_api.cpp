@@ -180,7 +180,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->ws.p, H * PR * DK));
   chk(dev_alloc(h, &h->ws.ctx, Bm * (size_t)h->max_T * d));
   chk(dev_alloc(h, &h->ws.bu, Bm * H * T_al));
-  chk(dev_alloc(h, &h->ws.bv, H * PR * 4));
+  chk(dev_alloc(h, &h->ws.bv, H * PR));
   chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK) * DK));
   if (e != hipSuccess) {
     free_handle(h);

@@ -14,8 +14,7 @@
 //                16-key tile starts a 16-row block.  The rows around the table keep
 //                every padded tile in bounds (their contents are never used).
 //   bu     int32 [B][H][T_al]       u . K_j  (rank-1 part of the content score)
-//   bv     int32 [H][P_ROWS][4]     v . P_r  (rank-1 part of the position score), four
-//                                   copies per row: the tuple seeds an MFMA accumulator
+//   bv     int32 [H][P_ROWS]        v . P_r  (rank-1 part of the position score)
 //   vsum   int32 [B][H][T_al/64][16][DK/16] sums of V over each 64-key chunk; channel n
 //                                   at [n % 16][n / 16]
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
