@@ -5,10 +5,12 @@
 // rescaled by a per-output-channel multiplier m and a right shift n with round to
 // nearest (ties up), and clamped to the symmetric int8 grid.
 //
-// Kernel shape: one 256-thread workgroup computes a TN (channels) x TM (tokens) tile
-// with v_mfma_i32_32x32x32_i8; the four waves form a 2 x 2 grid of (TN/2) x (TM/2)
-// sub-tiles.  K advances in 128-byte steps, so every global row segment is a whole
-// cache line; the next step is fetched into registers while the current one is
+// Kernel shape: one workgroup of 2 x NWM waves computes a TN (channels) x TM (tokens)
+// tile with v_mfma_i32_32x32x32_i8; the waves form a 2 x NWM grid of (TN/2) x (TM/NWM)
+// sub-tiles.  The loads, not the matrix cores, bound a step, and the operand bytes
+// per multiply-accumulate fall as the tile grows: the large projections use 256 x 256
+// tiles of eight waves.  K advances in 128-byte steps, so every global row segment is
+// a whole cache line; the next step is fetched into registers while the current one is
 // multiplied out of LDS.  LDS rows are 128 bytes with the eight 16-byte chunks
 // XOR-swizzled by the row index, which keeps both the 16-byte stores of the fetch
 // and the 16-byte MFMA operand reads free of bank conflicts.
@@ -55,7 +57,7 @@ struct GemmArgs {
   int tiles_total;
   int per_xcd;  // logical tiles dealt to each XCD
   int8_t *q, *k, *vt, *p, *y;
-  int T_al, H, DK, d, p_rows, p_base;
+  int T_al, H, dk_shift, d, p_rows, p_base;  // d_k = 2^dk_shift
 };
 
 constexpr int BK = 128;  // bytes of K per step
@@ -69,7 +71,11 @@ __device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ ((r
 // biased code y + 128 of one accumulator (exact, see the header comment)
 __device__ __forceinline__ uint32_t requant_code(int acc, double scale) {
   const double t = __builtin_fma((double)acc, scale, 128.5);
-  return (uint32_t)(int)__builtin_fmin(__builtin_fmax(t, 1.0), 255.0);
+  // v_cvt_i32_f64 truncates and saturates to the int32 range; truncation equals the
+  // floor wherever the clamp below does not decide the result (t >= 1)
+  int v;
+  asm("v_cvt_i32_f64 %0, %1" : "=v"(v) : "v"(t));
+  return (uint32_t)min(max(v, 1), 255);
 }
 
 // four biased codes -> four int8 bytes (code - 128 == code ^ 0x80 for code in [1, 255])
@@ -77,14 +83,19 @@ __device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2,
   return (c0 | (c1 << 8) | (c2 << 16) | (c3 << 24)) ^ 0x80808080u;
 }
 
-template <int TN, int TM>
-__global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
+template <int TN, int TM, int NWM>
+__global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
+  constexpr int NTH = 128 * NWM;            // threads: 2 waves along N, NWM along M
+  constexpr int WTM = TM / NWM;             // tokens per wave
   constexpr int FN = TN / 64;               // 32-row MFMA tiles per wave along N
-  constexpr int FM = TM / 64;               // 32-col MFMA tiles per wave along M
-  constexpr int LW = TN * (BK / 16) / 256;  // 16-byte global loads per thread, W tile
-  constexpr int LX = TM * (BK / 16) / 256;  // same for the X tile
-  __shared__ __align__(16) int8_t sw[TN * BK];
-  __shared__ __align__(16) int8_t sx[TM * BK];
+  constexpr int FM = WTM / 32;              // 32-col MFMA tiles per wave along M
+  constexpr int LW = TN * (BK / 16) / NTH;  // 16-byte global loads per thread, W tile
+  constexpr int LX = TM * (BK / 16) / NTH;  // same for the X tile
+  constexpr int FROWS = NTH / 8;            // rows one pass of the fetch covers
+  static_assert(FM >= 1 && LW >= 1 && LX >= 1 && WTM % 32 == 0 && NTH >= TN, "tile shape");
+  // two LDS buffers: the next K step is stored while the current one is multiplied
+  __shared__ __align__(16) int8_t sw[2][TN * BK];
+  __shared__ __align__(16) int8_t sx[2][TM * BK];
   __shared__ double ssc[TN];
 
   // XCD-aware deal: workgroup i runs on XCD i % 8; XCD x owns logical tiles
@@ -103,23 +114,26 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
   const int band_m = min(P.band, tiles_m - band_idx * P.band);
   const int nt = in_band / band_m;
   const int mt = band_idx * P.band + (in_band - nt * band_m);
-  const int n0 = nt * TN;
-  const int ub = mt / P.tiles_m_per;               // utterance
-  const int t0 = (mt - ub * P.tiles_m_per) * TM;   // first token of the tile
-  const int K = P.K, rows = P.rows;
+  // the divisions above run on the vector unit: readfirstlane keeps the tile
+  // coordinates (and the buffer descriptors built from them) in scalar registers
+  const int n0 = __builtin_amdgcn_readfirstlane(nt * TN);
+  const int ub = __builtin_amdgcn_readfirstlane(mt / P.tiles_m_per);                  // utterance
+  const int t0 = __builtin_amdgcn_readfirstlane((mt - (mt / P.tiles_m_per) * P.tiles_m_per) * TM);  // first token
+  const int K = __builtin_amdgcn_readfirstlane(P.K), rows = __builtin_amdgcn_readfirstlane(P.rows);
+  const int N = __builtin_amdgcn_readfirstlane(P.N), mode = __builtin_amdgcn_readfirstlane(P.mode);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wn = wave & 1, wm = wave >> 1;
+  const int wn = wave & 1, wm = wave >> 1;  // wm in [0, NWM)
 
-  if (tid < TN) ssc[tid] = P.scale[min(n0 + tid, P.N - 1)];
+  if (tid < TN) ssc[tid] = P.scale[min(n0 + tid, N - 1)];
 
   // thread -> (row, chunk) of the fetch: 8 threads cover one 128-byte row segment.
   // Raw buffer loads: rows past the end of the operand (their whole offset is in the
   // per-lane operand, which the bounds check covers) read as zeros.
-  const int fchunk = tid & 7, frow = tid >> 3;  // rows frow + 32 r
+  const int fchunk = tid & 7, frow = tid >> 3;  // rows frow + FROWS r
   const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(P.w + (size_t)n0 * K), (short)0, (P.N - n0) * K, BUF_WORD3);
+      (void*)(P.w + (size_t)n0 * K), (short)0, (N - n0) * K, BUF_WORD3);
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.x + ((size_t)ub * rows + t0) * K), (short)0, (rows - t0) * K, BUF_WORD3);
   const int foff = frow * K + fchunk * 16;
@@ -130,10 +144,10 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
     if (k0 + fchunk * 16 < K) {
 #pragma unroll
       for (int r = 0; r < LW; ++r)
-        rw[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, foff + 32 * r * K + k0, 0, 0);
+        rw[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, foff + FROWS * r * K + k0, 0, 0);
 #pragma unroll
       for (int r = 0; r < LX; ++r)
-        rx[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + 32 * r * K + k0, 0, 0);
+        rx[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
     } else {
 #pragma unroll
       for (int r = 0; r < LW; ++r) rw[r] = (v4i){};
@@ -141,16 +155,16 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
       for (int r = 0; r < LX; ++r) rx[r] = (v4i){};
     }
   };
-  auto stash = [&]() {
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int r = 0; r < LW; ++r) *(v4i*)(sw + lds_off(frow + 32 * r, fchunk)) = rw[r];
+    for (int r = 0; r < LW; ++r) *(v4i*)(sw[buf] + lds_off(frow + FROWS * r, fchunk)) = rw[r];
 #pragma unroll
-    for (int r = 0; r < LX; ++r) *(v4i*)(sx + lds_off(frow + 32 * r, fchunk)) = rx[r];
+    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[r];
   };
 
   // waves whose channels are V produce the transposed product (tokens along MFMA rows)
   const int nw0 = n0 + wn * (TN / 2);
-  const bool vwave = P.mode == OUT_QKV && nw0 >= 2 * args.d;
+  const bool vwave = mode == OUT_QKV && nw0 >= 2 * args.d;
 
   v16i acc[FN][FM];
 #pragma unroll
@@ -165,26 +179,33 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
   // branch inside it
   auto kloop = [&](auto swap_tag) {
     constexpr bool SWAP = decltype(swap_tag)::value;
+    // step kt is multiplied out of buffer kt % 2 while step kt + 1 (fetched during
+    // step kt - 1) is stored into the other one; one barrier per step orders both
     fetch(0);
+    stash(0);
+    if (nk > 1) fetch(BK);
+    __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
-      stash();
-      __syncthreads();
-      if (kt + 1 < nk) fetch((kt + 1) * BK);
+      const int cur = kt & 1;
 #pragma unroll
       for (int ks = 0; ks < BK / 32; ++ks) {
         v4i af[FN], bf[FM];
 #pragma unroll
         for (int i = 0; i < FN; ++i)
-          af[i] = *(const v4i*)(sw + lds_off(wn * (TN / 2) + i * 32 + frag_row, 2 * ks + half));
+          af[i] = *(const v4i*)(sw[cur] + lds_off(wn * (TN / 2) + i * 32 + frag_row, 2 * ks + half));
 #pragma unroll
         for (int j = 0; j < FM; ++j)
-          bf[j] = *(const v4i*)(sx + lds_off(wm * (TM / 2) + j * 32 + frag_row, 2 * ks + half));
+          bf[j] = *(const v4i*)(sx[cur] + lds_off(wm * WTM + j * 32 + frag_row, 2 * ks + half));
 #pragma unroll
         for (int i = 0; i < FN; ++i)
 #pragma unroll
           for (int j = 0; j < FM; ++j)
             acc[i][j] = SWAP ? __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[j], af[i], acc[i][j], 0, 0, 0)
                              : __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+      if (kt + 1 < nk) {
+        stash(cur ^ 1);
+        if (kt + 2 < nk) fetch((kt + 2) * BK);
       }
       __syncthreads();
     }
@@ -194,13 +215,37 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
 
   // Epilogue.  Accumulator g * 4 + e of a lane sits at MFMA row g * 8 + half * 4 + e
   // and column lane % 32.  After requantization each lane holds dwords D[g] (4 rows);
-  // trading D[2], D[3] of the low half for D[0], D[1] of the high half gives the low
-  // half rows 0..15 and the high half rows 16..31, 16 bytes each.
+  // v_permlane32_swap trades the low half's D[2], D[3] for the high half's D[0], D[1],
+  // which leaves the low half with rows 0..15 and the high half with rows 16..31 of
+  // its column, 16 bytes each.  A 32-channel sub-tile never straddles N, a head or the
+  // Q/K/V boundary (N and d_k are multiples of 64), so its destination is uniform.
   const int col = lane & 31;
-  const int tw0 = t0 + wm * (TM / 2);
+  const int tw0 = t0 + wm * WTM;
+  const int dks = args.dk_shift, DKm = (1 << dks) - 1;
+  const size_t head_bytes = (size_t)args.T_al << dks;  // one (utterance, head) block of Q, K or V^T
+  // frag_index / vt_index with d_k = 2^dks
+  auto frag_off = [&](int row, int kk) {
+    return ((size_t)(row >> 4) << (dks + 4)) + (size_t)((kk >> 6) << 10) + ((row & 15) << 6) + (kk & 63);
+  };
+  auto vt_off = [&](int t, int kk) { return ((size_t)(t >> 6) << (dks + 6)) + (size_t)(kk << 6) + (t & 63); };
 #pragma unroll
   for (int i = 0; i < FN; ++i) {
     const int nl = wn * (TN / 2) + i * 32;  // first channel of this sub-tile, tile-local
+    const int nb = n0 + nl;
+    if (nb >= N) continue;
+    int8_t* dst;
+    int kk = 0;  // channel of the sub-tile's first row inside its head
+    if (mode == OUT_QKV) {
+      const int which = (nb >= args.d) + (nb >= 2 * args.d);
+      const int c = nb - which * args.d;
+      dst = (which == 0 ? args.q : which == 1 ? args.k : args.vt) + ((size_t)ub * args.H + (c >> dks)) * head_bytes;
+      kk = c & DKm;
+    } else if (mode == OUT_POS) {
+      dst = args.p + ((size_t)(nb >> dks) * args.p_rows << dks);
+      kk = nb & DKm;
+    } else {
+      dst = args.y + (size_t)ub * rows * N + nb;
+    }
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       uint32_t D[4];
@@ -220,40 +265,22 @@ __global__ __launch_bounds__(256) void gemm_i8_requant(GemmArgs args) {
                        requant_code(acc[i][j][g * 4 + 2], ssc[c + 2]), requant_code(acc[i][j][g * 4 + 3], ssc[c + 3]));
         }
       }
-      const uint32_t s0 = __shfl_xor(half ? D[0] : D[2], 32);
-      const uint32_t s1 = __shfl_xor(half ? D[1] : D[3], 32);
-      v4i out;
-      if (half == 0) out = (v4i){(int)D[0], (int)s0, (int)D[1], (int)s1};
-      else out = (v4i){(int)s0, (int)D[2], (int)s1, (int)D[3]};
+      const auto x02 = __builtin_amdgcn_permlane32_swap(D[0], D[2], false, false);
+      const auto x13 = __builtin_amdgcn_permlane32_swap(D[1], D[3], false, false);
+      const v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
 
       if (vwave) {
-        // 16 consecutive tokens of channel n; tokens up to the next multiple of 16
+        // 16 consecutive tokens of one channel; tokens up to the next multiple of 16
         // stay inside the padded key range of V^T
-        const int n = n0 + nl + col;
         const int t = tw0 + j * 32 + half * 16;
-        if (n < P.N && t < rows) {
-          const int c = n - 2 * args.d;
-          const int h = c / args.DK, kk = c - h * args.DK;
-          int8_t* base = args.vt + ((size_t)ub * args.H + h) * args.T_al * args.DK;
-          *(v4i*)(base + vt_index(t, kk, args.DK)) = out;
-        }
+        if (t < rows) *(v4i*)(dst + vt_off(t, kk + col)) = out;
       } else {
         // 16 consecutive channels of token t
-        const int n = n0 + nl + half * 16;
         const int t = tw0 + j * 32 + col;
-        if (n < P.N && t < rows) {
-          if (P.mode == OUT_QKV) {
-            const int which = n / args.d;
-            const int c = n - which * args.d;
-            const int h = c / args.DK, kk = c - h * args.DK;
-            int8_t* base = (which == 0 ? args.q : args.k) + ((size_t)ub * args.H + h) * args.T_al * args.DK;
-            *(v4i*)(base + frag_index(t, kk, args.DK)) = out;
-          } else if (P.mode == OUT_POS) {
-            const int h = n / args.DK, kk = n - h * args.DK;
-            *(v4i*)(args.p + (size_t)h * args.p_rows * args.DK + frag_index(args.p_base + t, kk, args.DK)) = out;
-          } else {
-            *(v4i*)(args.y + ((size_t)ub * rows + t) * P.N + n) = out;
-          }
+        if (t < rows) {
+          if (mode == OUT_QKV) *(v4i*)(dst + frag_off(t, kk + half * 16)) = out;
+          else if (mode == OUT_POS) *(v4i*)(dst + frag_off(args.p_base + t, kk + half * 16)) = out;
+          else *(v4i*)(dst + (size_t)t * N + half * 16) = out;
         }
       }
     }
@@ -293,38 +320,38 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.y = y;
   a.T_al = rs.T_al;
   a.H = rs.H;
-  a.DK = rs.DK;
+  a.dk_shift = rs.DK == 128 ? 7 : 6;  // d_k is 64 or 128
   a.d = rs.d;
   a.p_rows = p_rows(rs.T_al);
   a.p_base = rs.p_base;
 }
 
-template <int TN, int TM>
+template <int TN, int TM, int NWM>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM>, dim3(8 * a.per_xcd), dim3(256), 0, st, ev, a);
+  return launch_kernel(gemm_i8_requant<TN, TM, NWM>, dim3(8 * a.per_xcd), dim3(128 * NWM), 0, st, ev, a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
-  constexpr int TN = 256, TM = 128;
+  constexpr int TN = 256, TM = 256, NWM = 4;
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
-  return launch_gemm<TN, TM>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWM>(a, tiles, st, ev);
 }
 
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, y);
-  constexpr int TN = 128, TM = 64;
+  constexpr int TN = 128, TM = 64, NWM = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  return launch_gemm<TN, TM>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWM>(a, tiles, st, ev);
 }
 
 }  // namespace ipk
