@@ -1,19 +1,21 @@
 // Relative-position attention core of the integer MHSA block (Sec. 3.1).
 //
 // Work split: a workgroup of ATTN_WAVES waves owns (utterance b, head h, WGQ
-// consecutive queries).  Each wave owns 32 queries (two 16-query MFMA tiles, so
-// every K, P and V fragment it loads feeds two MFMAs); KSPLIT waves share one set
-// of 32 queries and split its keys: phase 1 in 16-key steps, phases 2 and 3 in
-// 64-key chunks (scores are exchanged through LDS in between).
+// consecutive queries).  Each wave owns NTL 16-query MFMA tiles (32 or 48 queries:
+// every K, P and V fragment it loads feeds NTL MFMAs, and the loads bound the
+// kernel); KSPLIT waves share one set of queries and split its keys: phase 1 in
+// 16-key steps, phases 2 and 3 in 64-key chunks (scores are exchanged through LDS in
+// between).  The host picks (KSPLIT, NTL) per launch from the LDS the score rows need
+// and the rounds of workgroups over the CUs.
 //
 // Phase 1, per 16-key step, with v_mfma_i32_16x16x64_i8 (queries on MFMA rows):
 //  * content   c = Q K^T, accumulator seeded with the rank-1 term u.K_j
 //  * position  G = Q P_win^T, seeded with v.P_r, for the 16 table rows that
 //              start at relative position j0-i0+T-1 ("hi" window).  The rows
-//              just before it ("lo") are the previous step's hi window, and the
-//              second query tile reuses the first tile's previous P fragment,
-//              so each step loads one new P fragment and runs one new position
-//              MFMA pair per tile.
+//              just before it ("lo") are the previous step's hi window, and tile t
+//              reuses the P fragment tile 0 loaded t steps earlier, so each step
+//              loads one new P fragment and runs one new position MFMA pair per
+//              tile.
 //  * Phi       p_ij = G_i(j-i+T-1) is a rotation by the row index inside each
 //              16-lane row group: every source lane picks the window its value
 //              belongs to and ds_bpermute moves it to the lane of its key.
@@ -33,9 +35,13 @@
 // with the V fragments; V is streamed in parts of four 16-channel tiles); partial
 // contexts of the KSPLIT waves are added with LDS atomics (exact int32) and
 // requantized with (m_o, shift_o) by all waves together.
-// Both lookup tables are laid out [d][32] in dwords: the exp table holds one copy
-// per LDS bank (lane l reads copy l % 32), the code table holds row r in bank
-// r % 32, so a lookup is one multiply-add and one conflict-free ds_read_b32.
+// Both lookup tables are laid out [d][32 banks] in dwords: the exp table holds one
+// copy per bank (lane l reads copy l % 32); the code tables hold bytes, row r = 16 tt
+// + rr in byte tt of banks rr and rr + 16, and the two half-waves' lanes g = 0, 1 (2,
+// 3) read different copies, so a lookup is one multiply-add and one conflict-free
+// LDS read.
+#include <type_traits>
+
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -58,7 +64,7 @@ struct AttnArgs {
 };
 
 constexpr int SCORE_PAD = 16;  // bytes added to each LDS score row
-constexpr int TAB_BLOCK = 256 * 32;  // dwords of one [d][32] lookup table
+constexpr int TAB_DW = 256 * 32;  // dwords of the [d][32 banks] lookup-table region
 
 __device__ __forceinline__ uint32_t iexp_int(int d, int q_ln2, int q_b, int q_c) {
   // I-BERT integer exp of -d: d = z q_ln2 - r with r in (-q_ln2, 0]
@@ -85,13 +91,18 @@ __device__ __forceinline__ int mad_i24(int a, int b, int c) {
 
 constexpr int ATTN_WAVES = 8;  // waves per workgroup (two per SIMD)
 
-template <int DK, int KSPLIT, bool WIDE>
+template <int S>
+using Phase = std::integral_constant<int, S>;
+
+template <int DK, int KSPLIT, int NTL, bool WIDE>
 __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets of 32 per workgroup
-  constexpr int WGQ = 32 * NQS;              // queries per workgroup
-  constexpr int NKS = DK / 64;          // MFMA K-steps over d_k
-  constexpr int NT = DK / 16;           // 16-channel output tiles of the context
+  constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets per workgroup
+  constexpr int ROWS = 16 * NTL;            // queries per set: NTL 16-query MFMA tiles
+  constexpr int WGQ = ROWS * NQS;           // queries per workgroup
+  constexpr int NKS = DK / 64;              // MFMA K-steps over d_k
+  constexpr int NT = DK / 16;               // 16-channel output tiles of the context
+  static_assert(NQS * NTL <= 4, "the code tables hold four 16-row tiles");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in SGPRs
@@ -114,7 +125,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   }
   const int b = bhi / a.H, h = bhi - (bhi / a.H) * a.H;
   const int wg_q0 = qb * WGQ;
-  const int q0 = wg_q0 + 32 * qset;  // first query of this wave
+  const int q0 = wg_q0 + ROWS * qset;  // first query of this wave
   const int L = a.lens.len[b];
   const int T = a.T, T_al = a.T_al;
   const int srow = T_al + SCORE_PAD;
@@ -126,18 +137,17 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   // LDS carve-up (the host computes the same sizes)
   constexpr int RSTRIDE = DK + 4;  // dwords per row of the key-split partial sums
   const int s_bytes = WGQ * srow;
-  const int red_bytes = KSPLIT > 1 ? NQS * 32 * RSTRIDE * 4 : 0;
+  const int red_bytes = KSPLIT > 1 ? NQS * ROWS * RSTRIDE * 4 : 0;
   const int big = ((s_bytes > red_bytes ? s_bytes : red_bytes) + 15) & ~15;
   uint8_t* sbuf = smem;
   int32_t* red = (int32_t*)smem;  // reused once the scores are consumed
-  // lookup tables: first the per-bank copies of the exp table (phase 2), then the
-  // per-row code tables, 32 rows per block (phase 3)
+  // lookup tables, [d][32 banks] in dwords: first the per-bank copies of the exp
+  // table (phase 2), then the code tables (phase 3)
   uint32_t* tab = (uint32_t*)(smem + big);
-  constexpr int TAB_DW = (WGQ / 32) * TAB_BLOCK;
   uint32_t* etab = tab + TAB_DW;  // the 255 exp values, once
   int32_t* smax = (int32_t*)(etab + 256);
-  uint32_t* ssum = (uint32_t*)(smax + 32 * ATTN_WAVES);
-  uint32_t* sF = ssum + 32 * ATTN_WAVES;
+  uint32_t* ssum = (uint32_t*)(smax + ROWS * ATTN_WAVES);
+  uint32_t* sF = ssum + ROWS * ATTN_WAVES;
 
   const size_t bh = (size_t)b * a.H + h;
   const int8_t* Qh = a.q + bh * T_al * DK;
@@ -147,7 +157,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   const int32_t* bu = a.bu + bh * T_al;
   const int32_t* bvh = a.bv + (size_t)h * a.p_rows;
   const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
-  uint8_t* my_rows = sbuf + (size_t)(32 * qset) * srow;
+  uint8_t* my_rows = sbuf + (size_t)(ROWS * qset) * srow;
   // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
   const int frag_off = col * 64 + g * 16;
 
@@ -168,9 +178,9 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
 
   // ---------------- phase 1: fused scores into LDS, running row max
-  int mx[2][4];
+  int mx[NTL][4];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < NTL; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) mx[t][i] = LOCODE;
 
@@ -181,11 +191,15 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   const int j_full = max(j_begin, min(j_stop, L & ~15));  // steps below this are unmasked
   if (active && j_begin < j_stop) {
     const uint32_t frag = (uint32_t)frag_off;
-    v4i qf[2][NKS];
+    v4i qf[NTL][NKS];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < NTL; ++t) {
+      // a tile past the padded sequence (last workgroup, T_al not a multiple of the
+      // workgroup's queries) re-reads the last tile: its rows are never stored
+      const int qrow = min(q0 + 16 * t, T_al - 16);
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) qf[t][s] = *(const v4i*)(Qh + (size_t)(q0 + 16 * t) * DK + frag + s * 1024);
+      for (int s = 0; s < NKS; ++s) qf[t][s] = *(const v4i*)(Qh + (size_t)qrow * DK + frag + s * 1024);
+    }
     bool take_hi[4];
     int src_addr[4];
 #pragma unroll
@@ -198,88 +212,96 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     const uint32_t sel1 = (p & 1) ? 0x03070105u : 0x06020400u;
     const uint32_t sel2 = (p & 2) ? 0x03020706u : 0x05040100u;
     // after the transpose a lane stores query 4g+p of a tile, keys 4*(col/4) .. +3
-    uint8_t* sdst0 = my_rows + (size_t)(4 * g + p) * srow + (col >> 2) * 4;
-    uint8_t* sdst1 = sdst0 + (size_t)16 * srow;
+    uint8_t* sdst = my_rows + (size_t)(4 * g + p) * srow + (col >> 2) * 4;
 
-    // table row of (query q0, key j0) is j0 - q0 + T - 1; tile 1 sits 16 rows lower
+    // table row of (query q0, key j0) is j0 - q0 + T - 1; tile t sits 16 t rows lower
     const int8_t* kptr = Kh + (size_t)j_begin * DK;
     const int8_t* pptr = Ph + (size_t)(a.p_base + j_begin - q0 + T - 1) * DK;
     const int32_t* buptr = bu + j_begin;
     // v.P_r of this lane's column (one int32 per table row), splatted into the MFMA seed
     const int32_t* bvptr = bvh + (a.p_base + j_begin - q0 + T - 1);
-    auto splat = [](int b) { return (v4i){b, b, b, b}; };
+    auto splat = [](int bb) { return (v4i){bb, bb, bb, bb}; };
 
-    // ping-pong register sets: "A" is the current step, "B" the other one
-    v4i kA[NKS], kB[NKS], pA[NKS], pB[NKS], gA[2], gB[2];
-    int bvA, bvB;
-    int buA, buB;
-    // rows just below the first step: tile 0's lo window and tile 1's lo window
+    // Register rings over the step phase S = (step index) % NTL, all indices static:
+    //  pr[u], bvr[u]: tile 0's hi-window P fragment of the step with phase u; at
+    //                 phase S tile t uses slot (S - t) mod NTL (its window is tile
+    //                 0's window of t steps before)
+    //  kr[u], bur[u]: K fragment and u.K_j of the step with phase u (current, next)
+    //  gr[u][t]:      position MFMA results (hi windows) of the step with phase u;
+    //                 a step's lo windows are the previous step's hi windows
+    v4i pr[NTL][NKS], kr[NTL][NKS], gr[NTL][NTL];
+    int bvr[NTL], bur[NTL];
     {
-      v4i pm2[NKS];
+      // tile t's hi window of the first step: tile 0's window 16 t rows lower
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) {
-        pB[s] = *(const v4i*)(pptr - 16 * DK + frag + s * 1024);
-        pm2[s] = *(const v4i*)(pptr - 32 * DK + frag + s * 1024);
+      for (int t = 0; t < NTL; ++t) {
+        const int u = (NTL - t) % NTL;
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) pr[u][s] = *(const v4i*)(pptr - 16 * t * DK + frag + s * 1024);
+        bvr[u] = bvptr[(int)col - 16 * t];
       }
-      bvB = bvptr[(int)col - 16];
-      const int bvm2 = bvptr[(int)col - 32];
-      gB[0] = splat(bvB);
-      gB[1] = splat(bvm2);
+      // lo windows of the first step: tile t's lo window is tile (t + 1)'s hi window;
+      // the last tile's lies one more window lower
+      v4i plast[NKS];
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) {
-        gB[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], pB[s], gB[0], 0, 0, 0);
-        gB[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], pm2[s], gB[1], 0, 0, 0);
+      for (int s = 0; s < NKS; ++s) plast[s] = *(const v4i*)(pptr - 16 * NTL * DK + frag + s * 1024);
+      const int bvlast = bvptr[(int)col - 16 * NTL];
+#pragma unroll
+      for (int t = 0; t < NTL; ++t) {
+        const int u = (NTL - t - 1) % NTL;  // slot of tile (t + 1)'s hi window
+        v4i gacc = splat(t + 1 < NTL ? bvr[u] : bvlast);
+#pragma unroll
+        for (int s = 0; s < NKS; ++s)
+          gacc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], t + 1 < NTL ? pr[u][s] : plast[s], gacc, 0, 0, 0);
+        gr[NTL - 1][t] = gacc;
       }
     }
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) {
-      kA[s] = *(const v4i*)(kptr + frag + s * 1024);
-      pA[s] = *(const v4i*)(pptr + frag + s * 1024);
-    }
-    buA = buptr[col];
-    bvA = bvptr[col];
+    for (int s = 0; s < NKS; ++s) kr[0][s] = *(const v4i*)(kptr + frag + s * 1024);
+    bur[0] = buptr[col];
 
     int j0 = j_begin;
-    // One 16-key step.  Inputs: kc (K rows j0..), pc (table rows of tile 0's hi
-    // window) with its bias tuple bvc, po / bvo (tile 1's hi window = tile 0's
-    // previous one) and gl (the lo windows).  Writes the hi windows to gh and fetches
-    // the next step's K, P and biases into kn, po, bvo, bun (the last step re-reads
-    // its own rows, in bounds).
-    auto step = [&](const bool masked, v4i* kc, v4i* pc, const int bvc, const int buc, v4i* po, int& bvo,
-                    v4i* gl, v4i* gh, v4i* kn, int& bun) {
+    // One 16-key step at phase S: fetches the next step's K, P and biases (the last
+    // step re-reads its own rows, in bounds), runs the content and position MFMAs of
+    // every tile and turns them into score codes in LDS.
+    auto step = [&](auto Sc, const bool masked) {
+      constexpr int S = decltype(Sc)::value;
+      constexpr int SN = (S + 1) % NTL, SP = (S + NTL - 1) % NTL;
       const int adv = j0 + 16 < j_stop ? 16 : 0;
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) kn[s] = *(const v4i*)(kptr + adv * DK + frag + s * 1024);
-      bun = buptr[adv + col];
-      v4i cs[2];
-      cs[0] = cs[1] = (v4i){0, 0, 0, 0};
-      gh[0] = splat(bvc);
-      gh[1] = splat(bvo);
+      for (int s = 0; s < NKS; ++s) kr[SN][s] = *(const v4i*)(kptr + adv * DK + frag + s * 1024);
+      bur[SN] = buptr[adv + col];
+      v4i cs[NTL];
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) {
-        cs[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], kc[s], cs[0], 0, 0, 0);
-        cs[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], kc[s], cs[1], 0, 0, 0);
-        gh[0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[0][s], pc[s], gh[0], 0, 0, 0);
-        gh[1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[1][s], po[s], gh[1], 0, 0, 0);
+      for (int t = 0; t < NTL; ++t) {
+        cs[t] = (v4i){0, 0, 0, 0};
+        gr[S][t] = splat(bvr[(S + NTL - t) % NTL]);
       }
-      // tile 1's window of the next step is this step's tile-0 window: po is free now
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) po[s] = *(const v4i*)(pptr + adv * DK + frag + s * 1024);
-      bvo = bvptr[adv + col];
+      for (int s = 0; s < NKS; ++s)
+#pragma unroll
+        for (int t = 0; t < NTL; ++t) {
+          cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], kr[S][s], cs[t], 0, 0, 0);
+          gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], pr[(S + NTL - t) % NTL][s], gr[S][t], 0, 0, 0);
+        }
+      // the last tile's window (slot SN) is consumed: it takes the next step's tile-0 window
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) pr[SN][s] = *(const v4i*)(pptr + adv * DK + frag + s * 1024);
+      bvr[SN] = bvptr[adv + col];
       // rank-1 content term u.K_j folded into the addend: m_c (c0 + u.K_j) + rounding + code bias
       int k1 = 0;
       double k1d = 0.0;
       if (WIDE)
-        k1d = __builtin_fma(a.mcd, (double)buc, 128.5);
+        k1d = __builtin_fma(a.mcd, (double)bur[S], 128.5);
       else
-        k1 = __mul24(a.mc24, buc) + a.bias32;
+        k1 = __mul24(a.mc24, bur[S]) + a.bias32;
       const bool key_ok = j0 + col < L;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < NTL; ++t) {
         int code[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int sel = take_hi[i] ? gh[t][i] : gl[t][i];
+          const int sel = take_hi[i] ? gr[S][t][i] : gr[SP][t][i];
           const int pt = __builtin_amdgcn_ds_bpermute(src_addr[i], sel);
           int v;
           if (WIDE) {
@@ -304,7 +326,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
           packed = __builtin_amdgcn_perm((uint32_t)code[1], (uint32_t)code[0], 0x0c0c0602u) |
                    __builtin_amdgcn_perm((uint32_t)code[3], (uint32_t)code[2], 0x06020c0cu);
         }
-        *(uint32_t*)((t ? sdst1 : sdst0) + j0) = quad_transpose_bytes(packed, sel1, sel2);
+        *(uint32_t*)(sdst + (size_t)(16 * t) * srow + j0) = quad_transpose_bytes(packed, sel1, sel2);
       }
       kptr += 16 * DK;
       pptr += 16 * DK;
@@ -312,24 +334,28 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
       bvptr += 16;
       j0 += 16;
     };
-    // steps alternate register sets: A = (kA, pA, bvA) current with tile 1 on (pB, bvB)
-    while (j0 + 32 <= j_full) {
-      step(false, kA, pA, bvA, buA, pB, bvB, gB, gA, kB, buB);
-      step(false, kB, pB, bvB, buB, pA, bvA, gA, gB, kA, buA);
+    // NTL unmasked steps per iteration, so that every ring index stays static
+    while (j0 + 16 * NTL <= j_full) {
+      step(Phase<0>{}, false);
+      step(Phase<1>{}, false);
+      if constexpr (NTL > 2) step(Phase<2>{}, false);
     }
-    bool in_a = true;
+    // the rest (fewer than NTL steps below j_full, then the masked ones)
+    int ph = 0;
     while (j0 < j_stop) {
       const bool m = j0 + 16 > j_full;
-      if (in_a)
-        step(m, kA, pA, bvA, buA, pB, bvB, gB, gA, kB, buB);
+      if (ph == 0)
+        step(Phase<0>{}, m);
+      else if (ph == 1 || NTL == 2)
+        step(Phase<1 % NTL>{}, m);
       else
-        step(m, kB, pB, bvB, buB, pA, bvA, gA, gB, kA, buA);
-      in_a = !in_a;
+        step(Phase<2 % NTL>{}, m);
+      ph = ph + 1 == NTL ? 0 : ph + 1;
     }
   }
   // row max over the 16 key lanes of each row group
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < NTL; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       int v = mx[t][i];
@@ -339,46 +365,48 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     }
   if (col == 0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < NTL; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) smax[w * 32 + 16 * t + 4 * g + i] = WIDE ? mx[t][i] : (mx[t][i] >> 16);
+      for (int i = 0; i < 4; ++i) smax[w * ROWS + 16 * t + 4 * g + i] = WIDE ? mx[t][i] : (mx[t][i] >> 16);
   }
   __syncthreads();
 
   // phases 2 and 3: lane (g, col) works on query row `col` of each tile and keys
   // g*16 .. g*16+15 of a chunk
-  int Mrow[2];
+  int Mrow[NTL];
+  const uint8_t* srd[NTL];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < NTL; ++t) {
     int m = 1;
 #pragma unroll
-    for (int k2 = 0; k2 < KSPLIT; ++k2) m = max(m, smax[(qset * KSPLIT + k2) * 32 + 16 * t + col]);
+    for (int k2 = 0; k2 < KSPLIT; ++k2) m = max(m, smax[(qset * KSPLIT + k2) * ROWS + 16 * t + col]);
     Mrow[t] = m;
+    srd[t] = my_rows + (size_t)(16 * t + col) * srow + g * 16;
   }
-  const uint8_t* srd0 = my_rows + (size_t)col * srow + g * 16;
-  const uint8_t* srd1 = srd0 + (size_t)16 * srow;
 
   // ---------------- phase 2: row sums of the integer exp
   // lane l reads copy l % 32 of the exp table: e(M - code) at erow[-32 code]
-  uint32_t sum[2] = {0u, 0u};
+  uint32_t sum[NTL];
+#pragma unroll
+  for (int t = 0; t < NTL; ++t) sum[t] = 0u;
   if (active) {
-    const uint32_t* erow[2];
+    const uint32_t* erow[NTL];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) erow[t] = tab + Mrow[t] * 32 + (lane & 31);
+    for (int t = 0; t < NTL; ++t) erow[t] = tab + Mrow[t] * 32 + (lane & 31);
     for (int c = c_begin; c < c_full; ++c) {
-      // all 32 lookups of the chunk are issued before any is summed (LDS latency
+      // all lookups of the chunk are issued before any is summed (LDS latency
       // overlaps instead of being paid once per four codes)
-      v4i sv[2];
+      v4i sv[NTL];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) sv[t] = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
-      uint32_t ev[2][16];
+      for (int t = 0; t < NTL; ++t) sv[t] = *(const v4i*)(srd[t] + c * KCHUNK);
+      uint32_t ev[NTL][16];
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int k = 0; k < 16; ++k)
           ev[t][k] = erow[t][__mul24(-32, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < NTL; ++t) {
         uint32_t acc_e = 0;
 #pragma unroll
         for (int k = 0; k < 16; ++k) acc_e += ev[t][k];
@@ -388,8 +416,8 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     if (c_full < c_end) {  // the chunk that holds the utterance's last key
       const int c = c_full;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+      for (int t = 0; t < NTL; ++t) {
+        const v4i sv = *(const v4i*)(srd[t] + c * KCHUNK);
 #pragma unroll
         for (int by = 0; by < 16; ++by) {
           const bool ok = c * KCHUNK + g * 16 + by < L;
@@ -401,64 +429,71 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     }
   }
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < NTL; ++t) {
     sum[t] += __shfl_xor(sum[t], 16);
     sum[t] += __shfl_xor(sum[t], 32);
   }
   if (g == 0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) ssum[w * 32 + 16 * t + col] = sum[t];
+    for (int t = 0; t < NTL; ++t) ssum[w * ROWS + 16 * t + col] = sum[t];
   }
   __syncthreads();
   if (kpart == 0 && g == 0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < NTL; ++t) {
       uint32_t tot = 0;
 #pragma unroll
-      for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qset * KSPLIT + k2) * 32 + 16 * t + col];
-      sF[32 * qset + 16 * t + col] = tot ? (uint32_t)(((uint64_t)1 << 32) / tot) : 0u;
+      for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qset * KSPLIT + k2) * ROWS + 16 * t + col];
+      sF[ROWS * qset + 16 * t + col] = tot ? (uint32_t)(((uint64_t)1 << 32) / tot) : 0u;
     }
   }
   __syncthreads();
-  // softmax code tables (over the exp copies, which phase 2 has finished with):
-  // row r, distance d at dword (r / 32) * TAB_BLOCK + d * 32 + r % 32 holds
-  // min(floor(e(d) F_r / 2^24), 255) ^ 0x80, i.e. the byte a - 128
+  // softmax code tables (over the exp copies, which phase 2 has finished with): the
+  // dword of distance d and bank rr + 16 c (c = 0, 1: two copies) holds in byte tt
+  // min(floor(e(d) F_r / 2^24), 255) ^ 0x80 of row r = 16 tt + rr, i.e. a - 128.
+  // floor(e F / 2^24) is the high word of (e 2^8) F (e < 2^24).
   for (int idx = tid; idx < TAB_DW; idx += 64 * ATTN_WAVES) {
-    const int blk = idx / TAB_BLOCK, rem = idx - blk * TAB_BLOCK;
-    const int dd = rem >> 5, r = blk * 32 + (rem & 31);
-    const uint64_t v = ((uint64_t)etab[dd] * sF[r]) >> 24;
-    tab[idx] = (v > 255 ? 255u : (uint32_t)v) ^ 0x80u;
+    const int dd = idx >> 5, rr = idx & 15;
+    const uint32_t e8 = etab[dd] << 8;
+    uint32_t packed = 0;
+#pragma unroll
+    for (int tt = 0; tt < NQS * NTL; ++tt) {
+      const uint32_t v = __umulhi(e8, sF[16 * tt + rr]);
+      packed |= ((v > 255u ? 255u : v) ^ 0x80u) << (8 * tt);
+    }
+    tab[idx] = packed;
   }
   __syncthreads();
 
   // ---------------- phase 3: A.V on MFMA
-  v4i acc[2][NT];
+  v4i acc[NTL][NT];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < NTL; ++t)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[t][nt] = (v4i){0, 0, 0, 0};
   if (active && c_begin < c_end) {
-    // code of (row, M - code) at arow[-32 code]
-    const uint32_t* arow0 = tab + qset * TAB_BLOCK + Mrow[0] * 32 + col;
-    const uint32_t* arow1 = tab + qset * TAB_BLOCK + Mrow[1] * 32 + 16 + col;
+    // code byte of (row, M - code) at arow[-128 code]: lanes g = 0, 1 (and 2, 3) read
+    // the two bank copies of their row, so one read touches 32 distinct banks
+    const uint8_t* arow[NTL];
+#pragma unroll
+    for (int t = 0; t < NTL; ++t)
+      arow[t] = (const uint8_t*)tab + (Mrow[t] * 32 + col + 16 * (g & 1)) * 4 + (qset * NTL + t);
     const int vt_off = col * 64 + g * 16;       // lane's bytes of a 16-channel x 64-key block
     constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
-    // softmax codes (as a - 128) of one chunk of keys for both query tiles
-    // all 32 lookups of a chunk are issued before any is packed
+    // softmax codes (as a - 128) of one chunk of keys for every query tile;
+    // all lookups of a chunk are issued before any is packed
     auto codes_full = [&](int c, v4i* af) {
-      v4i sv[2];
+      v4i sv[NTL];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) sv[t] = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
-      uint32_t av[2][16];
+      for (int t = 0; t < NTL; ++t) sv[t] = *(const v4i*)(srd[t] + c * KCHUNK);
+      uint32_t av[NTL][16];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const uint32_t* arow = t ? arow1 : arow0;
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int k = 0; k < 16; ++k)
-          av[t][k] = arow[__mul24(-32, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
-      }
+          av[t][k] = arow[t][__mul24(-128, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
           const uint32_t* e = av[t] + 4 * wd;
@@ -467,9 +502,8 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     };
     auto codes_tail = [&](int c, v4i* af) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const uint32_t* arow = t ? arow1 : arow0;
-        const v4i sv = *(const v4i*)((t ? srd1 : srd0) + c * KCHUNK);
+      for (int t = 0; t < NTL; ++t) {
+        const v4i sv = *(const v4i*)(srd[t] + c * KCHUNK);
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
           uint32_t packed = 0;
@@ -477,7 +511,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
           for (int by = 0; by < 4; ++by) {
             const bool ok = c * KCHUNK + g * 16 + wd * 4 + by < L;
             const int code = ok ? (int)(((uint32_t)sv[wd] >> (8 * by)) & 0xff) : Mrow[t];
-            const uint32_t av = arow[-32 * code];
+            const uint32_t av = arow[t][-128 * code];
             packed |= (ok ? av : 0x80u) << (8 * by);  // a = 0 for padded keys
           }
           af[t][wd] = (int)packed;
@@ -492,22 +526,23 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
       v4i v[NP];
       v4i s;
     };
-    auto load_part = [&](int c, int h, VPart& dst) {
-      const int8_t* src = VTh + (size_t)c * CH + h * NP * 1024 + vt_off;
+    auto load_part = [&](int c, int hp, VPart& dst) {
+      const int8_t* src = VTh + (size_t)c * CH + hp * NP * 1024 + vt_off;
 #pragma unroll
       for (int k = 0; k < NP; ++k) dst.v[k] = *(const v4i*)(src + k * 1024);
-      dst.s = *(const v4i*)(vs + ((size_t)c * 16 + col) * NT + h * NP);
+      dst.s = *(const v4i*)(vs + ((size_t)c * 16 + col) * NT + hp * NP);
     };
     int vacc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) vacc[nt] = 0;
-    v4i af[2];
-    auto mma_part = [&](const int h, const VPart& vp) {
+    v4i af[NTL];
+    auto mma_part = [&](const int hp, const VPart& vp) {
 #pragma unroll
       for (int k = 0; k < NP; ++k) {
-        acc[0][h * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0], vp.v[k], acc[0][h * NP + k], 0, 0, 0);
-        acc[1][h * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[1], vp.v[k], acc[1][h * NP + k], 0, 0, 0);
-        vacc[h * NP + k] += vp.s[k];
+#pragma unroll
+        for (int t = 0; t < NTL; ++t)
+          acc[t][hp * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[t], vp.v[k], acc[t][hp * NP + k], 0, 0, 0);
+        vacc[hp * NP + k] += vp.s[k];
       }
     };
     auto codes = [&](int c) {
@@ -545,7 +580,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[t][nt][i] += 128 * vacc[nt];
   }
@@ -558,7 +593,7 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   };
   if (KSPLIT == 1) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < NTL; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int qi = q0 + 16 * t + 4 * g + i;
@@ -568,14 +603,14 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
         for (int nt = 0; nt < NT; ++nt) out[nt * 16] = (int8_t)(qi < L ? requant_o(acc[t][nt][i]) : 0);
       }
   } else {
-    // partial sums of one query set: [32 rows][RSTRIDE] int32; the padding puts
-    // rows 4 apart into different banks.  The first key split stores, the others
-    // add with LDS atomics (exact, order-free).
-    int32_t* rq = red + (size_t)qset * 32 * RSTRIDE;
+    // partial sums of one query set: [ROWS][RSTRIDE] int32; the padding puts rows 4
+    // apart into different banks.  The first key split stores, the others add with
+    // LDS atomics (exact, order-free).
+    int32_t* rq = red + (size_t)qset * ROWS * RSTRIDE;
     __syncthreads();  // every wave is done with the score rows
     if (kpart == 0) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -584,16 +619,16 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     __syncthreads();
     if (kpart != 0 && active) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < NTL; ++t)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) atomicAdd(&rq[(16 * t + 4 * g + i) * RSTRIDE + nt * 16 + col], acc[t][nt][i]);
     }
     __syncthreads();
-    // the KSPLIT waves of the set share its 32 rows: items of 4 channels, row-major
+    // the KSPLIT waves of the set share its rows: items of 4 channels, row-major
     constexpr int IPR = DK / 4;  // items per row
-    for (int it = kpart * 64 + lane; it < 32 * IPR; it += 64 * KSPLIT) {
+    for (int it = kpart * 64 + lane; it < ROWS * IPR; it += 64 * KSPLIT) {
       const int rr = it / IPR;
       const int ch = (it % IPR) * 4;
       const int qi = q0 + rr;
@@ -700,54 +735,66 @@ __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-size_t attn_lds_bytes(int DK, int ksplit, int T_al) {
-  const int wgq = 32 * ATTN_WAVES / ksplit;
+size_t attn_lds_bytes(int DK, int ksplit, int ntl, int T_al) {
+  const int rows = 16 * ntl, nqs = ATTN_WAVES / ksplit;
+  const int wgq = rows * nqs;
   const size_t s_bytes = (size_t)wgq * (T_al + SCORE_PAD);
-  const size_t red = ksplit > 1 ? (size_t)(ATTN_WAVES / ksplit) * 32 * (DK + 4) * 4 : 0;
+  const size_t red = ksplit > 1 ? (size_t)nqs * rows * (DK + 4) * 4 : 0;
   const size_t big = ((s_bytes > red ? s_bytes : red) + 15) & ~(size_t)15;
-  return big + (size_t)(wgq / 32) * TAB_BLOCK * 4 + 256 * 4 + 3 * 32 * ATTN_WAVES * 4;
+  return big + (size_t)TAB_DW * 4 + 256 * 4 + 2 * (size_t)rows * ATTN_WAVES * 4 + (size_t)wgq * 4;
 }
 
-// Key splits the kernel is built for (divisors of ATTN_WAVES; smaller splits put
-// more query rows in LDS than fit).
-static const int kKeySplits[] = {4, 8};
+// Workgroup shapes the kernel is built for: (key splits, 16-query tiles per wave).
+static const AttnCfg kAttnCfgs[] = {{4, 2}, {8, 2}, {8, 3}};
+constexpr size_t kLdsBudget = 160 * 1024;
+constexpr int kNumCUs = 256;
 
-// Key split per workgroup: the fewest splits whose workgroup fits in LDS and that
-// still gives every CU a workgroup; otherwise the largest split that fits (most
-// workgroups); 0 if none fits.
-int attn_key_split(int DK, int T_al, long bh_count, int T) {
-  const size_t budget = 160 * 1024;
-  int best = 0;
-  for (int ks : kKeySplits) {
-    if (attn_lds_bytes(DK, ks, T_al) > budget) continue;
-    const int wgq = 32 * ATTN_WAVES / ks;
+// Shape of one launch: among the shapes whose workgroup fits in LDS, the one with the
+// least estimated time.  A CU holds one workgroup (eight waves of more than 128
+// VGPRs), so the time is the rounds of workgroups over the CUs times the time of one
+// workgroup, modelled per key of a wave's share as 125 cycles for the K, P and V
+// streams (the same for any number of query tiles) plus 29 per 16-query tile (score
+// post-processing, exp sums, code lookups, combine), as measured on the long-form
+// workload.  {0, 0} if no shape fits.
+AttnCfg attn_config(int DK, int T_al, long bh_count, int T) {
+  AttnCfg best{0, 0};
+  double best_cost = 0.0;
+  for (const AttnCfg& c : kAttnCfgs) {
+    if (attn_lds_bytes(DK, c.ksplit, c.ntl, T_al) > kLdsBudget) continue;
+    const int wgq = 16 * c.ntl * (ATTN_WAVES / c.ksplit);
     const long wgs = bh_count * ((T + wgq - 1) / wgq);
-    if (wgs >= 256) return ks;
-    best = ks;
+    const long rounds = (wgs + kNumCUs - 1) / kNumCUs;
+    const double cost = (double)rounds * ((double)T / c.ksplit) * (125.0 + 29.0 * c.ntl);
+    if (best.ksplit == 0 || cost < best_cost) {
+      best = c;
+      best_cost = cost;
+    }
   }
   return best;
 }
 
-template <int DK, int KS, bool WIDE>
+template <int DK, int KS, int NTL, bool WIDE>
 static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int T_al, hipStream_t st,
                                   const LaunchEv& ev) {
-  const size_t shmem = attn_lds_bytes(DK, KS, T_al);
-  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS, WIDE>,
+  const size_t shmem = attn_lds_bytes(DK, KS, NTL, T_al);
+  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS, NTL, WIDE>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
   if (e != hipSuccess) return e;
-  const int wgq = 32 * ATTN_WAVES / KS;
+  const int wgq = 16 * NTL * (ATTN_WAVES / KS);
   AttnArgs a2 = args;
   a2.nqb = (T + wgq - 1) / wgq;
   a2.xcd_group = (B * H) % 8 == 0;
   dim3 grid(a2.nqb * B * H);
-  return launch_kernel(relpos_attn_core<DK, KS, WIDE>, grid, dim3(64 * ATTN_WAVES), (uint32_t)shmem, st, ev, a2);
+  return launch_kernel(relpos_attn_core<DK, KS, NTL, WIDE>, grid, dim3(64 * ATTN_WAVES), (uint32_t)shmem, st, ev,
+                       a2);
 }
 
 template <int DK, bool WIDE>
 static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st, const LaunchEv& ev) {
-  const int ks = attn_key_split(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
-  if (ks == 4) return launch_attn_cfg<DK, 4, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
-  if (ks == 8) return launch_attn_cfg<DK, 8, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
+  const AttnCfg c = attn_config(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
+  if (c.ksplit == 4 && c.ntl == 2) return launch_attn_cfg<DK, 4, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
+  if (c.ksplit == 8 && c.ntl == 2) return launch_attn_cfg<DK, 8, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
+  if (c.ksplit == 8 && c.ntl == 3) return launch_attn_cfg<DK, 8, 3, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
   return hipErrorInvalidValue;
 }
 

@@ -107,8 +107,11 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
                             hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev = {});
-// Key split of the attention core for a run (0 when T_al does not fit LDS).
-int attn_key_split(int DK, int T_al, long bh_count, int T);
+// Workgroup shape of the attention core for a run ({0, 0} when T_al does not fit LDS).
+struct AttnCfg {
+  int ksplit, ntl;  // key splits per query set, 16-query tiles per wave
+};
+AttnCfg attn_config(int DK, int T_al, long bh_count, int T);
 
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st);

@@ -82,6 +82,11 @@ SHAPES = [
     (100, 384, 3, 2, [100, 71]),
     (129, 256, 2, 1, [97]),
     (200, 512, 4, 3, [200, 131, 64]),
+    # longer rows: 48-query workgroups (the last one past T_al re-reads Q rows), d_k 128 and 64
+    (1600, 512, 4, 1, None),
+    (1500, 256, 4, 2, [1500, 1111]),
+    # four key splits per query set (64-query workgroups)
+    (1000, 256, 4, 4, [1000, 999, 500, 1]),
 ]
 
 
