@@ -41,6 +41,7 @@
 // 3) read different copies, so a lookup is one multiply-add and one conflict-free
 // LDS read.
 #include <type_traits>
+#include <vector>
 
 #include "ipk_internal.h"
 
@@ -54,8 +55,11 @@ struct AttnArgs {
   int8_t* ctx;
   Lengths lens;
   int T, T_al, H, d, p_rows, p_base;
-  int nqb;        // query blocks per (utterance, head)
+  int nqb;        // query blocks per (utterance, head) of the first segment
   int xcd_group;  // keep each (utterance, head) on one XCD
+  // second segment of a two-shape grid: blocks from seg2_block on cover the queries
+  // from seg2_q0 on, nqb2 blocks per (utterance, head), with the second shape
+  int seg2_block, seg2_q0, nqb2;
   // fused score: narrow path
   int32_t mc24, mp24, bias32, post_shift;
   // fused score: wide path (multipliers scaled by 2^-shift_s)
@@ -94,9 +98,11 @@ constexpr int ATTN_WAVES = 8;  // waves per workgroup (two per SIMD)
 template <int S>
 using Phase = std::integral_constant<int, S>;
 
+// One workgroup of the core: block `lin` of a segment of nqb query blocks per
+// (utterance, head) that starts at query q_base.
 template <int DK, int KSPLIT, int NTL, bool WIDE>
-__global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) {
-  extern __shared__ __align__(16) unsigned char smem[];
+__device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* smem, const int lin, const int nqb,
+                                           const int q_base) {
   constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets per workgroup
   constexpr int ROWS = 16 * NTL;            // queries per set: NTL 16-query MFMA tiles
   constexpr int WGQ = ROWS * NQS;           // queries per workgroup
@@ -112,19 +118,16 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   // pairs divide evenly, every workgroup of one pair is placed on the same XCD so that
   // its K, P and V stay in that XCD's L2.
   int qb, bhi;
-  {
-    const int lin = blockIdx.x;
-    if (a.xcd_group) {
-      const int x = lin & 7, k = lin >> 3, slot = k / a.nqb;
-      qb = k - slot * a.nqb;
-      bhi = x + 8 * slot;
-    } else {
-      qb = lin % a.nqb;
-      bhi = lin / a.nqb;
-    }
+  if (a.xcd_group) {
+    const int x = lin & 7, k = lin >> 3, slot = k / nqb;
+    qb = k - slot * nqb;
+    bhi = x + 8 * slot;
+  } else {
+    qb = lin % nqb;
+    bhi = lin / nqb;
   }
   const int b = bhi / a.H, h = bhi - (bhi / a.H) * a.H;
-  const int wg_q0 = qb * WGQ;
+  const int wg_q0 = q_base + qb * WGQ;
   const int q0 = wg_q0 + ROWS * qset;  // first query of this wave
   const int L = a.lens.len[b];
   const int T = a.T, T_al = a.T_al;
@@ -644,6 +647,22 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
   }
 }
 
+// The core kernel: one workgroup shape (NTL2 == 0), or two shapes in one grid, the
+// first one's blocks ahead of the second one's, so that the second shape fills what
+// the first leaves of the last round (workgroups start in block order).
+template <int DK, int KS1, int NTL1, int KS2, int NTL2, bool WIDE>
+__global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  if constexpr (NTL2 == 0) {
+    attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.nqb, 0);
+  } else {
+    if ((int)blockIdx.x < a.seg2_block)
+      attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.nqb, 0);
+    else
+      attn_block<DK, KS2, NTL2, WIDE>(a, smem, blockIdx.x - a.seg2_block, a.nqb2, a.seg2_q0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Rank-1 bias terms u.K_j and v.P_r, and sums of V over each 64-key chunk.
 struct BiasArgs {
@@ -749,52 +768,108 @@ static const AttnCfg kAttnCfgs[] = {{4, 2}, {8, 2}, {8, 3}};
 constexpr size_t kLdsBudget = 160 * 1024;
 constexpr int kNumCUs = 256;
 
-// Shape of one launch: among the shapes whose workgroup fits in LDS, the one with the
-// least estimated time.  A CU holds one workgroup (eight waves of more than 128
-// VGPRs), so the time is the rounds of workgroups over the CUs times the time of one
-// workgroup, modelled per key of a wave's share as 125 cycles for the K, P and V
-// streams (the same for any number of query tiles) plus 29 per 16-query tile (score
-// post-processing, exp sums, code lookups, combine), as measured on the long-form
-// workload.  {0, 0} if no shape fits.
-AttnCfg attn_config(int DK, int T_al, long bh_count, int T) {
-  AttnCfg best{0, 0};
-  double best_cost = 0.0;
-  for (const AttnCfg& c : kAttnCfgs) {
-    if (attn_lds_bytes(DK, c.ksplit, c.ntl, T_al) > kLdsBudget) continue;
-    const int wgq = 16 * c.ntl * (ATTN_WAVES / c.ksplit);
-    const long wgs = bh_count * ((T + wgq - 1) / wgq);
-    const long rounds = (wgs + kNumCUs - 1) / kNumCUs;
-    const double cost = (double)rounds * ((double)T / c.ksplit) * (125.0 + 29.0 * c.ntl);
-    if (best.ksplit == 0 || cost < best_cost) {
-      best = c;
-      best_cost = cost;
+static int wgq_of(const AttnCfg& c) { return 16 * c.ntl * (ATTN_WAVES / c.ksplit); }
+static bool fits(const AttnCfg& c, int DK, int T_al) { return attn_lds_bytes(DK, c.ksplit, c.ntl, T_al) <= kLdsBudget; }
+
+// Time of one workgroup, modelled per key of a wave's share as 125 cycles for the K, P
+// and V streams (the same for any number of query tiles) plus 29 per 16-query tile
+// (score post-processing, exp sums, code lookups, combine), as measured on the
+// long-form workload.
+static double wg_cost(const AttnCfg& c, int T) { return ((double)T / c.ksplit) * (125.0 + 29.0 * c.ntl); }
+
+// Finishing time of groups of workgroups (count[g] of cost[g] each) started in order on
+// the CUs, one workgroup per CU (eight waves of more than 128 VGPRs), each CU taking the
+// next workgroup when it is free.  CUs are kept in buckets of equal free time.
+static double makespan(const long* count, const double* cost, int ng) {
+  struct Bucket {
+    double t;
+    long n;
+  };
+  std::vector<Bucket> b{{0.0, (long)kNumCUs}};  // ascending t
+  auto insert = [&](Bucket x) {
+    size_t i = 0;
+    while (i < b.size() && b[i].t < x.t) ++i;
+    if (i < b.size() && b[i].t == x.t)
+      b[i].n += x.n;
+    else
+      b.insert(b.begin() + i, x);
+  };
+  for (int g = 0; g < ng; ++g) {
+    long left = count[g];
+    while (left > 0) {
+      Bucket e = b.front();
+      b.erase(b.begin());
+      const long take = left < e.n ? left : e.n;
+      left -= take;
+      if (e.n > take) b.insert(b.begin(), Bucket{e.t, e.n - take});
+      insert(Bucket{e.t + cost[g], take});
+    }
+  }
+  return b.back().t;
+}
+
+// Plan of one launch: a single workgroup shape, or 48-query workgroups for whole
+// rounds followed by 32-query ones for the remaining queries, whichever finishes
+// first by the model above.  c1.ksplit == 0 if no shape fits in LDS.
+AttnPlan attn_plan(int DK, int T_al, long bh_count, int T) {
+  AttnPlan best{};
+  double best_t = 0.0;
+  auto consider = [&](const AttnPlan& p) {
+    const long cnt[2] = {bh_count * p.nqb1, bh_count * p.nqb2};
+    const double cst[2] = {wg_cost(p.c1, T), p.c2.ksplit ? wg_cost(p.c2, T) : 0.0};
+    const double t = makespan(cnt, cst, p.c2.ksplit ? 2 : 1);
+    if (best.c1.ksplit == 0 || t < best_t) {
+      best = p;
+      best_t = t;
+    }
+  };
+  for (const AttnCfg& c : kAttnCfgs)
+    if (fits(c, DK, T_al)) consider(AttnPlan{c, (T + wgq_of(c) - 1) / wgq_of(c), AttnCfg{0, 0}, 0});
+  const AttnCfg c1{8, 3}, c2{8, 2};
+  if (fits(c1, DK, T_al) && fits(c2, DK, T_al)) {
+    const int per_round = (int)(kNumCUs / bh_count);  // blocks per (utterance, head) in one round
+    const int n1_all = (T + wgq_of(c1) - 1) / wgq_of(c1);
+    for (int n1 = per_round; n1 > 0 && n1 < n1_all; n1 += per_round) {
+      const int rest = T - n1 * wgq_of(c1);
+      consider(AttnPlan{c1, n1, c2, (rest + wgq_of(c2) - 1) / wgq_of(c2)});
     }
   }
   return best;
 }
 
-template <int DK, int KS, int NTL, bool WIDE>
-static hipError_t launch_attn_cfg(const AttnArgs& args, int B, int H, int T, int T_al, hipStream_t st,
-                                  const LaunchEv& ev) {
-  const size_t shmem = attn_lds_bytes(DK, KS, NTL, T_al);
-  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS, NTL, WIDE>,
+template <int DK, int KS1, int NTL1, int KS2, int NTL2, bool WIDE>
+static hipError_t launch_attn_plan(const AttnArgs& args, const AttnPlan& p, int B, int H, int T_al, hipStream_t st,
+                                   const LaunchEv& ev) {
+  size_t shmem = attn_lds_bytes(DK, KS1, NTL1, T_al);
+  if (NTL2) {
+    const size_t s2 = attn_lds_bytes(DK, KS2, NTL2, T_al);
+    shmem = s2 > shmem ? s2 : shmem;
+  }
+  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS1, NTL1, KS2, NTL2, WIDE>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
   if (e != hipSuccess) return e;
-  const int wgq = 16 * NTL * (ATTN_WAVES / KS);
   AttnArgs a2 = args;
-  a2.nqb = (T + wgq - 1) / wgq;
+  a2.nqb = p.nqb1;
   a2.xcd_group = (B * H) % 8 == 0;
-  dim3 grid(a2.nqb * B * H);
-  return launch_kernel(relpos_attn_core<DK, KS, NTL, WIDE>, grid, dim3(64 * ATTN_WAVES), (uint32_t)shmem, st, ev,
-                       a2);
+  a2.seg2_block = p.nqb1 * B * H;
+  a2.seg2_q0 = p.nqb1 * wgq_of(p.c1);
+  a2.nqb2 = p.nqb2;
+  dim3 grid((p.nqb1 + p.nqb2) * B * H);
+  return launch_kernel(relpos_attn_core<DK, KS1, NTL1, KS2, NTL2, WIDE>, grid, dim3(64 * ATTN_WAVES),
+                       (uint32_t)shmem, st, ev, a2);
 }
 
 template <int DK, bool WIDE>
 static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStream_t st, const LaunchEv& ev) {
-  const AttnCfg c = attn_config(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
-  if (c.ksplit == 4 && c.ntl == 2) return launch_attn_cfg<DK, 4, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
-  if (c.ksplit == 8 && c.ntl == 2) return launch_attn_cfg<DK, 8, 2, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
-  if (c.ksplit == 8 && c.ntl == 3) return launch_attn_cfg<DK, 8, 3, WIDE>(a, rs.B, rs.H, rs.T, rs.T_al, st, ev);
+  const AttnPlan p = attn_plan(DK, rs.T_al, (long)rs.B * rs.H, rs.T);
+  auto is = [](const AttnCfg& c, int ks, int ntl) { return c.ksplit == ks && c.ntl == ntl; };
+  if (p.c2.ksplit == 0) {
+    if (is(p.c1, 4, 2)) return launch_attn_plan<DK, 4, 2, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
+    if (is(p.c1, 8, 2)) return launch_attn_plan<DK, 8, 2, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
+    if (is(p.c1, 8, 3)) return launch_attn_plan<DK, 8, 3, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
+  } else if (is(p.c1, 8, 3) && is(p.c2, 8, 2)) {
+    return launch_attn_plan<DK, 8, 3, 8, 2, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
+  }
   return hipErrorInvalidValue;
 }
 

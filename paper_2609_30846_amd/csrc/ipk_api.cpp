@@ -133,7 +133,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   *out = nullptr;
   int st = validate_desc(desc);
   if (st != IPK_OK) return st;
-  if (attn_config(desc->d_k, t_aligned(desc->max_T), 1, desc->max_T).ksplit == 0)
+  if (attn_plan(desc->d_k, t_aligned(desc->max_T), 1, desc->max_T).c1.ksplit == 0)
     return fail(IPK_ERR_UNSUPPORTED, "max_T=%d does not fit the on-chip score rows", desc->max_T);
 
   ipk_relpos_attn* h = new (std::nothrow) ipk_relpos_attn();

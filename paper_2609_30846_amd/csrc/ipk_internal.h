@@ -107,11 +107,19 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
                             hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev = {});
-// Workgroup shape of the attention core for a run ({0, 0} when T_al does not fit LDS).
+// Workgroup shapes of the attention core for a run: the first shape's nqb1 query
+// blocks per (utterance, head), then (c2.ksplit != 0) the second shape's nqb2 blocks
+// for the remaining queries.  c1.ksplit == 0 when T_al does not fit LDS.
 struct AttnCfg {
   int ksplit, ntl;  // key splits per query set, 16-query tiles per wave
 };
-AttnCfg attn_config(int DK, int T_al, long bh_count, int T);
+struct AttnPlan {
+  AttnCfg c1;
+  int nqb1;
+  AttnCfg c2;
+  int nqb2;
+};
+AttnPlan attn_plan(int DK, int T_al, long bh_count, int T);
 
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st);

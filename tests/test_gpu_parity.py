@@ -82,11 +82,17 @@ SHAPES = [
     (100, 384, 3, 2, [100, 71]),
     (129, 256, 2, 1, [97]),
     (200, 512, 4, 3, [200, 131, 64]),
-    # longer rows: 48-query workgroups (the last one past T_al re-reads Q rows), d_k 128 and 64
+    # longer rows, one workgroup shape per launch: 32-query workgroups (d_k 128),
+    # 48-query workgroups (d_k 64), 48-query ones whose last block reaches past T_al
+    # (it re-reads the last Q rows), and four key splits per query set (64 queries)
     (1600, 512, 4, 1, None),
     (1500, 256, 4, 2, [1500, 1111]),
-    # four key splits per query set (64-query workgroups)
+    (1060, 128, 2, 4, [1060, 1059, 530, 64]),
     (1000, 256, 4, 4, [1000, 999, 500, 1]),
+    # two shapes in one grid: 48-query workgroups for one round, then 32-query ones
+    # (d_k 64; d_k 128 with the last block past T_al)
+    (1028, 256, 4, 4, [1028, 1000, 517, 3]),
+    (1396, 512, 4, 3, [1396, 1390, 700]),
 ]
 
 
