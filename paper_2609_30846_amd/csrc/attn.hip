@@ -164,19 +164,6 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
   const int frag_off = col * 64 + g * 16;
 
-  // I-BERT integer exp of every score distance d = M - s in [0, 254]: once, and
-  // in 32 per-bank copies (copy (d + c) % 32 of the pass is written by lane d,
-  // which keeps the writes free of bank conflicts)
-  {
-    const int dd = tid & 255;
-    const uint32_t e = dd < 255 ? iexp_int(dd, a.q_ln2, a.q_b, a.q_c) : 0u;
-    if (tid < 256) etab[dd] = e;
-    for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
-#pragma unroll
-      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e;
-    }
-  }
-
   constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
 
@@ -356,6 +343,20 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       ph = ph + 1 == NTL ? 0 : ph + 1;
     }
   }
+  // I-BERT integer exp of every score distance d = M - s in [0, 254] (first read in
+  // phase 2, so waves that finish phase 1 early fill it while the others score): once, and
+  // in 32 per-bank copies (copy (d + c) % 32 of the pass is written by lane d,
+  // which keeps the writes free of bank conflicts)
+  {
+    const int dd = tid & 255;
+    const uint32_t e = dd < 255 ? iexp_int(dd, a.q_ln2, a.q_b, a.q_c) : 0u;
+    if (tid < 256) etab[dd] = e;
+    for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e;
+    }
+  }
+
   // row max over the 16 key lanes of each row group
 #pragma unroll
   for (int t = 0; t < NTL; ++t)
@@ -441,22 +442,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     for (int t = 0; t < NTL; ++t) ssum[w * ROWS + 16 * t + col] = sum[t];
   }
   __syncthreads();
-  if (kpart == 0 && g == 0) {
+  // F = floor(2^32 / sum), one row per thread.  The float64 quotient is correctly
+  // rounded, and 2^32 / sum lies at least 1 / sum below the next integer while its
+  // rounding error is at most 2^32 / sum * 2^-53, so truncating it gives the floor.
+  if (tid < WGQ) {
+    const int qs = tid / ROWS, rr = tid - qs * ROWS;
+    uint32_t tot = 0;
 #pragma unroll
-    for (int t = 0; t < NTL; ++t) {
-      uint32_t tot = 0;
-#pragma unroll
-      for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qset * KSPLIT + k2) * ROWS + 16 * t + col];
-      sF[ROWS * qset + 16 * t + col] = tot ? (uint32_t)(((uint64_t)1 << 32) / tot) : 0u;
-    }
+    for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qs * KSPLIT + k2) * ROWS + rr];
+    sF[tid] = tot ? (uint32_t)(4294967296.0 / (double)tot) : 0u;
   }
   __syncthreads();
   // softmax code tables (over the exp copies, which phase 2 has finished with): the
   // dword of distance d and bank rr + 16 c (c = 0, 1: two copies) holds in byte tt
   // min(floor(e(d) F_r / 2^24), 255) ^ 0x80 of row r = 16 tt + rr, i.e. a - 128.
-  // floor(e F / 2^24) is the high word of (e 2^8) F (e < 2^24).
-  for (int idx = tid; idx < TAB_DW; idx += 64 * ATTN_WAVES) {
-    const int dd = idx >> 5, rr = idx & 15;
+  // floor(e F / 2^24) is the high word of (e 2^8) F (e < 2^24).  Each dword is
+  // computed once and written to both copies.
+  for (int idx = tid; idx < TAB_DW / 2; idx += 64 * ATTN_WAVES) {
+    const int dd = idx >> 4, rr = idx & 15;
     const uint32_t e8 = etab[dd] << 8;
     uint32_t packed = 0;
 #pragma unroll
@@ -464,7 +467,8 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       const uint32_t v = __umulhi(e8, sF[16 * tt + rr]);
       packed |= ((v > 255u ? 255u : v) ^ 0x80u) << (8 * tt);
     }
-    tab[idx] = packed;
+    tab[dd * 32 + rr] = packed;
+    tab[dd * 32 + rr + 16] = packed;
   }
   __syncthreads();
 
