@@ -143,9 +143,10 @@ def main():
     ms_step = ms_total / args.steps
 
     # stage pass: K more steps with per-kernel HIP events recorded by the library on
-    # the launch stream (event i at the start of kernel i, event 4 at the end of the
-    # last); stage_ms and the roofline's kernel duration come from it
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # the launch stream (event i at the start of kernel i, the last one at the end of
+    # the last kernel); stage_ms and the roofline's kernel duration come from it
+    nst = ipk.NUM_STAGES
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(args.steps)]
     for row in evs:
         for e in row:
             e.record(stream)
@@ -155,10 +156,10 @@ def main():
         mod(x, pe, lengths=lengths, y=y, stream=stream)
     torch.cuda.synchronize()
 
-    stage_names = ["projections", "bias_terms", "attention", "out_projection"]
-    stage_ms = np.zeros(4)
+    stage_names = ["projections", "attention", "out_projection"]
+    stage_ms = np.zeros(nst)
     for row in evs:
-        for i in range(4):
+        for i in range(nst):
             stage_ms[i] += row[i].elapsed_time(row[i + 1])
     stage_ms /= args.steps
 
@@ -166,7 +167,7 @@ def main():
     ops = 2 * (proj + pos + attn)
     tops = ops / (ms_step * 1e-3) / 1e12
     frames = float(np.sum(lengths)) / (ms_step * 1e-3)
-    attn_tops = 2 * attn / (stage_ms[2] * 1e-3) / 1e12
+    attn_tops = 2 * attn / (stage_ms[1] * 1e-3) / 1e12
 
     rec = {
         "metric": METRIC,

@@ -143,15 +143,17 @@ enum { IPK_INTER_Q = 0, IPK_INTER_K = 1, IPK_INTER_V = 2, IPK_INTER_P = 3, IPK_I
 int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
 
 /*
- * Stage timing for profiling: the NEXT run on `h` records the five caller-created
- * HIP events events[0..4] (hipEvent_t, created with timing enabled) on its stream:
- * events[0..3] when the Q|K|V and position projections, the bias kernel, the
- * attention core and the output projection start, events[4] when the output
- * projection ends.  The events are carried by the kernel dispatches themselves,
- * so recording them adds no work to the stream.  The events are used once; later
- * runs record nothing until this is called again.  events = NULL clears a pending
- * request.  Errors: IPK_ERR_INVALID_ARG (null handle, or a null entry in events).
+ * Stage timing for profiling: the NEXT run on `h` records the IPK_NUM_STAGES + 1
+ * caller-created HIP events events[0..3] (hipEvent_t, created with timing enabled)
+ * on its stream: events[0..2] when the three stages start (the Q|K|V and position
+ * projections, which also produce the rank-1 terms u.K_j, v.P_r and the V sums;
+ * the attention core; the output projection), events[3] when the output projection
+ * ends.  The events are carried by the kernel dispatches themselves, so recording
+ * them adds no work to the stream.  The events are used once; later runs record
+ * nothing until this is called again.  events = NULL clears a pending request.
+ * Errors: IPK_ERR_INVALID_ARG (null handle, or a null entry in events).
  */
+enum { IPK_NUM_STAGES = 3 };
 int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
 
 /* Human-readable name of a status code (static storage). */

@@ -668,68 +668,6 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
 }
 
 // ---------------------------------------------------------------------------
-// Rank-1 bias terms u.K_j and v.P_r, and sums of V over each 64-key chunk.
-struct BiasArgs {
-  const int8_t *k, *vt, *p, *u, *v;
-  int32_t *bu, *bv, *vsum;
-  int BH, H, T_al, DK, p_rows;
-};
-
-// u . row for a row stored fragment-major: DK/64 slabs of 64 contiguous bytes, 1 KB apart
-__device__ __forceinline__ int dot_frag_row(const int8_t* u, const int8_t* row, int DK) {
-  int acc = 0;
-  for (int s = 0; s < DK / 64; ++s)
-    for (int i = 0; i < 64; i += 16) {
-      const v4i xa = *(const v4i*)(u + s * 64 + i), ya = *(const v4i*)(row + s * 1024 + i);
-#pragma unroll
-      for (int wd = 0; wd < 4; ++wd) acc = __builtin_amdgcn_sdot4(xa[wd], ya[wd], acc, false);
-    }
-  return acc;
-}
-
-__global__ __launch_bounds__(256) void bias_terms(BiasArgs a) {
-  const long n_bu = (long)a.BH * a.T_al;
-  const long n_bv = (long)a.H * a.p_rows;
-  const long nch = a.T_al / KCHUNK;
-  const long n_vs = (long)a.BH * a.DK * nch;
-  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < n_bu) {
-    const long bh = idx / a.T_al;
-    const int t = (int)(idx - bh * a.T_al);
-    const int h = (int)(bh % a.H);
-    a.bu[idx] = dot_frag_row(a.u + (size_t)h * a.DK, a.k + bh * a.T_al * a.DK + frag_index(t, 0, a.DK), a.DK);
-    return;
-  }
-  idx -= n_bu;
-  if (idx < n_bv) {
-    const int h = (int)(idx / a.p_rows);
-    const int r = (int)(idx - (long)h * a.p_rows);
-    const int val = dot_frag_row(a.v + (size_t)h * a.DK, a.p + (size_t)h * a.p_rows * a.DK + frag_index(r, 0, a.DK), a.DK);
-    a.bv[idx] = val;
-    return;
-  }
-  idx -= n_bv;
-  if (idx < n_vs) {
-    // thread per (bh, chunk, channel): channel fastest so stores coalesce
-    const long n = idx % a.DK;
-    const long c = (idx / a.DK) % nch;
-    const long bh = idx / (a.DK * nch);
-    const int8_t* row = a.vt + bh * a.T_al * a.DK + vt_index((int)c * KCHUNK, (int)n, a.DK);
-    const int ones = 0x01010101;
-    int acc = 0;
-#pragma unroll
-    for (int i = 0; i < KCHUNK; i += 16) {
-      const v4i x = *(const v4i*)(row + i);
-#pragma unroll
-      for (int wd = 0; wd < 4; ++wd) acc = __builtin_amdgcn_sdot4(x[wd], ones, acc, false);
-    }
-    // [bh][chunk][n % 16][n / 16]: a lane of the attention core reads its NT
-    // channels n % 16 + 16 k of one chunk with one or two 16-byte loads
-    a.vsum[((bh * nch + c) * 16 + n % 16) * (a.DK / 16) + n / 16] = acc;
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Copies a workspace tensor back to the documented [B][T][d] / [2T-1][d] layouts.
 struct GatherArgs {
   const int8_t* src;
@@ -909,27 +847,6 @@ hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspa
   if (rs.DK == 128) return sc.fs_wide ? launch_attn_dk<128, true>(a, rs, st, ev) : launch_attn_dk<128, false>(a, rs, st, ev);
   if (rs.DK == 64) return sc.fs_wide ? launch_attn_dk<64, true>(a, rs, st, ev) : launch_attn_dk<64, false>(a, rs, st, ev);
   return hipErrorInvalidValue;
-}
-
-hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspace& ws, const Lengths& lens,
-                             hipStream_t st, const LaunchEv& ev) {
-  (void)lens;
-  BiasArgs a{};
-  a.k = ws.k;
-  a.vt = ws.vt;
-  a.p = ws.p;
-  a.u = w.u;
-  a.v = w.v;
-  a.bu = ws.bu;
-  a.bv = ws.bv;
-  a.vsum = ws.vsum;
-  a.BH = rs.B * rs.H;
-  a.H = rs.H;
-  a.T_al = rs.T_al;
-  a.DK = rs.DK;
-  a.p_rows = p_rows(rs.T_al);
-  const long total = (long)a.BH * a.T_al + (long)a.H * a.p_rows + (long)a.BH * a.DK * (a.T_al / KCHUNK);
-  return launch_kernel(bias_terms, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, ev, a);
 }
 
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,

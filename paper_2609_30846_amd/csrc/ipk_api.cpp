@@ -27,7 +27,7 @@ struct ipk_relpos_attn {
   std::vector<void*> allocs;
   RunShape last;
   bool has_run;
-  hipEvent_t stage_ev[5];
+  hipEvent_t stage_ev[IPK_NUM_STAGES + 1];
   bool stages_pending;
 };
 
@@ -246,16 +246,16 @@ extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const 
   const bool rec = h->stages_pending;
   h->stages_pending = false;
   // stage events ride on the kernel dispatches: event i is stamped when kernel i
-  // starts, event 4 when the last kernel ends (no separate event packets)
-  LaunchEv ev[4];
+  // starts, event 3 when the last kernel ends (no separate event packets)
+  LaunchEv ev[3];
   if (rec) {
-    for (int i = 0; i < 4; ++i) ev[i].start = h->stage_ev[i];
-    ev[3].stop = h->stage_ev[4];
+    for (int i = 0; i < 3; ++i) ev[i].start = h->stage_ev[i];
+    ev[2].stop = h->stage_ev[3];
   }
+  // the projections also produce the rank-1 terms and the V sums the core reads
   hipError_t e = launch_projections(rs, h->w, h->ws, x, pos_table, st, ev[0]);
-  if (e == hipSuccess) e = launch_bias_terms(rs, h->w, h->ws, lens, st, ev[1]);
-  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st, ev[2]);
-  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st, ev[3]);
+  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st, ev[1]);
+  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st, ev[2]);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;
   h->has_run = true;
@@ -281,9 +281,9 @@ extern "C" int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* 
     h->stages_pending = false;
     return IPK_OK;
   }
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < IPK_NUM_STAGES + 1; ++i)
     if (!events[i]) return fail(IPK_ERR_INVALID_ARG, "events[%d] is NULL", i);
-  for (int i = 0; i < 5; ++i) h->stage_ev[i] = (hipEvent_t)events[i];
+  for (int i = 0; i < IPK_NUM_STAGES + 1; ++i) h->stage_ev[i] = (hipEvent_t)events[i];
   h->stages_pending = true;
   return IPK_OK;
 }

@@ -7,16 +7,19 @@
 //   q, k   int8  [B][H] fragment-major rows: row t, channel kk sits at
 //                frag_index(t, kk) = (t/16)*16*DK + (kk/64)*1024 + (t%16)*64 + kk%64
 //   vt     int8  [B][H] V transposed, chunk-major: key t, channel kk sits at
-//                vt_index(t, kk) = (t/64)*64*DK + kk*64 + t%64
+//                vt_index(t, kk) = (t/64)*64*DK + kk*64 + t%64; keys T .. T_al-1
+//                hold zeros
 //   p      int8  [H] fragment-major rows of the projected relative-position table;
 //                table row r is stored at row p_base + r, where p_base >= P_PADLO is
 //                chosen per run so that the table row j-i+T-1 of every 16-query by
 //                16-key tile starts a 16-row block.  The rows around the table keep
 //                every padded tile in bounds (their contents are never used).
 //   bu     int32 [B][H][T_al]       u . K_j  (rank-1 part of the content score)
-//   bv     int32 [H][P_ROWS]        v . P_r  (rank-1 part of the position score)
+//   bv     int32 [H][P_ROWS]        v . P_r  (rank-1 part of the position score; rows
+//                                   of the table only)
 //   vsum   int32 [B][H][T_al/64][16][DK/16] sums of V over each 64-key chunk; channel n
 //                                   at [n % 16][n / 16]
+//   (bu, bv and vsum are written by the projection GEMM's epilogue)
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
@@ -101,8 +104,6 @@ inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem,
 // Enqueue the kernels of one run; return the first HIP error.
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev = {});
-hipError_t launch_bias_terms(const RunShape& rs, const Weights& w, const Workspace& ws, const Lengths& lens,
-                             hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
                             hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,

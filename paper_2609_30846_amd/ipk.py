@@ -143,12 +143,17 @@ def ipk_relpos_attn_intermediate(h: int, which: int, dst, stream=None) -> None:
                                                _stream_ptr(stream)))
 
 
+NUM_STAGES = 3  # projections (with the rank-1 terms), attention core, output projection
+
+
 def ipk_relpos_attn_record_stages(h: int, events) -> None:
-    """``events``: five torch.cuda.Event(enable_timing=True), already recorded once."""
+    """``events``: NUM_STAGES + 1 torch.cuda.Event(enable_timing=True), already recorded once."""
     if events is None:
         _check(load().ipk_relpos_attn_record_stages(h, None))
         return
-    arr = (_vp * 5)(*[int(e.cuda_event) for e in events])
+    if len(events) != NUM_STAGES + 1:
+        raise ValueError(f"{NUM_STAGES + 1} events are needed, got {len(events)}")
+    arr = (_vp * (NUM_STAGES + 1))(*[int(e.cuda_event) for e in events])
     _check(load().ipk_relpos_attn_record_stages(h, arr))
 
 
