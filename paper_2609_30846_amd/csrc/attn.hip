@@ -51,7 +51,8 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 
 struct AttnArgs {
   const int8_t *q, *k, *vt, *p;
-  const int32_t *bu, *bv, *vsum;
+  const int8_t *u, *v;  // [H][d_k]
+  const int32_t* vsum;
   int8_t* ctx;
   Lengths lens;
   int T, T_al, H, d, p_rows, p_base;
@@ -157,8 +158,6 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int8_t* Kh = a.k + bh * T_al * DK;
   const int8_t* VTh = a.vt + bh * DK * T_al;
   const int8_t* Ph = a.p + (size_t)h * a.p_rows * DK;
-  const int32_t* bu = a.bu + bh * T_al;
-  const int32_t* bvh = a.bv + (size_t)h * a.p_rows;
   const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
   uint8_t* my_rows = sbuf + (size_t)(ROWS * qset) * srow;
   // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
@@ -207,20 +206,35 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     // table row of (query q0, key j0) is j0 - q0 + T - 1; tile t sits 16 t rows lower
     const int8_t* kptr = Kh + (size_t)j_begin * DK;
     const int8_t* pptr = Ph + (size_t)(a.p_base + j_begin - q0 + T - 1) * DK;
-    const int32_t* buptr = bu + j_begin;
-    // v.P_r of this lane's column (one int32 per table row), splatted into the MFMA seed
-    const int32_t* bvptr = bvh + (a.p_base + j_begin - q0 + T - 1);
-    auto splat = [](int bb) { return (v4i){bb, bb, bb, bb}; };
+    // The rank-1 terms of Eq. 8 come from MFMAs of a 16-row operand whose rows all
+    // equal u (v): their products with a K (P) fragment hold u.K_j (v.P_r) in every
+    // row, which is the accumulator seed the content (position) MFMAs need.  No load
+    // is spent on them.
+    v4i uf[NKS], vf[NKS];
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
+      uf[s] = *(const v4i*)(a.u + (size_t)h * DK + s * 64 + g * 16);
+      vf[s] = *(const v4i*)(a.v + (size_t)h * DK + s * 64 + g * 16);
+    }
+    auto rank1 = [&](const v4i* vec, const v4i* fr) {
+      v4i r = (v4i){0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) r = __builtin_amdgcn_mfma_i32_16x16x64_i8(vec[s], fr[s], r, 0, 0, 0);
+      return r;
+    };
 
     // Register rings over the step phase S = (step index) % NTL, all indices static:
-    //  pr[u], bvr[u]: tile 0's hi-window P fragment of the step with phase u; at
-    //                 phase S tile t uses slot (S - t) mod NTL (its window is tile
-    //                 0's window of t steps before)
-    //  kr[u], bur[u]: K fragment and u.K_j of the step with phase u (current, next)
-    //  gr[u][t]:      position MFMA results (hi windows) of the step with phase u;
-    //                 a step's lo windows are the previous step's hi windows
+    //  pr[u]:    tile 0's hi-window P fragment of the step with phase u; at phase S
+    //            tile t uses slot (S - t) mod NTL (its window is tile 0's window of t
+    //            steps before)
+    //  bvp[u]:   v.P_r of that fragment's column (the same in every row), computed
+    //            when the step that loads it is the current one
+    //  kr[u]:    K fragment of the step with phase u (current, next)
+    //  gr[u][t]: position MFMA results (hi windows) of the step with phase u; a
+    //            step's lo windows are the previous step's hi windows
     v4i pr[NTL][NKS], kr[NTL][NKS], gr[NTL][NTL];
-    int bvr[NTL], bur[NTL];
+    int bvp[NTL];
+    auto splat = [](int bb) { return (v4i){bb, bb, bb, bb}; };
     {
       // tile t's hi window of the first step: tile 0's window 16 t rows lower
 #pragma unroll
@@ -228,18 +242,19 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
         const int u = (NTL - t) % NTL;
 #pragma unroll
         for (int s = 0; s < NKS; ++s) pr[u][s] = *(const v4i*)(pptr - 16 * t * DK + frag + s * 1024);
-        bvr[u] = bvptr[(int)col - 16 * t];
       }
       // lo windows of the first step: tile t's lo window is tile (t + 1)'s hi window;
       // the last tile's lies one more window lower
       v4i plast[NKS];
 #pragma unroll
       for (int s = 0; s < NKS; ++s) plast[s] = *(const v4i*)(pptr - 16 * NTL * DK + frag + s * 1024);
-      const int bvlast = bvptr[(int)col - 16 * NTL];
+#pragma unroll
+      for (int t = 0; t < NTL; ++t) bvp[(NTL - t) % NTL] = rank1(vf, pr[(NTL - t) % NTL])[0];
+      const int bvlast = rank1(vf, plast)[0];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         const int u = (NTL - t - 1) % NTL;  // slot of tile (t + 1)'s hi window
-        v4i gacc = splat(t + 1 < NTL ? bvr[u] : bvlast);
+        v4i gacc = splat(t + 1 < NTL ? bvp[u] : bvlast);
 #pragma unroll
         for (int s = 0; s < NKS; ++s)
           gacc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], t + 1 < NTL ? pr[u][s] : plast[s], gacc, 0, 0, 0);
@@ -248,10 +263,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
 #pragma unroll
     for (int s = 0; s < NKS; ++s) kr[0][s] = *(const v4i*)(kptr + frag + s * 1024);
-    bur[0] = buptr[col];
 
     int j0 = j_begin;
-    // One 16-key step at phase S: fetches the next step's K, P and biases (the last
+    // One 16-key step at phase S: fetches the next step's K and P fragments (the last
     // step re-reads its own rows, in bounds), runs the content and position MFMAs of
     // every tile and turns them into score codes in LDS.
     auto step = [&](auto Sc, const bool masked) {
@@ -260,12 +274,15 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       const int adv = j0 + 16 < j_stop ? 16 : 0;
 #pragma unroll
       for (int s = 0; s < NKS; ++s) kr[SN][s] = *(const v4i*)(kptr + adv * DK + frag + s * 1024);
-      bur[SN] = buptr[adv + col];
+      // seeds: u.K_j of this step's keys (shared by the tiles) and v.P_r of the
+      // window loaded by the previous step (tile 0's; later tiles reuse older slots)
+      const v4i uk = rank1(uf, kr[S]);
+      bvp[S] = rank1(vf, pr[S])[0];
       v4i cs[NTL];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        cs[t] = (v4i){0, 0, 0, 0};
-        gr[S][t] = splat(bvr[(S + NTL - t) % NTL]);
+        cs[t] = uk;
+        gr[S][t] = splat(bvp[(S + NTL - t) % NTL]);
       }
 #pragma unroll
       for (int s = 0; s < NKS; ++s)
@@ -277,14 +294,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       // the last tile's window (slot SN) is consumed: it takes the next step's tile-0 window
 #pragma unroll
       for (int s = 0; s < NKS; ++s) pr[SN][s] = *(const v4i*)(pptr + adv * DK + frag + s * 1024);
-      bvr[SN] = bvptr[adv + col];
-      // rank-1 content term u.K_j folded into the addend: m_c (c0 + u.K_j) + rounding + code bias
-      int k1 = 0;
-      double k1d = 0.0;
-      if (WIDE)
-        k1d = __builtin_fma(a.mcd, (double)bur[S], 128.5);
-      else
-        k1 = __mul24(a.mc24, bur[S]) + a.bias32;
+      // cs holds c0 + u.K_j: the addend is the rounding and code bias alone
+      const int k1 = a.bias32;
+      const double k1d = 128.5;
       const bool key_ok = j0 + col < L;
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
@@ -320,8 +332,6 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       }
       kptr += 16 * DK;
       pptr += 16 * DK;
-      buptr += 16;
-      bvptr += 16;
       j0 += 16;
     };
     // NTL unmasked steps per iteration, so that every ring index stays static
@@ -815,15 +825,15 @@ static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStrea
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
-                            hipStream_t st, const LaunchEv& ev) {
+hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars& sc, const Workspace& ws,
+                            const Lengths& lens, hipStream_t st, const LaunchEv& ev) {
   AttnArgs a{};
   a.q = ws.q;
   a.k = ws.k;
   a.vt = ws.vt;
   a.p = ws.p;
-  a.bu = ws.bu;
-  a.bv = ws.bv;
+  a.u = w.u;
+  a.v = w.v;
   a.vsum = ws.vsum;
   a.ctx = ws.ctx;
   a.lens = lens;

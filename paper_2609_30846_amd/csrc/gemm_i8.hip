@@ -58,9 +58,7 @@ struct GemmArgs {
   int per_xcd;  // logical tiles dealt to each XCD
   int8_t *q, *k, *vt, *p, *y;
   int T_al, H, dk_shift, d, p_rows, p_base;  // d_k = 2^dk_shift
-  // rank-1 terms of the attention scores and the V sums, produced by the epilogue
-  const int8_t *u, *v;         // [H][d_k]
-  int32_t *bu, *bv, *vsum;     // u.K_j [B][H][T_al], v.P_r [H][P_ROWS], sums of V per 64-key chunk
+  int32_t* vsum;  // sums of V over each 64-key chunk, produced by the epilogue
 };
 
 constexpr int BK = 128;  // bytes of K per step
@@ -223,11 +221,9 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // its column, 16 bytes each.  A 32-channel sub-tile never straddles N, a head or the
   // Q/K/V boundary (N and d_k are multiples of 64), so its destination is uniform.
   //
-  // The same pass produces the rank-1 terms of Eq. 8 from the int8 values it stores:
-  // u.K_j and v.P_r (a wave's channels start at a head boundary, so the partial dot
-  // products of a head's sub-tiles add up in registers and the two half-waves finish
-  // them), and the sums of V over each 64-key chunk (a wave's WTM = 64 tokens are one
-  // chunk).  V^T is written up to T_al, so the padded keys hold zeros, as the sums do.
+  // The same pass sums the int8 V values it stores over each 64-key chunk (a wave's
+  // WTM = 64 tokens are one chunk; the two half-waves hold its two halves).  V^T is
+  // written up to T_al, so the padded keys hold zeros, as the sums do.
   const int col = lane & 31;
   const int tw0 = t0 + wm * WTM;
   const int dks = args.dk_shift, DK = 1 << dks, DKm = DK - 1;
@@ -242,9 +238,6 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
     const auto s2 = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);
     return (int)(s2[0] + s2[1]);
   };
-  int part[FM];  // this lane's share of u.K_j or v.P_r over the head's sub-tiles so far
-#pragma unroll
-  for (int j = 0; j < FM; ++j) part[j] = 0;
 #pragma unroll
   for (int i = 0; i < FN; ++i) {
     const int nl = wn * (TN / 2) + i * 32;  // first channel of this sub-tile, tile-local
@@ -253,25 +246,19 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
     int8_t* dst;
     int kk = 0;  // channel of the sub-tile's first row inside its head
     int hd = 0;  // its head
-    int rk = 0;  // rank-1 work: 1 u.K_j, 2 v.P_r, 3 sums of V
     if (mode == OUT_QKV) {
       const int which = (nb >= args.d) + (nb >= 2 * args.d);
       const int c = nb - which * args.d;
       hd = c >> dks;
       dst = (which == 0 ? args.q : which == 1 ? args.k : args.vt) + ((size_t)ub * args.H + hd) * head_bytes;
       kk = c & DKm;
-      rk = which == 1 ? 1 : which == 2 ? 3 : 0;
     } else if (mode == OUT_POS) {
       hd = nb >> dks;
       dst = args.p + ((size_t)hd * args.p_rows << dks);
       kk = nb & DKm;
-      rk = 2;
     } else {
       dst = args.y + (size_t)ub * rows * N + nb;
     }
-    // the 16 bytes of u or v that meet this lane's 16 channels
-    v4i uv = (v4i){0, 0, 0, 0};
-    if (rk == 1 || rk == 2) uv = *(const v4i*)((rk == 1 ? args.u : args.v) + (hd << dks) + kk + half * 16);
     int vpart = 0;  // this lane's share of the chunk's V sum of channel kk + col
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
@@ -311,30 +298,14 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
           else if (mode == OUT_POS) *(v4i*)(dst + frag_off(args.p_base + t, kk + half * 16)) = out;
           else *(v4i*)(dst + (size_t)t * N + half * 16) = out;
         }
-        if (rk == 1 || rk == 2) {
-#pragma unroll
-          for (int wd = 0; wd < 4; ++wd) part[j] = __builtin_amdgcn_sdot4(out[wd], uv[wd], part[j], false);
-        }
       }
     }
-    if (rk == 3) {
+    if (vwave) {
       // sum of V over the 64-key chunk tw0 / 64, channel kk + col: [chunk][n % 16][n / 16]
       const int tot = half_sum(vpart);
       if (half == 0 && tw0 < args.T_al) {
         const int n = kk + col, nch = args.T_al >> 6;
         args.vsum[((((size_t)ub * args.H + hd) * nch + (tw0 >> 6)) * 16 + (n & 15)) * (DK >> 4) + (n >> 4)] = tot;
-      }
-    } else if ((rk == 1 || rk == 2) && kk + 32 == DK) {
-      // the head's last sub-tile: u.K_j of token t, or v.P_r of table row t
-#pragma unroll
-      for (int j = 0; j < FM; ++j) {
-        const int tot = half_sum(part[j]);
-        part[j] = 0;
-        const int t = tw0 + j * 32 + col;
-        if (half == 0) {
-          if (rk == 1 && t < args.T_al) args.bu[((size_t)ub * args.H + hd) * args.T_al + t] = tot;
-          if (rk == 2 && t < rows) args.bv[(size_t)hd * args.p_rows + args.p_base + t] = tot;
-        }
       }
     }
   }
@@ -377,8 +348,6 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.d = rs.d;
   a.p_rows = p_rows(rs.T_al);
   a.p_base = rs.p_base;
-  a.bu = ws.bu;
-  a.bv = ws.bv;
   a.vsum = ws.vsum;
 }
 
@@ -393,11 +362,8 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
-  a.u = w.u;
-  a.v = w.v;
   constexpr int TN = 256, TM = 256, NWM = 4;
-  // the epilogue's rank-1 terms: a wave's tokens are one 64-key chunk and its
-  // channels whole heads
+  // the epilogue's V sums: a wave's tokens are one 64-key chunk
   static_assert(TM / NWM == KCHUNK && (TN / 2) % 128 == 0, "projection tile shape");
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);

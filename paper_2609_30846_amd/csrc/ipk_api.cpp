@@ -179,8 +179,6 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->ws.vt, Bm * H * DK * T_al));
   chk(dev_alloc(h, &h->ws.p, H * PR * DK));
   chk(dev_alloc(h, &h->ws.ctx, Bm * (size_t)h->max_T * d));
-  chk(dev_alloc(h, &h->ws.bu, Bm * H * T_al));
-  chk(dev_alloc(h, &h->ws.bv, H * PR));
   chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK) * DK));
   if (e != hipSuccess) {
     free_handle(h);
@@ -252,9 +250,9 @@ extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const 
     for (int i = 0; i < 3; ++i) ev[i].start = h->stage_ev[i];
     ev[2].stop = h->stage_ev[3];
   }
-  // the projections also produce the rank-1 terms and the V sums the core reads
+  // the projections also produce the V sums the core reads
   hipError_t e = launch_projections(rs, h->w, h->ws, x, pos_table, st, ev[0]);
-  if (e == hipSuccess) e = launch_attention(rs, h->sc, h->ws, lens, st, ev[1]);
+  if (e == hipSuccess) e = launch_attention(rs, h->w, h->sc, h->ws, lens, st, ev[1]);
   if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st, ev[2]);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;

@@ -14,12 +14,9 @@
 //                chosen per run so that the table row j-i+T-1 of every 16-query by
 //                16-key tile starts a 16-row block.  The rows around the table keep
 //                every padded tile in bounds (their contents are never used).
-//   bu     int32 [B][H][T_al]       u . K_j  (rank-1 part of the content score)
-//   bv     int32 [H][P_ROWS]        v . P_r  (rank-1 part of the position score; rows
-//                                   of the table only)
 //   vsum   int32 [B][H][T_al/64][16][DK/16] sums of V over each 64-key chunk; channel n
-//                                   at [n % 16][n / 16]
-//   (bu, bv and vsum are written by the projection GEMM's epilogue)
+//                                   at [n % 16][n / 16] (written by the projection
+//                                   GEMM's epilogue)
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
@@ -48,7 +45,7 @@ __host__ __device__ inline size_t vt_index(int t, int kk, int DK) {
 
 struct Workspace {
   int8_t *q, *k, *vt, *p, *ctx;
-  int32_t *bu, *bv, *vsum;
+  int32_t* vsum;
 };
 
 struct Weights {
@@ -104,8 +101,8 @@ inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem,
 // Enqueue the kernels of one run; return the first HIP error.
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev = {});
-hipError_t launch_attention(const RunShape& rs, const Scalars& sc, const Workspace& ws, const Lengths& lens,
-                            hipStream_t st, const LaunchEv& ev = {});
+hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars& sc, const Workspace& ws,
+                            const Lengths& lens, hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev = {});
 // Workgroup shapes of the attention core for a run: the first shape's nqb1 query
