@@ -535,19 +535,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
         }
       }
     };
-    // V^T operands in parts of NP = 4 channel tiles (a d_k = 128 chunk is two parts),
-    // each with this lane's V sums over the chunk for channels (h NP + k) * 16 + col
-    constexpr int NP = 4;
-    constexpr int NSPLIT = NT / NP;
+    // V^T operands in parts of NP = 2 channel tiles, each with this lane's V sums over
+    // the chunk for channels (hp NP + k) * 16 + col.  One buffer per part of a chunk:
+    // a part is refilled with the next chunk's as soon as its MFMAs are issued, so a
+    // whole chunk of V is in flight while the current one is multiplied (past the last
+    // chunk the loads re-read it: in bounds, unused, and the loads stay unconditional).
+    constexpr int NP = 2;
+    constexpr int NPART = NT / NP;
     struct VPart {
       v4i v[NP];
-      v4i s;
+      int s[NP];
     };
     auto load_part = [&](int c, int hp, VPart& dst) {
       const int8_t* src = VTh + (size_t)c * CH + hp * NP * 1024 + vt_off;
 #pragma unroll
       for (int k = 0; k < NP; ++k) dst.v[k] = *(const v4i*)(src + k * 1024);
-      dst.s = *(const v4i*)(vs + ((size_t)c * 16 + col) * NT + hp * NP);
+      const int2 sv2 = *(const int2*)(vs + ((size_t)c * 16 + col) * NT + hp * NP);
+      dst.s[0] = sv2.x;
+      dst.s[1] = sv2.y;
     };
     int vacc[NT];
 #pragma unroll
@@ -562,35 +567,20 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
         vacc[hp * NP + k] += vp.s[k];
       }
     };
-    auto codes = [&](int c) {
+    const int c_last = c_end - 1;
+    VPart pb[NPART];
+#pragma unroll
+    for (int hp = 0; hp < NPART; ++hp) load_part(c_begin, hp, pb[hp]);
+    for (int c = c_begin; c < c_end; ++c) {
       if (c < c_full)
         codes_full(c, af);
       else
         codes_tail(c, af);
-    };
-    // the next part is always in flight; past the last chunk the loads re-read it
-    // (in bounds, unused), which keeps the loads unconditional
-    const int c_last = c_end - 1;
-    VPart pb0, pb1;
-    load_part(c_begin, 0, pb0);
-    if (NSPLIT == 2) {
-      for (int c = c_begin; c < c_end; ++c) {
-        load_part(c, 1, pb1);
-        codes(c);
-        mma_part(0, pb0);
-        load_part(min(c + 1, c_last), 0, pb0);
-        mma_part(1, pb1);
-      }
-    } else {
-      for (int c = c_begin; c < c_end;) {
-        load_part(min(c + 1, c_last), 0, pb1);
-        codes(c);
-        mma_part(0, pb0);
-        if (++c >= c_end) break;
-        load_part(min(c + 1, c_last), 0, pb0);
-        codes(c);
-        mma_part(0, pb1);
-        ++c;
+      const int cn = min(c + 1, c_last);
+#pragma unroll
+      for (int hp = 0; hp < NPART; ++hp) {
+        mma_part(hp, pb[hp]);
+        load_part(cn, hp, pb[hp]);
       }
     }
     // exact correction for the -128 offset: + 128 * sum of V over the same keys
