@@ -160,8 +160,8 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int8_t* Ph = a.p + (size_t)h * a.p_rows * DK;
   const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
   uint8_t* my_rows = sbuf + (size_t)(ROWS * qset) * srow;
-  // this lane's 16 bytes of a 1 KB operand fragment (16 rows x 64 bytes, row-major)
-  const int frag_off = col * 64 + g * 16;
+  // this lane's 16 bytes of a 1 KB operand fragment (stored in lane order)
+  const int frag_off = lane * 16;
 
   constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
@@ -495,7 +495,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
     for (int t = 0; t < NTL; ++t)
       arow[t] = (const uint8_t*)tab + (Mrow[t] * 32 + col + 16 * (g & 1)) * 4 + (qset * NTL + t);
-    const int vt_off = col * 64 + g * 16;       // lane's bytes of a 16-channel x 64-key block
+    const int vt_off = lane * 16;               // lane's bytes of a 16-channel x 64-key block
     constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
     // softmax codes (as a - 128) of one chunk of keys for every query tile;
     // all lookups of a chunk are issued before any is packed

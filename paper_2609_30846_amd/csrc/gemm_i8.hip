@@ -230,9 +230,13 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   const size_t head_bytes = (size_t)args.T_al << dks;  // one (utterance, head) block of Q, K or V^T
   // frag_index / vt_index with d_k = 2^dks
   auto frag_off = [&](int row, int kk) {
-    return ((size_t)(row >> 4) << (dks + 4)) + (size_t)((kk >> 6) << 10) + ((row & 15) << 6) + (kk & 63);
+    return ((size_t)(row >> 4) << (dks + 4)) + (size_t)((kk >> 6) << 10) + (((((kk >> 4) & 3) << 4) + (row & 15)) << 4) +
+           (kk & 15);
   };
-  auto vt_off = [&](int t, int kk) { return ((size_t)(t >> 6) << (dks + 6)) + (size_t)(kk << 6) + (t & 63); };
+  auto vt_off = [&](int t, int kk) {
+    return ((size_t)(t >> 6) << (dks + 6)) + (size_t)((kk >> 4) << 10) + (((((t >> 4) & 3) << 4) + (kk & 15)) << 4) +
+           (t & 15);
+  };
   // sum over both half-waves (lanes l and l ^ 32)
   auto half_sum = [](int x) {
     const auto s2 = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);

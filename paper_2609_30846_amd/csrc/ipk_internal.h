@@ -1,14 +1,21 @@
 // Internal declarations of the ipk library (not part of the C ABI).
 //
 // Workspace layout in HBM for one run of (B, T), with T_al = T rounded up to the
-// 64-key chunk and H heads of width DK.  Every layout is chosen so that the
-// attention core's MFMA operand fragments (16 rows x 64 bytes) are contiguous 1 KB
-// blocks, which the L2 serves at about twice the rate of 16 scattered half lines.
+// 64-key chunk and H heads of width DK.  Every layout is chosen so that an MFMA
+// operand fragment of the attention core (16 rows x 64 bytes of K-dimension) is a
+// contiguous 1 KB block in lane order: lane (g, col) of the fragment's load, which
+// feeds row col with bytes 16 g .. 16 g + 15, finds them at byte 16 (16 g + col).
+// A load whose lanes walk 16-byte pieces in address order streams about twice as
+// fast through the vector memory path as one whose neighbouring lanes sit 64 bytes
+// apart.
 //   q, k   int8  [B][H] fragment-major rows: row t, channel kk sits at
-//                frag_index(t, kk) = (t/16)*16*DK + (kk/64)*1024 + (t%16)*64 + kk%64
-//   vt     int8  [B][H] V transposed, chunk-major: key t, channel kk sits at
-//                vt_index(t, kk) = (t/64)*64*DK + kk*64 + t%64; keys T .. T_al-1
-//                hold zeros
+//                frag_index(t, kk) = (t/16)*16*DK + (kk/64)*1024
+//                                    + (16*((kk%64)/16) + t%16)*16 + kk%16
+//   vt     int8  [B][H] V transposed, chunk-major (the fragment rows are channels,
+//                its K-dimension keys): key t, channel kk sits at
+//                vt_index(t, kk) = (t/64)*64*DK + (kk/16)*1024
+//                                  + (16*((t%64)/16) + kk%16)*16 + t%16;
+//                keys T .. T_al-1 hold zeros
 //   p      int8  [H] fragment-major rows of the projected relative-position table;
 //                table row r is stored at row p_base + r, where p_base >= P_PADLO is
 //                chosen per run so that the table row j-i+T-1 of every 16-query by
@@ -37,10 +44,11 @@ inline int p_rows(int T_al) { return P_PADLO + 2 * T_al + P_PADHI; }
 inline int p_base_row(int T) { return P_PADLO + (16 - (T - 1) % 16) % 16; }
 
 __host__ __device__ inline size_t frag_index(int row, int kk, int DK) {
-  return (size_t)(row >> 4) * (16 * DK) + (size_t)(kk >> 6) * 1024 + (row & 15) * 64 + (kk & 63);
+  return (size_t)(row >> 4) * (16 * DK) + (size_t)(kk >> 6) * 1024 + ((((kk >> 4) & 3) << 4) + (row & 15)) * 16 +
+         (kk & 15);
 }
 __host__ __device__ inline size_t vt_index(int t, int kk, int DK) {
-  return (size_t)(t >> 6) * (64 * DK) + (size_t)kk * 64 + (t & 63);
+  return (size_t)(t >> 6) * (64 * DK) + (size_t)(kk >> 4) * 1024 + ((((t >> 4) & 3) << 4) + (kk & 15)) * 16 + (t & 15);
 }
 
 struct Workspace {
