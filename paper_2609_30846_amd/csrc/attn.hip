@@ -311,7 +311,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
             v = (int)__builtin_fma(a.mcd, (double)cs[t][i], __builtin_fma(a.mpd, (double)pt, k1d));
           } else {
             int x = mad_i24(a.mp24, pt, k1);
-            asm volatile("" : "+v"(x));  // keep the two multiply-adds from being re-associated
+            asm("" : "+v"(x));  // opaque to the optimizer (keeps the multiply-adds apart), not a scheduling barrier
             v = mad_i24(a.mc24, cs[t][i], x);
           }
           v = min(max(v, LOCODE), HICODE);
