@@ -84,7 +84,7 @@ __device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2,
   return (c0 | (c1 << 8) | (c2 << 16) | (c3 << 24)) ^ 0x80808080u;
 }
 
-template <int TN, int TM, int NWM>
+template <int TN, int TM, int NWM, int PF>
 __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 128 * NWM;            // threads: 2 waves along N, NWM along M
   constexpr int WTM = TM / NWM;             // tokens per wave
@@ -139,28 +139,31 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
       (void*)(P.x + ((size_t)ub * rows + t0) * K), (short)0, (rows - t0) * K, BUF_WORD3);
   const int foff = frow * K + fchunk * 16;
 
-  v4i rw[LW], rx[LX];
+  // PF register sets: a K step is fetched PF steps before it is stored to LDS (PF = 2
+  // for launches too short on tiles per CU to hide the load latency otherwise)
+  static_assert(PF == 1 || PF == 2, "prefetch depth");
+  v4i rw[PF][LW], rx[PF][LX];
   // K is a multiple of 64: the last step of an odd multiple fills its upper half with zeros
-  auto fetch = [&](int k0) {
+  auto fetch = [&](int k0, int set) {
     if (k0 + fchunk * 16 < K) {
 #pragma unroll
       for (int r = 0; r < LW; ++r)
-        rw[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, foff + FROWS * r * K + k0, 0, 0);
+        rw[set][r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, foff + FROWS * r * K + k0, 0, 0);
 #pragma unroll
       for (int r = 0; r < LX; ++r)
-        rx[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
+        rx[set][r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
     } else {
 #pragma unroll
-      for (int r = 0; r < LW; ++r) rw[r] = (v4i){};
+      for (int r = 0; r < LW; ++r) rw[set][r] = (v4i){};
 #pragma unroll
-      for (int r = 0; r < LX; ++r) rx[r] = (v4i){};
+      for (int r = 0; r < LX; ++r) rx[set][r] = (v4i){};
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, int set) {
 #pragma unroll
-    for (int r = 0; r < LW; ++r) *(v4i*)(sw[buf] + lds_off(frow + FROWS * r, fchunk)) = rw[r];
+    for (int r = 0; r < LW; ++r) *(v4i*)(sw[buf] + lds_off(frow + FROWS * r, fchunk)) = rw[set][r];
 #pragma unroll
-    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[r];
+    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[set][r];
   };
 
   // waves whose channels are V produce the transposed product (tokens along MFMA rows)
@@ -180,23 +183,16 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // branch inside it
   auto kloop = [&](auto swap_tag) {
     constexpr bool SWAP = decltype(swap_tag)::value;
-    // step kt is multiplied out of buffer kt % 2 while step kt + 1 (fetched during
-    // step kt - 1) is stored into the other one; one barrier per step orders both
-    fetch(0);
-    stash(0);
-    if (nk > 1) fetch(BK);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
+    auto mma = [&](const int buf) {
 #pragma unroll
       for (int ks = 0; ks < BK / 32; ++ks) {
         v4i af[FN], bf[FM];
 #pragma unroll
         for (int i = 0; i < FN; ++i)
-          af[i] = *(const v4i*)(sw[cur] + lds_off(wn * (TN / 2) + i * 32 + frag_row, 2 * ks + half));
+          af[i] = *(const v4i*)(sw[buf] + lds_off(wn * (TN / 2) + i * 32 + frag_row, 2 * ks + half));
 #pragma unroll
         for (int j = 0; j < FM; ++j)
-          bf[j] = *(const v4i*)(sx[cur] + lds_off(wm * WTM + j * 32 + frag_row, 2 * ks + half));
+          bf[j] = *(const v4i*)(sx[buf] + lds_off(wm * WTM + j * 32 + frag_row, 2 * ks + half));
 #pragma unroll
         for (int i = 0; i < FN; ++i)
 #pragma unroll
@@ -204,11 +200,46 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
             acc[i][j] = SWAP ? __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[j], af[i], acc[i][j], 0, 0, 0)
                              : __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < nk) {
-        stash(cur ^ 1);
-        if (kt + 2 < nk) fetch((kt + 2) * BK);
-      }
+    };
+    if constexpr (PF == 1) {
+      // step kt is multiplied out of buffer kt % 2 while step kt + 1 (fetched during
+      // step kt - 1) is stored into the other one; one barrier per step orders both
+      fetch(0, 0);
+      stash(0, 0);
+      if (nk > 1) fetch(BK, 0);
       __syncthreads();
+      for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        mma(cur);
+        if (kt + 1 < nk) {
+          stash(cur ^ 1, 0);
+          if (kt + 2 < nk) fetch((kt + 2) * BK, 0);
+        }
+        __syncthreads();
+      }
+    } else {
+      // even steps in register set 0 and LDS buffer 0, odd ones in set 1 and buffer 1;
+      // step k is fetched while step k - 2 is multiplied
+      fetch(0, 0);
+      if (nk > 1) fetch(BK, 1);
+      stash(0, 0);
+      if (nk > 2) fetch(2 * BK, 0);
+      __syncthreads();
+      for (int kt = 0; kt < nk; kt += 2) {
+        mma(0);
+        if (kt + 1 < nk) {
+          stash(1, 1);
+          if (kt + 3 < nk) fetch((kt + 3) * BK, 1);
+        }
+        __syncthreads();
+        if (kt + 1 >= nk) break;
+        mma(1);
+        if (kt + 2 < nk) {
+          stash(0, 0);
+          if (kt + 4 < nk) fetch((kt + 4) * BK, 0);
+        }
+        __syncthreads();
+      }
     }
   };
   if (vwave) kloop(std::true_type{});
@@ -355,11 +386,11 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWM>
+template <int TN, int TM, int NWM, int PF>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWM>, dim3(8 * a.per_xcd), dim3(128 * NWM), 0, st, ev, a);
+  return launch_kernel(gemm_i8_requant<TN, TM, NWM, PF>, dim3(8 * a.per_xcd), dim3(128 * NWM), 0, st, ev, a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
@@ -372,17 +403,19 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
-  return launch_gemm<TN, TM, NWM>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWM, 1>(a, tiles, st, ev);
 }
 
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, y);
-  constexpr int TN = 128, TM = 64, NWM = 2;
+  // small tiles and two steps of prefetch: with K = d_model and only a few tiles per
+  // CU, the K loop waits on load latency rather than on bandwidth
+  constexpr int TN = 64, TM = 64, NWM = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  return launch_gemm<TN, TM, NWM>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWM, 2>(a, tiles, st, ev);
 }
 
 }  // namespace ipk
