@@ -24,16 +24,18 @@ FLAGS = [
     "-Wall",
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA accumulators in ordinary VGPRs: the attention core post-processes every
-    # score tile with VALU code, which would otherwise copy them out of AGPRs
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
-# Per-source extra flags.  The attention core keeps two waves per SIMD whatever the
-# schedule, so the machine scheduler is asked for instruction-level parallelism
-# rather than the default occupancy-first order (measured faster on the core).
+# Per-source extra flags.  The attention core post-processes every score tile with
+# VALU code, so its MFMA accumulators live in ordinary VGPRs (in AGPRs they would be
+# copied out first); it keeps two waves per SIMD whatever the schedule, so the
+# machine scheduler is asked for instruction-level parallelism rather than the
+# default occupancy-first order (measured faster on the core).  The projection GEMMs
+# requantize their accumulators with VALU code too.
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
 EXTRA = {
-    "attn.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "attn.hip": VGPR_FORM + ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "gemm_i8.hip": VGPR_FORM,
 }
 
 

@@ -7,13 +7,16 @@
 //
 // Kernel shape: one workgroup of 2 x NWM waves computes a TN (channels) x TM (tokens)
 // tile with v_mfma_i32_32x32x32_i8; the waves form a 2 x NWM grid of (TN/2) x (TM/NWM)
-// sub-tiles.  The loads, not the matrix cores, bound a step, and the operand bytes
-// per multiply-accumulate fall as the tile grows: the large projections use 256 x 256
-// tiles of eight waves.  K advances in 128-byte steps, so every global row segment is
-// a whole cache line; the next step is fetched into registers while the current one is
+// sub-tiles.  K advances in 128-byte steps, so every global row segment is a whole
+// cache line; the next step is fetched into registers while the current one is
 // multiplied out of LDS.  LDS rows are 128 bytes with the eight 16-byte chunks
 // XOR-swizzled by the row index, which keeps both the 16-byte stores of the fetch
 // and the 16-byte MFMA operand reads free of bank conflicts.
+//
+// The large projections use 256 x 256 tiles of eight waves (two per SIMD, 128 x 64
+// outputs each, accumulators in VGPRs).  A K step then moves 192 KB of MFMA fragments
+// and 64 KB of staged tile through LDS, which at 128 bytes per clock per CU takes
+// longer than the step's matrix-core work: LDS bandwidth, not MFMA, bounds the loop.
 //
 // Token tiles never straddle two utterances (each utterance is tiled on its own), so
 // every destination layout receives whole aligned 16-byte pieces.  Tiles are dealt
@@ -69,19 +72,31 @@ constexpr int BUF_WORD3 = 0x00020000;  // buffer resource word 3 for gfx9-family
 // read one logical chunk touch 16 distinct (row parity, chunk) bank groups.
 __device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ ((r ^ (r >> 3)) & 7)) << 4); }
 
-// biased code y + 128 of one accumulator (exact, see the header comment)
-__device__ __forceinline__ uint32_t requant_code(int acc, double scale) {
-  const double t = __builtin_fma((double)acc, scale, 128.5);
-  // v_cvt_i32_f64 truncates and saturates to the int32 range; truncation equals the
-  // floor wherever the clamp below does not decide the result (t >= 1)
-  int v;
-  asm("v_cvt_i32_f64 %0, %1" : "=v"(v) : "v"(t));
-  return (uint32_t)min(max(v, 1), 255);
-}
-
 // four biased codes -> four int8 bytes (code - 128 == code ^ 0x80 for code in [1, 255])
 __device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3) {
   return (c0 | (c1 << 8) | (c2 << 16) | (c3 << 24)) ^ 0x80808080u;
+}
+
+// int8 codes of the 16 accumulators of one MFMA output block (exact, see the header
+// comment), packed four per dword: D[g] holds elements 4g .. 4g + 3.  All sixteen
+// products are formed before any is converted, and the conversions go four to an asm
+// statement, so independent values overlap instead of running as one long chain.
+// v_cvt_i32_f64 truncates and saturates to the int32 range; truncation equals the
+// floor wherever the clamp to [1, 255] does not decide the result (t >= 1).
+__device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16], uint32_t (&D)[4]) {
+  double t[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) t[e] = __builtin_fma((double)a[e], sc[e], 128.5);
+  int v[16];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    asm("v_cvt_i32_f64 %0, %4\n\tv_cvt_i32_f64 %1, %5\n\tv_cvt_i32_f64 %2, %6\n\tv_cvt_i32_f64 %3, %7"
+        : "=&v"(v[4 * g]), "=&v"(v[4 * g + 1]), "=&v"(v[4 * g + 2]), "=&v"(v[4 * g + 3])
+        : "v"(t[4 * g]), "v"(t[4 * g + 1]), "v"(t[4 * g + 2]), "v"(t[4 * g + 3]));
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    D[g] = pack4((uint32_t)min(max(v[4 * g], 1), 255), (uint32_t)min(max(v[4 * g + 1], 1), 255),
+                 (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
 }
 
 template <int TN, int TM, int NWM, int PF>
@@ -94,6 +109,7 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   constexpr int LX = TM * (BK / 16) / NTH;  // same for the X tile
   constexpr int FROWS = NTH / 8;            // rows one pass of the fetch covers
   static_assert(FM >= 1 && LW >= 1 && LX >= 1 && WTM % 32 == 0 && NTH >= TN, "tile shape");
+  constexpr int CPW = WTM >= KCHUNK ? WTM / KCHUNK : 1;  // 64-key chunks per wave (V sums)
   // two LDS buffers: the next K step is stored while the current one is multiplied
   __shared__ __align__(16) int8_t sw[2][TN * BK];
   __shared__ __align__(16) int8_t sx[2][TM * BK];
@@ -253,8 +269,9 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // Q/K/V boundary (N and d_k are multiples of 64), so its destination is uniform.
   //
   // The same pass sums the int8 V values it stores over each 64-key chunk (a wave's
-  // WTM = 64 tokens are one chunk; the two half-waves hold its two halves).  V^T is
-  // written up to T_al, so the padded keys hold zeros, as the sums do.
+  // WTM tokens are WTM / 64 whole chunks, two 32-token MFMA columns each; the two
+  // half-waves hold the two halves of a column).  V^T is written up to T_al, so the
+  // padded keys hold zeros, as the sums do.
   const int col = lane & 31;
   const int tw0 = t0 + wm * WTM;
   const int dks = args.dk_shift, DK = 1 << dks, DKm = DK - 1;
@@ -294,53 +311,67 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
     } else {
       dst = args.y + (size_t)ub * rows * N + nb;
     }
-    int vpart = 0;  // this lane's share of the chunk's V sum of channel kk + col
+    // the scales of this sub-tile's channels, the same for all its token columns
+    double sc[16];
+    if (vwave) {
+      // rows are tokens, the column is the channel
+      const double s1 = ssc[nl + col];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = s1;
+    } else {
+      // rows are channels (element 4g + e is channel g * 8 + half * 4 + e), the
+      // column is the token
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = ssc[nl + (e >> 2) * 8 + half * 4 + (e & 3)];
+    }
+    // this lane's destination for token column j = 0 (relative to dst, under 2^31),
+    // the first token it stores and the bound on tokens: one 32-token column further
+    // is a uniform step (jstep; for V^T, 512 bytes within a 64-key block, and the
+    // next block at even columns)
+    int tl, tmax;
+    uint32_t off0;
+    if (vwave) {
+      tl = tw0 + half * 16;
+      tmax = args.T_al;
+      off0 = (uint32_t)vt_off(tl, kk + col);
+    } else {
+      tl = tw0 + col;
+      tmax = rows;
+      off0 = mode == OUT_ROWMAJOR ? (uint32_t)(tl * N + half * 16)
+                                  : (uint32_t)frag_off((mode == OUT_POS ? args.p_base : 0) + tl, kk + half * 16);
+    }
+    const uint32_t jstep = mode == OUT_ROWMAJOR ? 32u * (uint32_t)N : 2u << (dks + 4);
+    // this lane's share of the V sum of channel kk + col over each of the wave's chunks
+    int vpart[CPW];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) vpart[c] = 0;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       uint32_t D[4];
-      if (vwave) {
-        // rows are tokens, the column is the channel
-        const double sc = ssc[nl + col];
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          D[g] = pack4(requant_code(acc[i][j][g * 4 + 0], sc), requant_code(acc[i][j][g * 4 + 1], sc),
-                       requant_code(acc[i][j][g * 4 + 2], sc), requant_code(acc[i][j][g * 4 + 3], sc));
-      } else {
-        // rows are channels, the column is the token
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = nl + g * 8 + half * 4;
-          D[g] = pack4(requant_code(acc[i][j][g * 4 + 0], ssc[c]), requant_code(acc[i][j][g * 4 + 1], ssc[c + 1]),
-                       requant_code(acc[i][j][g * 4 + 2], ssc[c + 2]), requant_code(acc[i][j][g * 4 + 3], ssc[c + 3]));
-        }
-      }
+      requant16(acc[i][j], sc, D);
       const auto x02 = __builtin_amdgcn_permlane32_swap(D[0], D[2], false, false);
       const auto x13 = __builtin_amdgcn_permlane32_swap(D[1], D[3], false, false);
       const v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
 
+      // V^T: 16 consecutive tokens of one channel, stored up to T_al (zeros past the
+      // utterance: the operand rows there read as zeros); otherwise 16 consecutive
+      // channels of one token
+      const uint32_t joff = vwave ? ((uint32_t)(j >> 1) << (dks + 6)) + (uint32_t)(j & 1) * 512u : (uint32_t)j * jstep;
+      if (tl + j * 32 < tmax) *(v4i*)(dst + (off0 + joff)) = out;
       if (vwave) {
-        // 16 consecutive tokens of one channel, stored up to T_al (zeros past the
-        // utterance: the operand rows there read as zeros)
-        const int t = tw0 + j * 32 + half * 16;
-        if (t < args.T_al) *(v4i*)(dst + vt_off(t, kk + col)) = out;
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) vpart = __builtin_amdgcn_sdot4(out[wd], 0x01010101, vpart, false);
-      } else {
-        // 16 consecutive channels of token t
-        const int t = tw0 + j * 32 + col;
-        if (t < rows) {
-          if (mode == OUT_QKV) *(v4i*)(dst + frag_off(t, kk + half * 16)) = out;
-          else if (mode == OUT_POS) *(v4i*)(dst + frag_off(args.p_base + t, kk + half * 16)) = out;
-          else *(v4i*)(dst + (size_t)t * N + half * 16) = out;
-        }
+        for (int wd = 0; wd < 4; ++wd) vpart[j / 2] = __builtin_amdgcn_sdot4(out[wd], 0x01010101, vpart[j / 2], false);
       }
     }
     if (vwave) {
-      // sum of V over the 64-key chunk tw0 / 64, channel kk + col: [chunk][n % 16][n / 16]
-      const int tot = half_sum(vpart);
-      if (half == 0 && tw0 < args.T_al) {
-        const int n = kk + col, nch = args.T_al >> 6;
-        args.vsum[((((size_t)ub * args.H + hd) * nch + (tw0 >> 6)) * 16 + (n & 15)) * (DK >> 4) + (n >> 4)] = tot;
+      // sums of V over the 64-key chunks tw0 / 64 + c, channel kk + col: [chunk][n % 16][n / 16]
+      const int n = kk + col, nch = args.T_al >> 6;
+#pragma unroll
+      for (int c = 0; c < CPW; ++c) {
+        const int tot = half_sum(vpart[c]);
+        const int tc = tw0 + c * KCHUNK;
+        if (half == 0 && tc < args.T_al)
+          args.vsum[((((size_t)ub * args.H + hd) * nch + (tc >> 6)) * 16 + (n & 15)) * (DK >> 4) + (n >> 4)] = tot;
       }
     }
   }
@@ -398,8 +429,8 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
   constexpr int TN = 256, TM = 256, NWM = 4;
-  // the epilogue's V sums: a wave's tokens are one 64-key chunk
-  static_assert(TM / NWM == KCHUNK && (TN / 2) % 128 == 0, "projection tile shape");
+  // the epilogue's V sums: a wave's tokens are whole 64-key chunks
+  static_assert((TM / NWM) % KCHUNK == 0 && (TN / 2) % 128 == 0, "projection tile shape");
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
