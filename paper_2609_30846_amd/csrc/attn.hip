@@ -95,6 +95,12 @@ __device__ __forceinline__ int mad_i24(int a, int b, int c) {
 }
 
 constexpr int ATTN_WAVES = 8;  // waves per workgroup (two per SIMD)
+// Share (out of 256) of a SIMD's keys that its older wave takes in phase 1 and in
+// phases 2 and 3.  With equal shares the younger wave of a pair ends phase 1 about
+// 1.35x and phase 3 about 1.25x later than the older one on the long-form workload;
+// these shares (about 65 % and 59 %) measured fastest over the whole kernel.
+constexpr int P1_OLDER = 166;
+constexpr int P3_OLDER = 150;
 
 template <int S>
 using Phase = std::integral_constant<int, S>;
@@ -114,7 +120,29 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in SGPRs
   const int col = lane & 15, g = lane >> 4;
-  const int qset = w / KSPLIT, kpart = w % KSPLIT;
+  // Waves w and w + 4 share SIMD w % 4, whose instruction arbiter favours the older
+  // one (the lower index): given equal work, the younger wave finishes long after it
+  // and runs its tail alone.  The two waves of a SIMD therefore take the same query set
+  // and split its keys unevenly, the older one taking the larger share.
+  constexpr int HK = KSPLIT > 1 ? KSPLIT / 2 : 1;  // key parts per age class
+  const int simd = w & 3, younger = w >> 2;
+  const int qset = KSPLIT > 1 ? simd / HK : w;
+  const int kpart = KSPLIT > 1 ? younger * HK + simd % HK : 0;
+  const int slot = qset * KSPLIT + kpart;  // this wave's row-max and row-sum slot
+  // work units [*b, *e) of this wave out of n: every SIMD gets n / HK of them, of
+  // which its older wave takes older / 256 (rounded) and its younger wave the rest
+  auto split = [&](const int n, const int older, int* b, int* e) {
+    if (KSPLIT == 1) {
+      *b = 0;
+      *e = n;
+      return;
+    }
+    const int pair = kpart % HK;
+    const int ps = n * pair / HK, pe = n * (pair + 1) / HK;
+    const int mid = ps + ((pe - ps) * older + 128) / 256;
+    *b = younger ? mid : ps;
+    *e = younger ? pe : mid;
+  };
   // Workgroups go round-robin to the 8 XCDs (id % 8); when the (utterance, head)
   // pairs divide evenly, every workgroup of one pair is placed on the same XCD so that
   // its K, P and V stay in that XCD's L2.
@@ -134,8 +162,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int T = a.T, T_al = a.T_al;
   const int srow = T_al + SCORE_PAD;
   const int nkc = (L + KCHUNK - 1) / KCHUNK;
-  const int c_begin = kpart * nkc / KSPLIT, c_end = (kpart + 1) * nkc / KSPLIT;
-  const int c_full = min(c_end, L / KCHUNK);  // chunks below this hold only valid keys
+  int c_begin, c_end;
+  split(nkc, P3_OLDER, &c_begin, &c_end);
+  // chunks below c_full hold only valid keys; c_full < c_end only when this wave's
+  // range holds the chunk with the utterance's last key (an empty range past it too
+  // ends at c_full = c_end)
+  const int c_full = max(c_begin, min(c_end, L / KCHUNK));
   const bool active = q0 < L;
 
   // LDS carve-up (the host computes the same sizes)
@@ -173,10 +205,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
     for (int i = 0; i < 4; ++i) mx[t][i] = LOCODE;
 
-  // phase 1 splits the 16-key steps that hold a valid key evenly over the key splits
+  // phase 1 splits the 16-key steps that hold a valid key over the key parts
   const int nst = (L + 15) >> 4;
-  const int j_begin = 16 * (kpart * nst / KSPLIT);
-  const int j_stop = 16 * ((kpart + 1) * nst / KSPLIT);
+  int j_begin, j_stop;
+  split(nst, P1_OLDER, &j_begin, &j_stop);
+  j_begin *= 16;
+  j_stop *= 16;
   const int j_full = max(j_begin, min(j_stop, L & ~15));  // steps below this are unmasked
   if (active && j_begin < j_stop) {
     const uint32_t frag = (uint32_t)frag_off;
@@ -381,7 +415,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
     for (int t = 0; t < NTL; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) smax[w * ROWS + 16 * t + 4 * g + i] = WIDE ? mx[t][i] : (mx[t][i] >> 16);
+      for (int i = 0; i < 4; ++i) smax[slot * ROWS + 16 * t + 4 * g + i] = WIDE ? mx[t][i] : (mx[t][i] >> 16);
   }
   __syncthreads();
 
@@ -449,7 +483,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   }
   if (g == 0) {
 #pragma unroll
-    for (int t = 0; t < NTL; ++t) ssum[w * ROWS + 16 * t + col] = sum[t];
+    for (int t = 0; t < NTL; ++t) ssum[slot * ROWS + 16 * t + col] = sum[t];
   }
   __syncthreads();
   // F = floor(2^32 / sum), one row per thread.  The float64 quotient is correctly
