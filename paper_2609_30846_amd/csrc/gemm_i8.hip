@@ -32,6 +32,7 @@
 // produced by swapping the MFMA operands in the waves whose channels are V, so that
 // its 16-byte pieces run along tokens.
 #include <type_traits>
+#include <utility>
 
 #include "ipk_internal.h"
 
@@ -71,6 +72,16 @@ constexpr int BUF_WORD3 = 0x00020000;  // buffer resource word 3 for gfx9-family
 // is XORed with (r ^ r/8) mod 8, so any 16 consecutive rows (16-row aligned) that
 // read one logical chunk touch 16 distinct (row parity, chunk) bank groups.
 __device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ ((r ^ (r >> 3)) & 7)) << 4); }
+
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>), in order
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // four biased codes -> four int8 bytes (code - 128 == code ^ 0x80 for code in [1, 255])
 __device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3) {
@@ -156,8 +167,9 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   const int foff = frow * K + fchunk * 16;
 
   // PF register sets: a K step is fetched PF steps before it is stored to LDS (PF = 2
-  // for launches too short on tiles per CU to hide the load latency otherwise)
-  static_assert(PF == 1 || PF == 2, "prefetch depth");
+  // for the output projection, whose short launch has few tiles per CU; 4 and 6
+  // measured slower there)
+  static_assert(PF == 1 || PF % 2 == 0, "prefetch depth");
   v4i rw[PF][LW], rx[PF][LX];
   // K is a multiple of 64: the last step of an odd multiple fills its upper half with zeros
   auto fetch = [&](int k0, int set) {
@@ -234,27 +246,28 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
         __syncthreads();
       }
     } else {
-      // even steps in register set 0 and LDS buffer 0, odd ones in set 1 and buffer 1;
-      // step k is fetched while step k - 2 is multiplied
-      fetch(0, 0);
-      if (nk > 1) fetch(BK, 1);
+      // step k is fetched into register set k % PF, PF steps before it is stored to
+      // LDS buffer k % 2 (PF is even, so both indices are static in a loop unrolled PF
+      // times); one barrier per step
+#pragma unroll
+      for (int st = 0; st < PF; ++st)
+        if (st < nk) fetch(st * BK, st);
       stash(0, 0);
-      if (nk > 2) fetch(2 * BK, 0);
+      if (PF < nk) fetch(PF * BK, 0);
       __syncthreads();
-      for (int kt = 0; kt < nk; kt += 2) {
-        mma(0);
-        if (kt + 1 < nk) {
-          stash(1, 1);
-          if (kt + 3 < nk) fetch((kt + 3) * BK, 1);
-        }
-        __syncthreads();
-        if (kt + 1 >= nk) break;
-        mma(1);
-        if (kt + 2 < nk) {
-          stash(0, 0);
-          if (kt + 4 < nk) fetch((kt + 4) * BK, 0);
-        }
-        __syncthreads();
+      for (int kt = 0; kt < nk; kt += PF) {
+        static_for<PF>([&](auto ph) {
+          constexpr int P = decltype(ph)::value;  // (kt + P) % PF
+          constexpr int SN = (P + 1) % PF;        // register set of step kt + P + 1
+          if (kt + P < nk) {
+            mma(P & 1);
+            if (kt + P + 1 < nk) {
+              stash((P + 1) & 1, SN);
+              if (kt + P + 1 + PF < nk) fetch((kt + P + 1 + PF) * BK, SN);
+            }
+            __syncthreads();
+          }
+        });
       }
     }
   };
