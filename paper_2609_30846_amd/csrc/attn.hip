@@ -40,7 +40,9 @@
 // + rr in byte tt of banks rr and rr + 16, and the two half-waves' lanes g = 0, 1 (2,
 // 3) read different copies, so a lookup is one multiply-add and one conflict-free
 // LDS read.
+#include <mutex>
 #include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "ipk_internal.h"
@@ -77,15 +79,6 @@ __device__ __forceinline__ uint32_t iexp_int(int d, int q_ln2, int q_b, int q_c)
   const int r = z * q_ln2 - d;
   const int poly = (r + q_b) * (r + q_b) + q_c;  // < 2^24 (checked at create)
   return z >= 32 ? 0u : ((uint32_t)poly >> z);
-}
-
-// 4x4 byte transpose inside each lane quad: lane p of a quad holds bytes
-// m(0..3, p) and ends with m(p, 0..3).
-__device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t x, uint32_t sel1, uint32_t sel2) {
-  const uint32_t o1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
-  const uint32_t z = __builtin_amdgcn_perm(o1, x, sel1);
-  const uint32_t o2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)z, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
-  return __builtin_amdgcn_perm(o2, z, sel2);
 }
 
 // Low 32 bits of a * b + c for 24-bit signed a, b (v_mad_i32_i24); the addition
@@ -231,15 +224,23 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       take_hi[i] = (col + arow) < 16;                    // as a source lane
       src_addr[i] = (g * 16 + ((col - arow) & 15)) * 4;  // as a destination lane
     }
-    const int p = col & 3;
-    const uint32_t sel1 = (p & 1) ? 0x03070105u : 0x06020400u;
-    const uint32_t sel2 = (p & 2) ? 0x03020706u : 0x05040100u;
-    // after the transpose a lane stores query 4g+p of a tile, keys 4*(col/4) .. +3
-    uint8_t* sdst = my_rows + (size_t)(4 * g + p) * srow + (col >> 2) * 4;
+    // a lane's score of query row 4g + i of tile t and key j0 + col is one byte of
+    // the row: stored directly, so no packing or transposing is spent on it
+    uint8_t* sdst = my_rows + (size_t)(4 * g) * srow + col;
 
-    // table row of (query q0, key j0) is j0 - q0 + T - 1; tile t sits 16 t rows lower
-    const int8_t* kptr = Kh + (size_t)j_begin * DK;
-    const int8_t* pptr = Ph + (size_t)(a.p_base + j_begin - q0 + T - 1) * DK;
+    // K and the position table are streamed with raw buffer loads: the lane's offset in
+    // a fragment is fixed and the step's offset is a scalar, so no vector address
+    // arithmetic is spent per load.  Table row of (query q0, key j0) is
+    // j0 - q0 + T - 1; tile t sits 16 t rows lower.  Every offset stays inside the
+    // padded buffers (the table keeps P_PADLO rows below row 0).
+    const __amdgpu_buffer_rsrc_t kres =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Kh, (short)0, T_al * DK, BUF_WORD3);
+    const __amdgpu_buffer_rsrc_t pres =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Ph, (short)0, a.p_rows * DK, BUF_WORD3);
+    int koff = __builtin_amdgcn_readfirstlane(j_begin * DK);
+    int poff = __builtin_amdgcn_readfirstlane((a.p_base + j_begin - q0 + T - 1) * DK);
+    auto ldk = [&](int off, int s) { return (v4i)__builtin_amdgcn_raw_buffer_load_b128(kres, frag + s * 1024, off, 0); };
+    auto ldp = [&](int off, int s) { return (v4i)__builtin_amdgcn_raw_buffer_load_b128(pres, frag + s * 1024, off, 0); };
     // The rank-1 terms of Eq. 8 come from MFMAs of a 16-row operand whose rows all
     // equal u (v): their products with a K (P) fragment hold u.K_j (v.P_r) in every
     // row, which is the accumulator seed the content (position) MFMAs need.  No load
@@ -261,8 +262,6 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     //  pr[u]:    tile 0's hi-window P fragment of the step with phase u; at phase S
     //            tile t uses slot (S - t) mod NTL (its window is tile 0's window of t
     //            steps before)
-    //  bvp[u]:   v.P_r of that fragment's column (the same in every row), computed
-    //            when the step that loads it is the current one
     //  kr[u]:    K fragment of the step with phase u (current, next)
     //  gr[u][t]: position MFMA results (hi windows) of the step with phase u; a
     //            step's lo windows are the previous step's hi windows
@@ -275,13 +274,13 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       for (int t = 0; t < NTL; ++t) {
         const int u = (NTL - t) % NTL;
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) pr[u][s] = *(const v4i*)(pptr - 16 * t * DK + frag + s * 1024);
+        for (int s = 0; s < NKS; ++s) pr[u][s] = ldp(poff - 16 * t * DK, s);
       }
       // lo windows of the first step: tile t's lo window is tile (t + 1)'s hi window;
       // the last tile's lies one more window lower
       v4i plast[NKS];
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) plast[s] = *(const v4i*)(pptr - 16 * NTL * DK + frag + s * 1024);
+      for (int s = 0; s < NKS; ++s) plast[s] = ldp(poff - 16 * NTL * DK, s);
 #pragma unroll
       for (int t = 0; t < NTL; ++t) bvp[(NTL - t) % NTL] = rank1(vf, pr[(NTL - t) % NTL])[0];
       const int bvlast = rank1(vf, plast)[0];
@@ -296,7 +295,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       }
     }
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) kr[0][s] = *(const v4i*)(kptr + frag + s * 1024);
+    for (int s = 0; s < NKS; ++s) kr[0][s] = ldk(koff, s);
 
     int j0 = j_begin;
     // One 16-key step at phase S: fetches the next step's K and P fragments (the last
@@ -305,21 +304,23 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     auto step = [&](auto Sc, const bool masked) {
       constexpr int S = decltype(Sc)::value;
       constexpr int SN = (S + 1) % NTL, SP = (S + NTL - 1) % NTL;
-      const int adv = j0 + 16 < j_stop ? 16 : 0;
+      const int adv = j0 + 16 < j_stop ? 16 * DK : 0;
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) kr[SN][s] = *(const v4i*)(kptr + adv * DK + frag + s * 1024);
-      // seeds: u.K_j of this step's keys (shared by the tiles) and v.P_r of the
-      // window loaded by the previous step (tile 0's; later tiles reuse older slots)
+      for (int s = 0; s < NKS; ++s) kr[SN][s] = ldk(koff + adv, s);
+      // seeds: u.K_j of this step's keys (shared by the tiles) and, per tile, v.P_r
+      // of the tile's window (recomputed rather than kept: the matrix pipe has room,
+      // the registers do not)
       const v4i uk = rank1(uf, kr[S]);
       bvp[S] = rank1(vf, pr[S])[0];
       v4i cs[NTL];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        cs[t] = uk;
-        gr[S][t] = splat(bvp[(S + NTL - t) % NTL]);
+        cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], kr[S][0], uk, 0, 0, 0);
+        gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], pr[(S + NTL - t) % NTL][0],
+                                                         splat(bvp[(S + NTL - t) % NTL]), 0, 0, 0);
       }
 #pragma unroll
-      for (int s = 0; s < NKS; ++s)
+      for (int s = 1; s < NKS; ++s)
 #pragma unroll
         for (int t = 0; t < NTL; ++t) {
           cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], kr[S][s], cs[t], 0, 0, 0);
@@ -327,14 +328,13 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
         }
       // the last tile's window (slot SN) is consumed: it takes the next step's tile-0 window
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) pr[SN][s] = *(const v4i*)(pptr + adv * DK + frag + s * 1024);
+      for (int s = 0; s < NKS; ++s) pr[SN][s] = ldp(poff + adv, s);
       // cs holds c0 + u.K_j: the addend is the rounding and code bias alone
       const int k1 = a.bias32;
       const double k1d = 128.5;
       const bool key_ok = j0 + col < L;
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        int code[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int sel = take_hi[i] ? gr[S][t][i] : gr[SP][t][i];
@@ -351,21 +351,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
           v = min(max(v, LOCODE), HICODE);
           if (masked && !key_ok) v = LOCODE;
           mx[t][i] = max(mx[t][i], v);
-          code[i] = v;
+          // the code is bits 0..7 (wide path) or 16..23 (narrow path) of v
+          sdst[(size_t)(16 * t + i) * srow + j0] = (uint8_t)(WIDE ? v : (v >> 16));
         }
-        // four queries of one key -> one dword, then four keys of one query
-        uint32_t packed;
-        if (WIDE) {
-          packed = __builtin_amdgcn_perm((uint32_t)code[1], (uint32_t)code[0], 0x0c0c0400u) |
-                   __builtin_amdgcn_perm((uint32_t)code[3], (uint32_t)code[2], 0x04000c0cu);
-        } else {
-          packed = __builtin_amdgcn_perm((uint32_t)code[1], (uint32_t)code[0], 0x0c0c0602u) |
-                   __builtin_amdgcn_perm((uint32_t)code[3], (uint32_t)code[2], 0x06020c0cu);
-        }
-        *(uint32_t*)(sdst + (size_t)(16 * t) * srow + j0) = quad_transpose_bytes(packed, sel1, sel2);
       }
-      kptr += 16 * DK;
-      pptr += 16 * DK;
+      koff += 16 * DK;
+      poff += 16 * DK;
       j0 += 16;
     };
     // NTL unmasked steps per iteration, so that every ring index stays static
@@ -813,6 +804,22 @@ AttnPlan attn_plan(int DK, int T_al, long bh_count, int T) {
   return best;
 }
 
+// Raises a kernel's dynamic-LDS ceiling to the whole budget, once per device (per
+// launch the call would cost host time on every run).
+static hipError_t allow_full_lds(const void* kernel) {
+  static std::mutex mu;
+  static std::vector<std::pair<const void*, int>> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto& d : done)
+    if (d.first == kernel && d.second == dev) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBudget);
+  if (e == hipSuccess) done.emplace_back(kernel, dev);
+  return e;
+}
+
 template <int DK, int KS1, int NTL1, int KS2, int NTL2, bool WIDE>
 static hipError_t launch_attn_plan(const AttnArgs& args, const AttnPlan& p, int B, int H, int T_al, hipStream_t st,
                                    const LaunchEv& ev) {
@@ -821,8 +828,7 @@ static hipError_t launch_attn_plan(const AttnArgs& args, const AttnPlan& p, int 
     const size_t s2 = attn_lds_bytes(DK, KS2, NTL2, T_al);
     shmem = s2 > shmem ? s2 : shmem;
   }
-  hipError_t e = hipFuncSetAttribute((const void*)relpos_attn_core<DK, KS1, NTL1, KS2, NTL2, WIDE>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+  hipError_t e = allow_full_lds((const void*)relpos_attn_core<DK, KS1, NTL1, KS2, NTL2, WIDE>);
   if (e != hipSuccess) return e;
   AttnArgs a2 = args;
   a2.nqb = p.nqb1;

@@ -5,8 +5,8 @@
 // rescaled by a per-output-channel multiplier m and a right shift n with round to
 // nearest (ties up), and clamped to the symmetric int8 grid.
 //
-// Kernel shape: one workgroup of 2 x NWM waves computes a TN (channels) x TM (tokens)
-// tile with v_mfma_i32_32x32x32_i8; the waves form a 2 x NWM grid of (TN/2) x (TM/NWM)
+// Kernel shape: one workgroup of WN x WM waves computes a TN (channels) x TM (tokens)
+// tile with v_mfma_i32_32x32x32_i8; the waves form a WN x WM grid of (TN/WN) x (TM/WM)
 // sub-tiles.  K advances in 128-byte steps, so every global row segment is a whole
 // cache line; the next step is fetched into registers while the current one is
 // multiplied out of LDS.  LDS rows are 128 bytes with the eight 16-byte chunks
@@ -66,7 +66,6 @@ struct GemmArgs {
 };
 
 constexpr int BK = 128;  // bytes of K per step
-constexpr int BUF_WORD3 = 0x00020000;  // buffer resource word 3 for gfx9-family raw loads
 
 // Byte offset of 16-byte chunk c of LDS row r.  Rows are 128 bytes; the chunk index
 // is XORed with (r ^ r/8) mod 8, so any 16 consecutive rows (16-row aligned) that
@@ -110,19 +109,28 @@ __device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16],
                  (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
 }
 
-template <int TN, int TM, int NWM, int PF>
-__global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
-  constexpr int NTH = 128 * NWM;            // threads: 2 waves along N, NWM along M
-  constexpr int WTM = TM / NWM;             // tokens per wave
-  constexpr int FN = TN / 64;               // 32-row MFMA tiles per wave along N
+// WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  With WDIRECT the
+// weights come pre-packed in MFMA fragment order (wfrag_index) and each wave streams its
+// own fragments from memory straight into registers, one K step ahead; only the token
+// tile goes through LDS.  Otherwise both operands are staged in LDS.
+template <int TN, int TM, int NWAVE, int WN, int PF, bool WDIRECT>
+__global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
+  constexpr int NTH = 64 * NWAVE;
+  constexpr int WM = NWAVE / WN;            // waves along M
+  constexpr int WTN = TN / WN;              // channels per wave
+  constexpr int WTM = TM / WM;              // tokens per wave
+  constexpr int FN = WTN / 32;              // 32-row MFMA tiles per wave along N
   constexpr int FM = WTM / 32;              // 32-col MFMA tiles per wave along M
-  constexpr int LW = TN * (BK / 16) / NTH;  // 16-byte global loads per thread, W tile
+  constexpr int LW = WDIRECT ? 0 : TN * (BK / 16) / NTH;  // 16-byte global loads per thread, W tile
   constexpr int LX = TM * (BK / 16) / NTH;  // same for the X tile
   constexpr int FROWS = NTH / 8;            // rows one pass of the fetch covers
-  static_assert(FM >= 1 && LW >= 1 && LX >= 1 && WTM % 32 == 0 && NTH >= TN, "tile shape");
+  constexpr int KSL = BK / 32;              // 32-byte K slices per step
+  static_assert(FN >= 1 && FM >= 1 && (WDIRECT || LW >= 1) && LX >= 1 && WTM % 32 == 0 && NTH >= TN &&
+                    NWAVE % WN == 0, "tile shape");
+  static_assert(!WDIRECT || PF == 1, "direct weight fragments are fetched one step ahead");
   constexpr int CPW = WTM >= KCHUNK ? WTM / KCHUNK : 1;  // 64-key chunks per wave (V sums)
   // two LDS buffers: the next K step is stored while the current one is multiplied
-  __shared__ __align__(16) int8_t sw[2][TN * BK];
+  __shared__ __align__(16) int8_t sw[WDIRECT ? 1 : 2][WDIRECT ? 16 : TN * BK];
   __shared__ __align__(16) int8_t sx[2][TM * BK];
   __shared__ double ssc[TN];
 
@@ -152,7 +160,7 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wn = wave & 1, wm = wave >> 1;  // wm in [0, NWM)
+  const int wn = wave % WN, wm = wave / WN;
 
   if (tid < TN) ssc[tid] = P.scale[min(n0 + tid, N - 1)];
 
@@ -160,8 +168,9 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // Raw buffer loads: rows past the end of the operand (their whole offset is in the
   // per-lane operand, which the bounds check covers) read as zeros.
   const int fchunk = tid & 7, frow = tid >> 3;  // rows frow + FROWS r
+  // row-major W tile rows from n0 (staged path); the whole packed matrix (direct path)
   const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(P.w + (size_t)n0 * K), (short)0, (N - n0) * K, BUF_WORD3);
+      (void*)(WDIRECT ? P.w : P.w + (size_t)n0 * K), (short)0, WDIRECT ? N * K : (N - n0) * K, BUF_WORD3);
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.x + ((size_t)ub * rows + t0) * K), (short)0, (rows - t0) * K, BUF_WORD3);
   const int foff = frow * K + fchunk * 16;
@@ -170,7 +179,25 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // for the output projection, whose short launch has few tiles per CU; 4 and 6
   // measured slower there)
   static_assert(PF == 1 || PF % 2 == 0, "prefetch depth");
-  v4i rw[PF][LW], rx[PF][LX];
+  v4i rw[PF][LW > 0 ? LW : 1], rx[PF][LX];
+  // direct path: this wave's weight fragments of one K step (FN channel blocks x KSL
+  // slices, 1 KB each, the slices of a block contiguous), two steps in registers.  A
+  // slice past K (odd multiples of 64) meets zero tokens, so its contents do not matter;
+  // reads past the matrix return zeros.
+  v4i wf[2][WDIRECT ? FN : 1][KSL];
+  const int cb0 = (n0 + wn * WTN) >> 5;  // first 32-channel block of this wave
+  auto wfetch = [&](int kt, auto set_tag) {
+    constexpr int SET = decltype(set_tag)::value;
+    if constexpr (WDIRECT) {
+#pragma unroll
+      for (int i = 0; i < FN; ++i) {
+        const int base = __builtin_amdgcn_readfirstlane(((cb0 + i) * (K >> 5) + kt * KSL) * 1024);
+#pragma unroll
+        for (int ks = 0; ks < KSL; ++ks)
+          wf[SET][i][ks] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, lane * 16 + ks * 1024, base, 0);
+      }
+    }
+  };
   // K is a multiple of 64: the last step of an odd multiple fills its upper half with zeros
   auto fetch = [&](int k0, int set) {
     if (k0 + fchunk * 16 < K) {
@@ -195,7 +222,7 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   };
 
   // waves whose channels are V produce the transposed product (tokens along MFMA rows)
-  const int nw0 = n0 + wn * (TN / 2);
+  const int nw0 = n0 + wn * WTN;
   const bool vwave = mode == OUT_QKV && nw0 >= 2 * args.d;
 
   v16i acc[FN][FM];
@@ -211,13 +238,18 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   // branch inside it
   auto kloop = [&](auto swap_tag) {
     constexpr bool SWAP = decltype(swap_tag)::value;
-    auto mma = [&](const int buf) {
+    auto mma = [&](const int buf, auto wset_tag) {
+      constexpr int WSET = decltype(wset_tag)::value;
 #pragma unroll
-      for (int ks = 0; ks < BK / 32; ++ks) {
+      for (int ks = 0; ks < KSL; ++ks) {
         v4i af[FN], bf[FM];
 #pragma unroll
-        for (int i = 0; i < FN; ++i)
-          af[i] = *(const v4i*)(sw[buf] + lds_off(wn * (TN / 2) + i * 32 + frag_row, 2 * ks + half));
+        for (int i = 0; i < FN; ++i) {
+          if constexpr (WDIRECT)
+            af[i] = wf[WSET][i][ks];
+          else
+            af[i] = *(const v4i*)(sw[buf] + lds_off(wn * WTN + i * 32 + frag_row, 2 * ks + half));
+        }
 #pragma unroll
         for (int j = 0; j < FM; ++j)
           bf[j] = *(const v4i*)(sx[buf] + lds_off(wm * WTM + j * 32 + frag_row, 2 * ks + half));
@@ -230,20 +262,32 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
       }
     };
     if constexpr (PF == 1) {
-      // step kt is multiplied out of buffer kt % 2 while step kt + 1 (fetched during
-      // step kt - 1) is stored into the other one; one barrier per step orders both
+      // step k is multiplied out of LDS buffer k % 2 (and weight set k % 2) while step
+      // k + 1 (fetched during step k - 1) is stored into the other buffer; one barrier
+      // per step orders both.  Unrolled twice so that the weight set is static.
+      wfetch(0, std::integral_constant<int, 0>{});
       fetch(0, 0);
       stash(0, 0);
-      if (nk > 1) fetch(BK, 0);
+      if (nk > 1) {
+        fetch(BK, 0);
+        wfetch(1, std::integral_constant<int, 1>{});
+      }
       __syncthreads();
-      for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        mma(cur);
-        if (kt + 1 < nk) {
-          stash(cur ^ 1, 0);
-          if (kt + 2 < nk) fetch((kt + 2) * BK, 0);
-        }
-        __syncthreads();
+      for (int kt = 0; kt < nk; kt += 2) {
+        static_for<2>([&](auto ph) {
+          constexpr int P2 = decltype(ph)::value;  // (kt + P2) % 2
+          if (kt + P2 < nk) {
+            mma(P2, ph);
+            if (kt + P2 + 1 < nk) {
+              stash(P2 ^ 1, 0);
+              if (kt + P2 + 2 < nk) {
+                fetch((kt + P2 + 2) * BK, 0);
+                wfetch(kt + P2 + 2, ph);
+              }
+            }
+            __syncthreads();
+          }
+        });
       }
     } else {
       // step k is fetched into register set k % PF, PF steps before it is stored to
@@ -260,7 +304,7 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
           constexpr int P = decltype(ph)::value;  // (kt + P) % PF
           constexpr int SN = (P + 1) % PF;        // register set of step kt + P + 1
           if (kt + P < nk) {
-            mma(P & 1);
+            mma(P & 1, std::integral_constant<int, 0>{});
             if (kt + P + 1 < nk) {
               stash((P + 1) & 1, SN);
               if (kt + P + 1 + PF < nk) fetch((kt + P + 1 + PF) * BK, SN);
@@ -305,7 +349,7 @@ __global__ __launch_bounds__(128 * NWM) void gemm_i8_requant(GemmArgs args) {
   };
 #pragma unroll
   for (int i = 0; i < FN; ++i) {
-    const int nl = wn * (TN / 2) + i * 32;  // first channel of this sub-tile, tile-local
+    const int nl = wn * WTN + i * 32;  // first channel of this sub-tile, tile-local
     const int nb = n0 + nl;
     if (nb >= N) continue;
     int8_t* dst;
@@ -430,24 +474,28 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWM, int PF>
+template <int TN, int TM, int NWAVE, int WN, int PF, bool WDIRECT>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWM, PF>, dim3(8 * a.per_xcd), dim3(128 * NWM), 0, st, ev, a);
+  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, PF, WDIRECT>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st,
+                       ev, a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
-  constexpr int TN = 256, TM = 256, NWM = 4;
+  // 256 x 256 tiles of eight waves in a 4 x 2 grid (64 channels x 128 tokens each), the
+  // weights streamed from fragment order: per K step a workgroup moves 32 KB of token
+  // tile and 128 KB of token fragments through LDS (both operands staged: 256 KB)
+  constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
   // the epilogue's V sums: a wave's tokens are whole 64-key chunks
-  static_assert((TM / NWM) % KCHUNK == 0 && (TN / 2) % 128 == 0, "projection tile shape");
+  static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
-  return launch_gemm<TN, TM, NWM, 1>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWAVE, WN, 1, true>(a, tiles, st, ev);
 }
 
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
@@ -456,10 +504,30 @@ hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Wor
   fill_dest(a, rs, ws, y);
   // small tiles and two steps of prefetch: with K = d_model and only a few tiles per
   // CU, the K loop waits on load latency rather than on bandwidth
-  constexpr int TN = 64, TM = 64, NWM = 2;
+  constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  return launch_gemm<TN, TM, NWM, 2>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWAVE, WN, 2, false>(a, tiles, st, ev);
+}
+
+// one thread per 16-byte piece of the destination
+__global__ __launch_bounds__(256) void pack_wfrag(const int8_t* __restrict__ w, int8_t* __restrict__ dst, int N,
+                                                  int K) {
+  const long p = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= (long)N * K / 16) return;
+  const int l = (int)(p & 63);
+  const long frag = p >> 6;
+  const int ksl = K >> 5;
+  const int cb = (int)(frag / ksl), ks = (int)(frag - (long)cb * ksl);
+  const int8_t* src = w + (size_t)(cb * 32 + (l & 31)) * K + ks * 32 + (l >> 5) * 16;
+  *(uint4*)(dst + p * 16) = *(const uint4*)src;
+}
+
+hipError_t pack_weight_fragments(const int8_t* w, int8_t* dst, int N, int K, hipStream_t st) {
+  if (N % 32 || K % 32) return hipErrorInvalidValue;
+  const long pieces = (long)N * K / 16;
+  hipLaunchKernelGGL(pack_wfrag, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, st, w, dst, N, K);
+  return hipGetLastError();
 }
 
 }  // namespace ipk

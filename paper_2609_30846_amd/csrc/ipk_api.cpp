@@ -11,6 +11,7 @@
 #include <string.h>
 
 #include <new>
+#include <algorithm>
 #include <vector>
 
 #include "../../include/ipk.h"
@@ -186,11 +187,18 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
     return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
                 hipGetErrorString(e));
   }
-  // weights (device to device), multipliers (host to device)
-  chk(hipMemcpy(h->w.w_qkv, desc->w_q, d * d, hipMemcpyDefault));
-  chk(hipMemcpy(h->w.w_qkv + d * d, desc->w_k, d * d, hipMemcpyDefault));
-  chk(hipMemcpy(h->w.w_qkv + 2 * d * d, desc->w_v, d * d, hipMemcpyDefault));
-  chk(hipMemcpy(h->w.w_pos, desc->w_pos, d * d, hipMemcpyDefault));
+  // weights (device to device), multipliers (host to device).  The Q|K|V and position
+  // weights are kept in MFMA fragment order (the projection kernel streams them straight
+  // into registers): they are staged row-major in the output-projection weight buffer
+  // and rearranged from there, the stacked Q|K|V in one pass.
+  int8_t* stage = nullptr;
+  chk(dev_alloc(h, &stage, 3 * d * d));
+  chk(hipMemcpy(stage, desc->w_q, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(stage + d * d, desc->w_k, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(stage + 2 * d * d, desc->w_v, d * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w.w_qkv, 3 * (int)d, (int)d, nullptr));
+  chk(hipMemcpy(stage, desc->w_pos, d * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w.w_pos, (int)d, (int)d, nullptr));
   chk(hipMemcpy(h->w.w_out, desc->w_out, d * d, hipMemcpyDefault));
   chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
   chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
@@ -217,6 +225,9 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
     (void)hipGetLastError();
     return fail(IPK_ERR_HIP, "copying the weights failed: %s", hipGetErrorString(e));
   }
+  // the staging copy is no longer needed
+  h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), (void*)stage));
+  (void)hipFree(stage);
   *out = h;
   return IPK_OK;
 }

@@ -36,6 +36,7 @@ namespace ipk {
 constexpr int KCHUNK = 64;    // keys per chunk of the A.V contraction (MFMA K = 64)
 constexpr int P_PADLO = 128;  // rows kept before relative-position row 0
 constexpr int P_PADHI = 128;  // rows kept after the last table row
+constexpr int BUF_WORD3 = 0x00020000;  // buffer resource word 3 for gfx9-family raw loads
 
 inline int round_up(int v, int m) { return (v + m - 1) / m * m; }
 inline int t_aligned(int T) { return round_up(T, KCHUNK); }
@@ -56,9 +57,18 @@ struct Workspace {
   int32_t* vsum;
 };
 
+// Fragment order of a weight matrix W [N][K] (N, K multiples of 32) for the A operand of
+// v_mfma_i32_32x32x32_i8: the fragment of channels 32 cb .. 32 cb + 31 and bytes
+// 32 ks .. 32 ks + 31 is the 1 KB block (cb K/32 + ks), and the lane l that feeds channel
+// 32 cb + l % 32 with bytes 32 ks + 16 (l / 32) .. + 15 finds them at byte 16 l of it.
+__host__ __device__ inline size_t wfrag_index(int n, int k, int K) {
+  return ((size_t)(n >> 5) * (K >> 5) + (k >> 5)) * 1024 + (size_t)(((((k >> 4) & 1) << 5) + (n & 31)) << 4) +
+         (k & 15);
+}
+
 struct Weights {
-  int8_t* w_qkv;       // [3d][d]: w_q, w_k, w_v stacked
-  int8_t* w_pos;       // [d][d]
+  int8_t* w_qkv;       // [3d][d]: w_q, w_k, w_v stacked, in fragment order (wfrag_index)
+  int8_t* w_pos;       // [d][d], in fragment order
   int8_t* w_out;       // [d][d]
   int8_t *u, *v;       // [H][DK]
   // per-output-channel requantization scales m * 2^-n (exact in float64)
@@ -126,6 +136,9 @@ struct AttnPlan {
   int nqb2;
 };
 AttnPlan attn_plan(int DK, int T_al, long bh_count, int T);
+
+// Rearranges a row-major int8 matrix [N][K] into fragment order (wfrag_index).
+hipError_t pack_weight_fragments(const int8_t* w, int8_t* dst, int N, int K, hipStream_t st);
 
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st);
