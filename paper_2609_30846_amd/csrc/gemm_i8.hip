@@ -8,15 +8,19 @@
 // Kernel shape: one workgroup of WN x WM waves computes a TN (channels) x TM (tokens)
 // tile with v_mfma_i32_32x32x32_i8; the waves form a WN x WM grid of (TN/WN) x (TM/WM)
 // sub-tiles.  K advances in 128-byte steps, so every global row segment is a whole
-// cache line; the next step is fetched into registers while the current one is
-// multiplied out of LDS.  LDS rows are 128 bytes with the eight 16-byte chunks
-// XOR-swizzled by the row index, which keeps both the 16-byte stores of the fetch
-// and the 16-byte MFMA operand reads free of bank conflicts.
+// cache line.  The weights are stored in MFMA operand-fragment order (each 32-channel x
+// 32-byte fragment a contiguous 1 KB block in lane order), so every wave loads its own
+// weight fragments straight into registers with fully coalesced 16-byte loads, one K
+// step ahead.  The token tile is fetched into registers one step ahead and staged in
+// LDS, whose rows are 128 bytes with the eight 16-byte chunks XOR-swizzled by the row
+// index, which keeps both the 16-byte stores of the fetch and the 16-byte MFMA operand
+// reads free of bank conflicts.
 //
-// The large projections use 256 x 256 tiles of eight waves (two per SIMD, 128 x 64
-// outputs each, accumulators in VGPRs).  A K step then moves 192 KB of MFMA fragments
-// and 64 KB of staged tile through LDS, which at 128 bytes per clock per CU takes
-// longer than the step's matrix-core work: LDS bandwidth, not MFMA, bounds the loop.
+// The large projections use 256 x 256 tiles of eight waves (two per SIMD, 64 channels x
+// 128 tokens each, accumulators in VGPRs).  Per K step a workgroup then moves 32 KB of
+// token tile and 128 KB of token fragments through LDS and streams 64 KB of weight
+// fragments (each block read by the two waves that share its channels); with both
+// operands staged in LDS the step moved 256 KB through LDS and ran about 17 % slower.
 //
 // Token tiles never straddle two utterances (each utterance is tiled on its own), so
 // every destination layout receives whole aligned 16-byte pieces.  Tiles are dealt
@@ -109,11 +113,11 @@ __device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16],
                  (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
 }
 
-// WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  With WDIRECT the
-// weights come pre-packed in MFMA fragment order (wfrag_index) and each wave streams its
-// own fragments from memory straight into registers, one K step ahead; only the token
-// tile goes through LDS.  Otherwise both operands are staged in LDS.
-template <int TN, int TM, int NWAVE, int WN, int PF, bool WDIRECT>
+// WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  The weights
+// come pre-packed in MFMA fragment order (wfrag_index): each wave streams its own
+// fragments from memory straight into registers, one K step ahead, and only the token
+// tile goes through LDS.
+template <int TN, int TM, int NWAVE, int WN>
 __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 64 * NWAVE;
   constexpr int WM = NWAVE / WN;            // waves along M
@@ -121,16 +125,12 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int WTM = TM / WM;              // tokens per wave
   constexpr int FN = WTN / 32;              // 32-row MFMA tiles per wave along N
   constexpr int FM = WTM / 32;              // 32-col MFMA tiles per wave along M
-  constexpr int LW = WDIRECT ? 0 : TN * (BK / 16) / NTH;  // 16-byte global loads per thread, W tile
-  constexpr int LX = TM * (BK / 16) / NTH;  // same for the X tile
+  constexpr int LX = TM * (BK / 16) / NTH;  // 16-byte global loads per thread of the token tile
   constexpr int FROWS = NTH / 8;            // rows one pass of the fetch covers
   constexpr int KSL = BK / 32;              // 32-byte K slices per step
-  static_assert(FN >= 1 && FM >= 1 && (WDIRECT || LW >= 1) && LX >= 1 && WTM % 32 == 0 && NTH >= TN &&
-                    NWAVE % WN == 0, "tile shape");
-  static_assert(!WDIRECT || PF == 1, "direct weight fragments are fetched one step ahead");
+  static_assert(FN >= 1 && FM >= 1 && LX >= 1 && WTM % 32 == 0 && NTH >= TN && NWAVE % WN == 0, "tile shape");
   constexpr int CPW = WTM >= KCHUNK ? WTM / KCHUNK : 1;  // 64-key chunks per wave (V sums)
   // two LDS buffers: the next K step is stored while the current one is multiplied
-  __shared__ __align__(16) int8_t sw[WDIRECT ? 1 : 2][WDIRECT ? 16 : TN * BK];
   __shared__ __align__(16) int8_t sx[2][TM * BK];
   __shared__ double ssc[TN];
 
@@ -168,57 +168,42 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   // Raw buffer loads: rows past the end of the operand (their whole offset is in the
   // per-lane operand, which the bounds check covers) read as zeros.
   const int fchunk = tid & 7, frow = tid >> 3;  // rows frow + FROWS r
-  // row-major W tile rows from n0 (staged path); the whole packed matrix (direct path)
-  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(WDIRECT ? P.w : P.w + (size_t)n0 * K), (short)0, WDIRECT ? N * K : (N - n0) * K, BUF_WORD3);
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc((void*)P.w, (short)0, N * K, BUF_WORD3);
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.x + ((size_t)ub * rows + t0) * K), (short)0, (rows - t0) * K, BUF_WORD3);
   const int foff = frow * K + fchunk * 16;
 
-  // PF register sets: a K step is fetched PF steps before it is stored to LDS (PF = 2
-  // for the output projection, whose short launch has few tiles per CU; 4 and 6
-  // measured slower there)
-  static_assert(PF == 1 || PF % 2 == 0, "prefetch depth");
-  v4i rw[PF][LW > 0 ? LW : 1], rx[PF][LX];
-  // direct path: this wave's weight fragments of one K step (FN channel blocks x KSL
-  // slices, 1 KB each, the slices of a block contiguous), two steps in registers.  A
-  // slice past K (odd multiples of 64) meets zero tokens, so its contents do not matter;
-  // reads past the matrix return zeros.
-  v4i wf[2][WDIRECT ? FN : 1][KSL];
+  // the next step's token tile in registers
+  v4i rx[LX];
+  // this wave's weight fragments of one K step (FN channel blocks x KSL slices, 1 KB
+  // each, the slices of a block contiguous), two steps in registers.  A slice past K
+  // (odd multiples of 64) meets zero tokens, so its contents do not matter; reads past
+  // the matrix return zeros.
+  v4i wf[2][FN][KSL];
   const int cb0 = (n0 + wn * WTN) >> 5;  // first 32-channel block of this wave
   auto wfetch = [&](int kt, auto set_tag) {
     constexpr int SET = decltype(set_tag)::value;
-    if constexpr (WDIRECT) {
 #pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const int base = __builtin_amdgcn_readfirstlane(((cb0 + i) * (K >> 5) + kt * KSL) * 1024);
+    for (int i = 0; i < FN; ++i) {
+      const int base = __builtin_amdgcn_readfirstlane(((cb0 + i) * (K >> 5) + kt * KSL) * 1024);
 #pragma unroll
-        for (int ks = 0; ks < KSL; ++ks)
-          wf[SET][i][ks] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, lane * 16 + ks * 1024, base, 0);
-      }
+      for (int ks = 0; ks < KSL; ++ks)
+        wf[SET][i][ks] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, lane * 16 + ks * 1024, base, 0);
     }
   };
   // K is a multiple of 64: the last step of an odd multiple fills its upper half with zeros
-  auto fetch = [&](int k0, int set) {
+  auto fetch = [&](int k0) {
     if (k0 + fchunk * 16 < K) {
 #pragma unroll
-      for (int r = 0; r < LW; ++r)
-        rw[set][r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(wres, foff + FROWS * r * K + k0, 0, 0);
-#pragma unroll
-      for (int r = 0; r < LX; ++r)
-        rx[set][r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
+      for (int r = 0; r < LX; ++r) rx[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
     } else {
 #pragma unroll
-      for (int r = 0; r < LW; ++r) rw[set][r] = (v4i){};
-#pragma unroll
-      for (int r = 0; r < LX; ++r) rx[set][r] = (v4i){};
+      for (int r = 0; r < LX; ++r) rx[r] = (v4i){};
     }
   };
-  auto stash = [&](int buf, int set) {
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int r = 0; r < LW; ++r) *(v4i*)(sw[buf] + lds_off(frow + FROWS * r, fchunk)) = rw[set][r];
-#pragma unroll
-    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[set][r];
+    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[r];
   };
 
   // waves whose channels are V produce the transposed product (tokens along MFMA rows)
@@ -242,14 +227,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       constexpr int WSET = decltype(wset_tag)::value;
 #pragma unroll
       for (int ks = 0; ks < KSL; ++ks) {
-        v4i af[FN], bf[FM];
-#pragma unroll
-        for (int i = 0; i < FN; ++i) {
-          if constexpr (WDIRECT)
-            af[i] = wf[WSET][i][ks];
-          else
-            af[i] = *(const v4i*)(sw[buf] + lds_off(wn * WTN + i * 32 + frag_row, 2 * ks + half));
-        }
+        v4i bf[FM];
 #pragma unroll
         for (int j = 0; j < FM; ++j)
           bf[j] = *(const v4i*)(sx[buf] + lds_off(wm * WTM + j * 32 + frag_row, 2 * ks + half));
@@ -257,62 +235,36 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
         for (int i = 0; i < FN; ++i)
 #pragma unroll
           for (int j = 0; j < FM; ++j)
-            acc[i][j] = SWAP ? __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[j], af[i], acc[i][j], 0, 0, 0)
-                             : __builtin_amdgcn_mfma_i32_32x32x32_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = SWAP ? __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[j], wf[WSET][i][ks], acc[i][j], 0, 0, 0)
+                             : __builtin_amdgcn_mfma_i32_32x32x32_i8(wf[WSET][i][ks], bf[j], acc[i][j], 0, 0, 0);
       }
     };
-    if constexpr (PF == 1) {
-      // step k is multiplied out of LDS buffer k % 2 (and weight set k % 2) while step
-      // k + 1 (fetched during step k - 1) is stored into the other buffer; one barrier
-      // per step orders both.  Unrolled twice so that the weight set is static.
-      wfetch(0, std::integral_constant<int, 0>{});
-      fetch(0, 0);
-      stash(0, 0);
-      if (nk > 1) {
-        fetch(BK, 0);
-        wfetch(1, std::integral_constant<int, 1>{});
-      }
-      __syncthreads();
-      for (int kt = 0; kt < nk; kt += 2) {
-        static_for<2>([&](auto ph) {
-          constexpr int P2 = decltype(ph)::value;  // (kt + P2) % 2
-          if (kt + P2 < nk) {
-            mma(P2, ph);
-            if (kt + P2 + 1 < nk) {
-              stash(P2 ^ 1, 0);
-              if (kt + P2 + 2 < nk) {
-                fetch((kt + P2 + 2) * BK, 0);
-                wfetch(kt + P2 + 2, ph);
-              }
+    // step k is multiplied out of LDS buffer k % 2 (and weight set k % 2) while step
+    // k + 1 (fetched during step k - 1) is stored into the other buffer; one barrier
+    // per step orders both.  Unrolled twice so that the weight set is static.
+    wfetch(0, std::integral_constant<int, 0>{});
+    fetch(0);
+    stash(0);
+    if (nk > 1) {
+      fetch(BK);
+      wfetch(1, std::integral_constant<int, 1>{});
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      static_for<2>([&](auto ph) {
+        constexpr int P2 = decltype(ph)::value;  // (kt + P2) % 2
+        if (kt + P2 < nk) {
+          mma(P2, ph);
+          if (kt + P2 + 1 < nk) {
+            stash(P2 ^ 1);
+            if (kt + P2 + 2 < nk) {
+              fetch((kt + P2 + 2) * BK);
+              wfetch(kt + P2 + 2, ph);
             }
-            __syncthreads();
           }
-        });
-      }
-    } else {
-      // step k is fetched into register set k % PF, PF steps before it is stored to
-      // LDS buffer k % 2 (PF is even, so both indices are static in a loop unrolled PF
-      // times); one barrier per step
-#pragma unroll
-      for (int st = 0; st < PF; ++st)
-        if (st < nk) fetch(st * BK, st);
-      stash(0, 0);
-      if (PF < nk) fetch(PF * BK, 0);
-      __syncthreads();
-      for (int kt = 0; kt < nk; kt += PF) {
-        static_for<PF>([&](auto ph) {
-          constexpr int P = decltype(ph)::value;  // (kt + P) % PF
-          constexpr int SN = (P + 1) % PF;        // register set of step kt + P + 1
-          if (kt + P < nk) {
-            mma(P & 1, std::integral_constant<int, 0>{});
-            if (kt + P + 1 < nk) {
-              stash((P + 1) & 1, SN);
-              if (kt + P + 1 + PF < nk) fetch((kt + P + 1 + PF) * BK, SN);
-            }
-            __syncthreads();
-          }
-        });
-      }
+          __syncthreads();
+        }
+      });
     }
   };
   if (vwave) kloop(std::true_type{});
@@ -474,40 +426,39 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWAVE, int WN, int PF, bool WDIRECT>
+template <int TN, int TM, int NWAVE, int WN>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, PF, WDIRECT>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st,
-                       ev, a);
+  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev, a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, nullptr);
-  // 256 x 256 tiles of eight waves in a 4 x 2 grid (64 channels x 128 tokens each), the
-  // weights streamed from fragment order: per K step a workgroup moves 32 KB of token
-  // tile and 128 KB of token fragments through LDS (both operands staged: 256 KB)
+  // 256 x 256 tiles of eight waves in a 4 x 2 grid (64 channels x 128 tokens each): per
+  // K step a workgroup moves 32 KB of token tile and 128 KB of token fragments through
+  // LDS and streams 64 KB of weight fragments (each wave's own, two waves per block)
   constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
   // the epilogue's V sums: a wave's tokens are whole 64-key chunks
   static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
   tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
   a.nprob = 2;
-  return launch_gemm<TN, TM, NWAVE, WN, 1, true>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
 }
 
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
                                  hipStream_t st, const LaunchEv& ev) {
   GemmArgs a{};
   fill_dest(a, rs, ws, y);
-  // small tiles and two steps of prefetch: with K = d_model and only a few tiles per
-  // CU, the K loop waits on load latency rather than on bandwidth
+  // small tiles (640 at T = 2500): with K = d_model and few 64-token blocks the launch
+  // is bound by load latency, and larger tiles measured no faster
   constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  return launch_gemm<TN, TM, NWAVE, WN, 2, false>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
 }
 
 // one thread per 16-byte piece of the destination

@@ -187,10 +187,10 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
     return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
                 hipGetErrorString(e));
   }
-  // weights (device to device), multipliers (host to device).  The Q|K|V and position
-  // weights are kept in MFMA fragment order (the projection kernel streams them straight
-  // into registers): they are staged row-major in the output-projection weight buffer
-  // and rearranged from there, the stacked Q|K|V in one pass.
+  // weights (device to device), multipliers (host to device).  Every weight matrix is
+  // kept in MFMA fragment order (the projection kernels stream them straight into
+  // registers): each is staged row-major in a temporary buffer and rearranged from
+  // there, the stacked Q|K|V in one pass.
   int8_t* stage = nullptr;
   chk(dev_alloc(h, &stage, 3 * d * d));
   chk(hipMemcpy(stage, desc->w_q, d * d, hipMemcpyDefault));
@@ -199,7 +199,8 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(pack_weight_fragments(stage, h->w.w_qkv, 3 * (int)d, (int)d, nullptr));
   chk(hipMemcpy(stage, desc->w_pos, d * d, hipMemcpyDefault));
   chk(pack_weight_fragments(stage, h->w.w_pos, (int)d, (int)d, nullptr));
-  chk(hipMemcpy(h->w.w_out, desc->w_out, d * d, hipMemcpyDefault));
+  chk(hipMemcpy(stage, desc->w_out, d * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w.w_out, (int)d, (int)d, nullptr));
   chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
   chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
   // Eq. 7 scales m * 2^-n: m < 2^23 and n <= 40, so each is an exact double

@@ -69,7 +69,7 @@ __host__ __device__ inline size_t wfrag_index(int n, int k, int K) {
 struct Weights {
   int8_t* w_qkv;       // [3d][d]: w_q, w_k, w_v stacked, in fragment order (wfrag_index)
   int8_t* w_pos;       // [d][d], in fragment order
-  int8_t* w_out;       // [d][d]
+  int8_t* w_out;       // [d][d], in fragment order
   int8_t *u, *v;       // [H][DK]
   // per-output-channel requantization scales m * 2^-n (exact in float64)
   double* scale_qkv;  // [3d]
