@@ -65,6 +65,15 @@ def lib():
             L.ipk_oracle_iexp.argtypes = [C.c_int64, C.c_int64, C.c_int64, C.c_int64]
             L.ipk_oracle_softmax_row.restype = None
             L.ipk_oracle_softmax_row.argtypes = [i64p, C.c_int32, C.c_int64, C.c_int64, C.c_int64, u8p]
+            L.ipk_oracle_isqrt.restype = C.c_int64
+            L.ipk_oracle_isqrt.argtypes = [C.c_int64]
+            L.ipk_oracle_layernorm_row.restype = None
+            L.ipk_oracle_layernorm_row.argtypes = [i8p, C.c_int32, i32p, i64p, C.c_int32, i8p]
+            L.ipk_oracle_residual.restype = C.c_int64
+            L.ipk_oracle_residual.argtypes = [C.c_int64, C.c_int64, C.c_int64, C.c_int64, C.c_int32]
+            L.ipk_oracle_mhsa_residual.restype = C.c_int
+            L.ipk_oracle_mhsa_residual.argtypes = [C.POINTER(OracleDesc), i32p, i64p, C.c_int32, C.c_int32, C.c_int32,
+                                                   C.c_int32, i8p, i8p, i32p, C.c_int32, C.c_int32, i8p, i8p, i8p]
             L.ipk_oracle_relpos_attn.restype = C.c_int
             L.ipk_oracle_relpos_attn.argtypes = [C.POINTER(OracleDesc), i8p, i8p, i32p, C.c_int32, C.c_int32,
                                                  i8p, C.POINTER(OracleTrace)]
@@ -191,3 +200,56 @@ def stack(wl, layers: Optional[int] = None) -> np.ndarray:
     for blk in wl.blocks[: (layers or len(wl.blocks))]:
         x = relpos_attn(blk, x=x)
     return x
+
+
+# ---- the MHSA residual sub-module of Eq. 2 (LayerNorm, block, residual add)
+
+
+def isqrt(n: int) -> int:
+    """I-BERT's integer square root, floor(sqrt(n))."""
+    return int(lib().ipk_oracle_isqrt(int(n)))
+
+
+def layernorm(z: np.ndarray, res) -> np.ndarray:
+    """Integer LayerNorm of every row of z [..., d] into the block's input grid."""
+    z = np.ascontiguousarray(z, dtype=np.int8)
+    d = z.shape[-1]
+    flat = z.reshape(-1, d)
+    g = np.ascontiguousarray(res.ln_mult, dtype=np.int32)
+    c = np.ascontiguousarray(res.ln_bias, dtype=np.int64)
+    out = np.empty_like(flat)
+    for r in range(flat.shape[0]):
+        lib().ipk_oracle_layernorm_row(_p(flat[r], i8p), d, _p(g, i32p), _p(c, i64p), int(res.ln_shift),
+                                       _p(out[r], i8p))
+    return out.reshape(z.shape)
+
+
+def residual(z1: int, y: int, m_z: int, m_y: int, shift: int) -> int:
+    return int(lib().ipk_oracle_residual(int(z1), int(y), int(m_z), int(m_y), int(shift)))
+
+
+def mhsa_residual(blk, res, z1: Optional[np.ndarray] = None, lengths: Optional[np.ndarray] = None,
+                  trace: bool = False):
+    """Z2 = residual(Z1, block(LN(Z1))) on host memory ([B][T][d] int8); with trace,
+    also returns the LayerNorm output x and the block output y."""
+    z1 = blk.x if z1 is None else z1
+    z1 = np.ascontiguousarray(z1, dtype=np.int8)
+    B, T, d = z1.shape
+    lengths = blk.lengths if lengths is None else lengths
+    lens = np.ascontiguousarray(lengths, dtype=np.int32)
+    pe = np.ascontiguousarray(blk.pos_table, dtype=np.int8)
+    assert pe.shape == (2 * T - 1, d)
+    D, keep = make_desc(blk)
+    g = np.ascontiguousarray(res.ln_mult, dtype=np.int32)
+    c = np.ascontiguousarray(res.ln_bias, dtype=np.int64)
+    z2 = np.empty_like(z1)
+    x = np.empty_like(z1) if trace else None
+    y = np.empty_like(z1) if trace else None
+    rc = lib().ipk_oracle_mhsa_residual(C.byref(D), _p(g, i32p), _p(c, i64p), int(res.ln_shift), int(res.m_z),
+                                        int(res.m_y), int(res.shift_r), _p(z1, i8p), _p(pe, i8p), _p(lens, i32p),
+                                        B, T, _p(z2, i8p), _p(x, i8p) if trace else None,
+                                        _p(y, i8p) if trace else None)
+    del keep
+    if rc != 0:
+        raise ValueError(f"oracle rejected its arguments (status {rc})")
+    return (z2, {"x": x, "y": y}) if trace else z2

@@ -220,3 +220,95 @@ int ipk_oracle_relpos_attn(const oracle_desc* D, const int8_t* x, const int8_t* 
   free(Q); free(K); free(V); free(P); free(ctx);
   return 0;
 }
+
+/* ------------------------------------------------------------------------------
+ * The MHSA residual sub-module of Eq. 2: Z2 = Z1 + MHSA(LN(Z1)), on integer grids.
+ * The paper takes LayerNorm from I-BERT; the integer steps below are this oracle's
+ * reading of it (kept with the design notes):
+ *  - mean mu = round(sum / d), ties upward;
+ *  - y = z - mu, sigma = floor(sqrt(sum y^2)) by I-BERT's integer Newton iteration
+ *    (at least 1);
+ *  - F = floor(2^31 / sigma) and u = floor(y F / 2), so u ~ 2^30 (z - mean) / sigma,
+ *    i.e. the normalized value (z - mean) / std is u sqrt(d) / 2^30;
+ *  - the affine gamma, beta and the move to the MHSA input grid S_x are one
+ *    fixed-point step per channel: x = clamp8(floor((u g + c + 2^(n-1)) / 2^n)) with
+ *    g = round(2^n sqrt(d) gamma / (2^30 S_x)) and c = round(2^n beta / S_x).
+ *  - the residual add requantizes both terms to Z2's grid in one step, as Eq. 11
+ *    does for the two score branches: z2 = clamp8(floor((m_z z1 + m_y y + 2^(n-1))
+ *    / 2^n)) with m_z = round(2^n S_z1 / S_z2), m_y = round(2^n S_y / S_z2).
+ * ------------------------------------------------------------------------------ */
+
+/* floor(a / b) for b > 0 */
+static int64_t floor_div(int64_t a, int64_t b) {
+  int64_t q = a / b;
+  if ((a % b) != 0 && a < 0) q -= 1;
+  return q;
+}
+
+/* I-BERT's integer square root: floor(sqrt(n)) for n >= 0.  Newton's iteration on
+ * integers, x <- floor((x + floor(n / x)) / 2), started at a power of two not below
+ * the root, decreases strictly until it reaches the floor of the root. */
+int64_t ipk_oracle_isqrt(int64_t n) {
+  if (n <= 0) return 0;
+  int bits = 0;
+  for (int64_t t = n; t > 0; t >>= 1) ++bits;
+  int64_t x = (int64_t)1 << ((bits + 1) / 2);
+  for (;;) {
+    const int64_t nx = (x + n / x) / 2;
+    if (nx >= x) return x;
+    x = nx;
+  }
+}
+
+/* Integer LayerNorm of one row of d int8 values (steps as listed above). */
+void ipk_oracle_layernorm_row(const int8_t* z, int32_t d, const int32_t* g, const int64_t* c, int32_t shift,
+                              int8_t* x) {
+  int64_t s = 0;
+  for (int32_t k = 0; k < d; ++k) s += z[k];
+  const int64_t mu = floor_div(2 * s + d, 2 * (int64_t)d);
+  int64_t v = 0;
+  for (int32_t k = 0; k < d; ++k) v += (z[k] - mu) * (z[k] - mu);
+  int64_t sigma = ipk_oracle_isqrt(v);
+  if (sigma < 1) sigma = 1;
+  const int64_t F = ((int64_t)1 << 31) / sigma;
+  const int64_t half = (int64_t)1 << (shift - 1);
+  for (int32_t k = 0; k < d; ++k) {
+    const int64_t u = floor_div_pow2((z[k] - mu) * F, 1);
+    x[k] = (int8_t)ipk_oracle_clamp8(floor_div_pow2(u * g[k] + c[k] + half, shift));
+  }
+}
+
+/* Eq. 2's residual add of one element on integer grids. */
+int64_t ipk_oracle_residual(int64_t z1, int64_t y, int64_t m_z, int64_t m_y, int32_t shift) {
+  return ipk_oracle_clamp8(floor_div_pow2(m_z * z1 + m_y * y + ((int64_t)1 << (shift - 1)), shift));
+}
+
+/* The sub-module on [B][T][d]: x = LN(z1) row by row, y = the block on x, z2 =
+ * residual(z1, y).  x_out and y_out (may be NULL) receive the intermediates.
+ * Returns 0, or -1 on an invalid argument. */
+int ipk_oracle_mhsa_residual(const oracle_desc* D, const int32_t* ln_g, const int64_t* ln_c, int32_t ln_shift,
+                             int32_t m_z, int32_t m_y, int32_t shift_r, const int8_t* z1, const int8_t* pos_table,
+                             const int32_t* lengths, int32_t B, int32_t T, int8_t* z2, int8_t* x_out, int8_t* y_out) {
+  if (!D || !ln_g || !ln_c || !z1 || !z2 || B < 1 || T < 1 || ln_shift < 1 || ln_shift > 62 || shift_r < 1 ||
+      shift_r > 40)
+    return -1;
+  const int32_t d = D->d_model;
+  const int64_t rows = (int64_t)B * T;
+  int8_t* x = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* y = (int8_t*)malloc((size_t)(rows * d));
+  if (!x || !y) {
+    free(x);
+    free(y);
+    return -1;
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) ipk_oracle_layernorm_row(z1 + r * d, d, ln_g, ln_c, ln_shift, x + r * d);
+  const int rc = ipk_oracle_relpos_attn(D, x, pos_table, lengths, B, T, y, NULL);
+  if (rc == 0)
+    for (int64_t i = 0; i < rows * d; ++i) z2[i] = (int8_t)ipk_oracle_residual(z1[i], y[i], m_z, m_y, shift_r);
+  if (rc == 0 && x_out) memcpy(x_out, x, (size_t)(rows * d));
+  if (rc == 0 && y_out) memcpy(y_out, y, (size_t)(rows * d));
+  free(x);
+  free(y);
+  return rc;
+}

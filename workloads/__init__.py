@@ -10,9 +10,11 @@ score, softmax or requantization of data).
 from .generate import (  # noqa: F401
     CONFIGS,
     Block,
+    Residual,
     Workload,
     config_by_name,
     make_block,
+    make_residual,
     make_workload,
     sinusoid_table,
 )

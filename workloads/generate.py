@@ -292,3 +292,62 @@ def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = No
         S_x = blk.scales["S_y"]
         lengths = blk.lengths
     return Workload(shape=shape, regime=regime, seed=seed, blocks=blocks)
+
+
+# ---------------------------------------------------------------------------------
+# The MHSA residual sub-module of Eq. 2, Z2 = Z1 + MHSA(LN(Z1)): the block's input x
+# becomes Z1, LayerNorm maps it to the block's input grid S_x, and the residual add
+# maps Z1 and the block output y (grid S_y) to Z2's grid.  LayerNorm's gamma and beta
+# are drawn per channel (no trained weights exist): gamma ~ U[0.5, 1.5],
+# beta ~ U[-0.25, 0.25].  Literal regime: S_z1 and S_z2 ~ U[2^-8, 2^-4]; calibrated:
+# Z1 has unit variance (S_z1 = 1 / sigma of its int8 draw) and S_z2 covers +-4 standard
+# deviations of Z1 + y.
+LN_SHIFT = 40  # fixed-point shift of the LayerNorm affine step
+LN_UNIT = 30  # I-BERT's normalized value carries 2^30 / sqrt(d) per unit
+
+
+@dataclasses.dataclass
+class Residual:
+    """Integer parameters of the sub-module and the real values they came from."""
+
+    ln_mult: np.ndarray  # int32 [d]: round(2^LN_SHIFT sqrt(d) gamma / (2^LN_UNIT S_x))
+    ln_bias: np.ndarray  # int64 [d]: round(2^LN_SHIFT beta / S_x)
+    ln_shift: int
+    m_z: int  # round(2^n S_z1 / S_z2)
+    m_y: int  # round(2^n S_y / S_z2)
+    shift_r: int
+    scales: Dict[str, object]
+
+
+def _round_dec(v: Decimal) -> int:
+    return int((v + Decimal("0.5")).to_integral_value(rounding=ROUND_FLOOR))
+
+
+def make_residual(blk: Block, regime: str, seed: int) -> Residual:
+    """Draws LayerNorm's gamma, beta and the grids of Z1 and Z2 for one block (a
+    generator of its own, so the block's draws are unchanged)."""
+    rng = np.random.default_rng(seed)
+    d = blk.shape.d_model
+    gamma = rng.uniform(0.5, 1.5, size=d)
+    beta = rng.uniform(-0.25, 0.25, size=d)
+    S_x, S_y = blk.scales["S_x"], blk.scales["S_y"]
+    if regime == "literal":
+        S_z1, S_z2 = (float(rng.uniform(SCALE_LO, SCALE_HI)) for _ in range(2))
+    elif regime == "calibrated":
+        S_z1 = 1.0 / _sigma_x(blk.shape)
+        sy = S_y * 127.0 / 4.0  # y's grid covers +-4 of its standard deviations
+        S_z2 = 4.0 * math.sqrt(1.0 + sy * sy) / 127.0
+    else:
+        raise ValueError(regime)
+    two_n = Decimal(2) ** LN_SHIFT
+    unit = Decimal(2) ** LN_UNIT
+    sqrt_d = Decimal(d).sqrt()
+    sx = _dec(S_x)
+    g = np.array([_round_dec(two_n * sqrt_d * _dec(gm) / (unit * sx)) for gm in gamma], dtype=np.int64)
+    c = np.array([_round_dec(two_n * _dec(bt) / sx) for bt in beta], dtype=np.int64)
+    if np.any(np.abs(g) >= (1 << 24)):
+        raise ValueError("LayerNorm multiplier outside (-2^24, 2^24)")
+    return Residual(ln_mult=g.astype(np.int32), ln_bias=c, ln_shift=LN_SHIFT,
+                    m_z=fixed_point(_dec(S_z1) / _dec(S_z2)), m_y=fixed_point(_dec(S_y) / _dec(S_z2)),
+                    shift_r=SHIFT_N,
+                    scales={"S_z1": S_z1, "S_z2": S_z2, "S_x": S_x, "S_y": S_y, "gamma": gamma, "beta": beta})
