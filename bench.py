@@ -107,7 +107,7 @@ def main():
         return
 
     from paper_2609_30846_amd import ipk
-    from workloads import make_workload
+    from workloads import make_residual, make_workload
 
     ipk.load()  # fails loudly when the HIP library is missing
     wl = make_workload(args.workload, args.regime)
@@ -164,6 +164,29 @@ def main():
             stage_ms[i] += row[i].elapsed_time(row[i + 1])
     stage_ms /= n_stage
 
+    # two variants on the same input, timed like the main region over n_stage steps:
+    # the position projection kept on the handle (the paper computes q_P offline), and
+    # the MHSA module of Eq. 2 (integer LayerNorm, the block, the residual add)
+    def timed(fn, n):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    y_kept = torch.empty_like(x)
+    mod.cache_positions(pe, stream=stream)
+    ms_kept = timed(lambda: mod(x, None, lengths=lengths, y=y_kept, stream=stream), n_stage)
+    z2 = torch.empty_like(x)
+    mod.set_residual_from(make_residual(blk, args.regime, seed=wl.seed + 1))
+    ms_module = timed(lambda: mod.residual(x, pe, lengths=lengths, z2=z2, stream=stream), n_stage)
+    y_kept_matches = bool(torch.equal(y_kept, y))
+
     proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
     ops = 2 * (proj + pos + attn)
     tops = ops / (ms_step * 1e-3) / 1e12
@@ -196,6 +219,19 @@ def main():
         "stage_ms": {n: round(float(v), 5) for n, v in zip(stage_names, stage_ms)},
         "stage_timing": f"separate pass of {n_stage} steps with per-kernel HIP events on the launch stream",
         "wall_s_timed_region": round(wall, 4),
+        "variants": {
+            "kept_position_projection": {
+                "ms_per_step": round(ms_kept, 5),
+                "frames_per_s": round(float(np.sum(lengths)) / (ms_kept * 1e-3), 1),
+                "tops_without_position_projection": round(2 * (proj + attn) / (ms_kept * 1e-3) / 1e12, 3),
+                "output_equals_per_call_table": y_kept_matches,
+            },
+            "mhsa_module_layernorm_residual": {
+                "ms_per_step": round(ms_module, 5),
+                "frames_per_s": round(float(np.sum(lengths)) / (ms_module * 1e-3), 1),
+            },
+            "timing": f"{n_stage} steps each between two HIP events, after 5 warm-up steps",
+        },
         "roofline": {
             "kernel": "relpos_attn_core",
             "bound": "mfma",

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define IPK_ABI_VERSION 1
+#define IPK_ABI_VERSION 2
 
 /* Status codes. */
 typedef enum ipk_status {
@@ -108,7 +108,8 @@ int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t**
  * Runs the block on `stream` (a hipStream_t; NULL is the default stream).
  * x        DEVICE int8 [B][T][d_model]   block input
  * pos_table DEVICE int8 [2T-1][d_model]  sinusoidal relative-position table; row r
- *                                        holds relative position T-1-r
+ *                                        holds relative position T-1-r; NULL uses the
+ *                                        projection kept by ipk_relpos_attn_cache_positions
  * lengths  HOST int32 [B] valid frames L_b in [1, T], or NULL for all T; the values
  *          are captured when the call returns (the array may be reused at once)
  * y        DEVICE int8 [B][T][d_model]   block output; rows t >= L_b are zero
@@ -117,8 +118,9 @@ int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t**
  * until the stream work completes.  The handle's workspace is shared by all calls:
  * calls on one handle must be ordered on one stream (calls on different streams
  * race).  x and y may not overlap.
- * Errors: IPK_ERR_INVALID_ARG (null handle/x/pos_table/y, B < 1, T < 1,
- * B > max_batch, T > max_T, a length outside [1, T]); IPK_ERR_HIP (launch failure).
+ * Errors: IPK_ERR_INVALID_ARG (null handle/x/y, B < 1, T < 1, B > max_batch,
+ * T > max_T, a length outside [1, T], a NULL pos_table with no kept projection of at
+ * least T rows); IPK_ERR_HIP (launch failure).
  * On an error nothing is enqueued.
  */
 int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
@@ -136,10 +138,12 @@ int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h);
  *   IPK_INTER_V:               int8 [B][T][d_model]
  *   IPK_INTER_P:               int8 [2T-1][d_model]
  *   IPK_INTER_CTX:             int8 [B][T][d_model] (attention output before W_out)
- * Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`, bytes too small, null),
- * IPK_ERR_HIP.
+ *   IPK_INTER_XLN:             int8 [B][T][d_model] (LayerNorm output; only after
+ *                              ipk_mhsa_residual_run)
+ * Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`, bytes too small, null,
+ * IPK_INTER_XLN when the last run was not ipk_mhsa_residual_run), IPK_ERR_HIP.
  */
-enum { IPK_INTER_Q = 0, IPK_INTER_K = 1, IPK_INTER_V = 2, IPK_INTER_P = 3, IPK_INTER_CTX = 4 };
+enum { IPK_INTER_Q = 0, IPK_INTER_K = 1, IPK_INTER_V = 2, IPK_INTER_P = 3, IPK_INTER_CTX = 4, IPK_INTER_XLN = 5 };
 int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
 
 /*
@@ -155,6 +159,71 @@ int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst,
  */
 enum { IPK_NUM_STAGES = 3 };
 int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
+
+/*
+ * Position projection kept on the handle (Sec. 3.1: q_P depends only on the
+ * sinusoidal table and W_pos, so the paper computes it offline).
+ * Projects `pos_table` (DEVICE int8 [2 T_table - 1][d_model], row r = relative
+ * position T_table-1-r, 16-byte aligned) once, on `stream`, and keeps the result.
+ * Later runs (ipk_relpos_attn_run, ipk_mhsa_residual_run) that pass pos_table = NULL
+ * use it for any T <= T_table: the table of a shorter T is rows T_table - T ..
+ * T_table + T - 2 of the longer one (each row is a function of its relative position
+ * only), so the result is byte for byte that of passing the T-row table.  A run that
+ * passes a table still projects it and leaves the kept one unchanged.  Calling this
+ * again replaces the kept projection (stream-ordered with the runs on `stream`).
+ * The first call allocates device memory for max_T (synchronously).
+ * Errors: IPK_ERR_INVALID_ARG (null handle or table, misaligned table, T_table
+ * outside [1, max_T]); IPK_ERR_OUT_OF_MEMORY; IPK_ERR_HIP.
+ * A later run with pos_table = NULL and no kept projection, or T > T_table, fails
+ * with IPK_ERR_INVALID_ARG.
+ */
+int ipk_relpos_attn_cache_positions(ipk_relpos_attn_t* h, const int8_t* pos_table, int32_t T_table, void* stream);
+
+/*
+ * The MHSA module of the Conformer block (Eq. 2) on integer grids:
+ *   x  = LN(z1)                     integer LayerNorm (I-BERT, Sec. 3.1) into the block's input grid
+ *   y  = the block above on x
+ *   z2 = clamp8(RS(m_z z1 + m_y y, 1, shift_r))   residual add, both terms moved to z2's grid
+ * LayerNorm of a row z of d_model int8 values:
+ *   mu    = floor((2 sum_k z_k + d) / (2 d))           (mean, ties up)
+ *   sigma = max(1, floor(sqrt(sum_k (z_k - mu)^2)))    (integer square root)
+ *   F     = floor(2^31 / sigma)
+ *   u_k   = floor((z_k - mu) F / 2)                    (~ 2^30 (z_k - mu) / sigma)
+ *   x_k   = clamp8(floor((u_k ln_mult[k] + ln_bias[k] + 2^(ln_shift-1)) / 2^ln_shift))
+ * where ln_mult and ln_bias fold LayerNorm's gamma, beta and the move to the block's
+ * input grid into one fixed-point step per channel.
+ * Ranges: |ln_mult[k]| < 2^24, |ln_bias[k]| < 2^56, 1 <= ln_shift <= 62;
+ * 0 <= m_z, m_y < 2^23; 1 <= shift_r <= 40.
+ */
+typedef struct ipk_mhsa_residual_desc {
+  const int32_t* ln_mult; /* HOST int32 [d_model] */
+  const int64_t* ln_bias; /* HOST int64 [d_model] */
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
+} ipk_mhsa_residual_desc;
+
+/*
+ * Attaches (or replaces) the LayerNorm and residual constants of `r` on the handle;
+ * the first call allocates the LayerNorm output workspace for (max_batch, max_T).
+ * Synchronizes its own copies; the caller may free `r`'s arrays when it returns.
+ * Errors: IPK_ERR_INVALID_ARG (null handle/desc/array, a value outside its range);
+ * IPK_ERR_OUT_OF_MEMORY; IPK_ERR_HIP.
+ */
+int ipk_mhsa_residual_set(ipk_relpos_attn_t* h, const ipk_mhsa_residual_desc* r);
+
+/*
+ * Runs the MHSA module on `stream`: z2 = z1 + MHSA(LN(z1)) as defined above.
+ * z1 DEVICE int8 [B][T][d_model], z2 DEVICE int8 [B][T][d_model], both 16-byte
+ * aligned; z2 may be z1 itself (in place) but may not overlap it otherwise.
+ * pos_table, lengths, B, T, stream: as for ipk_relpos_attn_run (pos_table may be
+ * NULL after ipk_relpos_attn_cache_positions).  Rows t >= L_b of z2 hold the
+ * residual of z1 alone (the block's output there is zero).
+ * Errors: as ipk_relpos_attn_run, and IPK_ERR_INVALID_ARG when no constants were set.
+ * If stage events are pending (ipk_relpos_attn_record_stages), events[0] is stamped
+ * when the LayerNorm kernel starts.
+ */
+int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* pos_table, const int32_t* lengths,
+                          int32_t B, int32_t T, int8_t* z2, void* stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* ipk_status_string(int status);

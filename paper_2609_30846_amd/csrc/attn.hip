@@ -710,7 +710,7 @@ __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
   int8_t v;
   if (a.which == 3) {
     v = a.src[(size_t)h * a.p_rows * a.DK + frag_index(a.p_base + (int)m, kk, a.DK)];
-  } else if (a.which == 4) {
+  } else if (a.which >= 4) {  // the context or the LayerNorm output, [B][T][d]
     v = a.src[idx];
   } else {
     const long b = m / a.T, t = m % a.T;
@@ -871,7 +871,7 @@ hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars&
   a.T_al = rs.T_al;
   a.H = rs.H;
   a.d = rs.d;
-  a.p_rows = p_rows(rs.T_al);
+  a.p_rows = rs.p_rows;
   a.p_base = rs.p_base;
   a.mc24 = sc.fs_mc24;
   a.mp24 = sc.fs_mp24;
@@ -892,7 +892,7 @@ hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars&
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st) {
   GatherArgs a{};
-  a.src = which == 0 ? ws.q : which == 1 ? ws.k : which == 2 ? ws.vt : which == 3 ? ws.p : ws.ctx;
+  a.src = which == 0 ? ws.q : which == 1 ? ws.k : which == 2 ? ws.vt : which == 3 ? ws.p : which == 4 ? ws.ctx : ws.xln;
   a.dst = dst;
   a.which = which;
   a.B = rs.B;
@@ -901,7 +901,7 @@ hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, i
   a.H = rs.H;
   a.DK = rs.DK;
   a.d = rs.d;
-  a.p_rows = p_rows(rs.T_al);
+  a.p_rows = rs.p_rows;
   a.p_base = rs.p_base;
   const long rows = which == 3 ? (long)(2 * rs.T - 1) : (long)rs.B * rs.T;
   const long total = rows * rs.d;

@@ -67,6 +67,10 @@ struct GemmArgs {
   int8_t *q, *k, *vt, *p, *y;
   int T_al, H, dk_shift, d, p_rows, p_base;  // d_k = 2^dk_shift
   int32_t* vsum;  // sums of V over each 64-key chunk, produced by the epilogue
+  // residual add of the MHSA module (row-major outputs only): y := clamp8(RS(m_z z1 +
+  // m_y y, 1, shift_r)) with z1 laid out as y
+  const int8_t* z1;
+  int m_z, m_y, shift_r;
 };
 
 constexpr int BK = 128;  // bytes of K per step
@@ -113,11 +117,31 @@ __device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16],
                  (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
 }
 
+// The residual add of Eq. 2 on 16 int8 pairs: clamp8(floor((m_z z + m_y y + 2^(n-1)) / 2^n)).
+// m_z z + m_y y is exact in int32 (multipliers below 2^23, |z|, |y| <= 128); the
+// rounding term and the shift (n <= 40) need 64 bits.
+__device__ __forceinline__ v4i residual16(const v4i& y, const v4i& z, int m_z, int m_y, int shift) {
+  const long long half = 1ll << (shift - 1);
+  v4i r;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t o = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int yb = (y[w] << (24 - 8 * b)) >> 24, zb = (z[w] << (24 - 8 * b)) >> 24;
+      const long long q = ((long long)(m_z * zb + m_y * yb) + half) >> shift;
+      o |= ((uint32_t)(int)min(max(q, -127ll), 127ll) & 0xFFu) << (8 * b);
+    }
+    r[w] = (int)o;
+  }
+  return r;
+}
+
 // WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  The weights
 // come pre-packed in MFMA fragment order (wfrag_index): each wave streams its own
 // fragments from memory straight into registers, one K step ahead, and only the token
-// tile goes through LDS.
-template <int TN, int TM, int NWAVE, int WN>
+// tile goes through LDS.  RESID: row-major outputs with the residual add fused.
+template <int TN, int TM, int NWAVE, int WN, bool RESID>
 __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 64 * NWAVE;
   constexpr int WM = NWAVE / WN;            // waves along M
@@ -305,6 +329,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
     const int nb = n0 + nl;
     if (nb >= N) continue;
     int8_t* dst;
+    const int8_t* zsrc = nullptr;  // residual input, laid out as dst (row-major mode)
     int kk = 0;  // channel of the sub-tile's first row inside its head
     int hd = 0;  // its head
     if (mode == OUT_QKV) {
@@ -319,6 +344,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       kk = nb & DKm;
     } else {
       dst = args.y + (size_t)ub * rows * N + nb;
+      zsrc = args.z1 + (size_t)ub * rows * N + nb;
     }
     // the scales of this sub-tile's channels, the same for all its token columns
     double sc[16];
@@ -360,13 +386,17 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       requant16(acc[i][j], sc, D);
       const auto x02 = __builtin_amdgcn_permlane32_swap(D[0], D[2], false, false);
       const auto x13 = __builtin_amdgcn_permlane32_swap(D[1], D[3], false, false);
-      const v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
+      v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
 
       // V^T: 16 consecutive tokens of one channel, stored up to T_al (zeros past the
       // utterance: the operand rows there read as zeros); otherwise 16 consecutive
       // channels of one token
       const uint32_t joff = vwave ? ((uint32_t)(j >> 1) << (dks + 6)) + (uint32_t)(j & 1) * 512u : (uint32_t)j * jstep;
-      if (tl + j * 32 < tmax) *(v4i*)(dst + (off0 + joff)) = out;
+      if (tl + j * 32 < tmax) {
+        if (RESID)
+          out = residual16(out, *(const v4i*)(zsrc + (off0 + joff)), args.m_z, args.m_y, args.shift_r);
+        *(v4i*)(dst + (off0 + joff)) = out;
+      }
       if (vwave) {
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) vpart[j / 2] = __builtin_amdgcn_sdot4(out[wd], 0x01010101, vpart[j / 2], false);
@@ -416,21 +446,23 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.k = ws.k;
   a.vt = ws.vt;
   a.p = ws.p;
+  a.z1 = nullptr;
   a.y = y;
   a.T_al = rs.T_al;
   a.H = rs.H;
   a.dk_shift = rs.DK == 128 ? 7 : 6;  // d_k is 64 or 128
   a.d = rs.d;
-  a.p_rows = p_rows(rs.T_al);
+  a.p_rows = rs.p_rows;
   a.p_base = rs.p_base;
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWAVE, int WN>
+template <int TN, int TM, int NWAVE, int WN, bool RESID = false>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev, a);
+  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, RESID>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
+                       a);
 }
 
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
@@ -444,20 +476,42 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
   // the epilogue's V sums: a wave's tokens are whole 64-key chunks
   static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
   int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
-  tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
-  a.nprob = 2;
+  a.nprob = 1;
+  if (pos_table) {
+    tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
+    a.nprob = 2;
+  }
   return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
 }
 
+hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p, const int8_t* pos_table,
+                                 hipStream_t st) {
+  GemmArgs a{};
+  Workspace ws{};
+  ws.p = p;
+  fill_dest(a, rs, ws, nullptr);
+  constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
+  const int tiles = add_problem(a, 0, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, 0, TN, TM);
+  a.nprob = 1;
+  return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, LaunchEv{});
+}
+
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
-                                 hipStream_t st, const LaunchEv& ev) {
+                                 hipStream_t st, const LaunchEv& ev, const Residual* res, const int8_t* z1) {
   GemmArgs a{};
   fill_dest(a, rs, ws, y);
+  if (res) {
+    a.z1 = z1;
+    a.m_z = res->m_z;
+    a.m_y = res->m_y;
+    a.shift_r = res->shift_r;
+  }
   // small tiles (640 at T = 2500): with K = d_model and few 64-token blocks the launch
   // is bound by load latency, and larger tiles measured no faster
   constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
+  if (res) return launch_gemm<TN, TM, NWAVE, WN, true>(a, tiles, st, ev);
   return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
 }
 

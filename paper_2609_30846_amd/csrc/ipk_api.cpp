@@ -1,7 +1,8 @@
 // C-ABI entry points of the ipk library: descriptor validation, the handle and its
 // workspace, and the per-run launch sequence
 //   projections (Q|K|V and the position table) -> rank-1 bias terms and V prefix
-//   sums -> attention core -> output projection.
+//   sums -> attention core -> output projection; for the MHSA module of Eq. 2 an
+//   integer LayerNorm first and the residual add in the output projection's epilogue.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdarg.h>
@@ -28,8 +29,17 @@ struct ipk_relpos_attn {
   std::vector<void*> allocs;
   RunShape last;
   bool has_run;
+  bool last_was_residual;
+  int8_t* last_p;  // buffer of the last run's projected table (ws.p or pcache)
   hipEvent_t stage_ev[IPK_NUM_STAGES + 1];
   bool stages_pending;
+  // projected position table kept by ipk_relpos_attn_cache_positions
+  int8_t* pcache;
+  int pcache_T;     // table length T_table, 0 when nothing is kept
+  int pcache_rows;  // rows per head of pcache
+  // LayerNorm and residual constants of the MHSA module
+  Residual res;
+  bool has_res;
 };
 
 static thread_local char g_last_error[512];
@@ -159,7 +169,14 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   h->sc.q_c = desc->q_c;
   plan_fused_score(&h->sc, desc->d_k);
   h->has_run = false;
+  h->last_was_residual = false;
+  h->last_p = nullptr;
   h->stages_pending = false;
+  h->pcache = nullptr;
+  h->pcache_T = 0;
+  h->pcache_rows = 0;
+  h->res = Residual{};
+  h->has_res = false;
 
   const size_t d = h->d, H = h->H, DK = h->DK, Bm = h->max_B;
   const size_t T_al = t_aligned(h->max_T), PR = p_rows((int)T_al);
@@ -233,14 +250,20 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   return IPK_OK;
 }
 
-extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
-                                   const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream) {
-  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
-  if (!x || !pos_table || !y) return fail(IPK_ERR_INVALID_ARG, "x, pos_table and y must be non-NULL");
+// Validates a run's arguments and enqueues it: LayerNorm (z1 != NULL, the MHSA
+// module), projections, attention core, output projection (with the residual add
+// when z1 != NULL).
+static int enqueue_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths, int32_t B,
+                       int32_t T, int8_t* y, void* stream, const int8_t* z1) {
   if (((uintptr_t)x | (uintptr_t)pos_table | (uintptr_t)y) & 15)
-    return fail(IPK_ERR_INVALID_ARG, "x, pos_table and y must be 16-byte aligned");
+    return fail(IPK_ERR_INVALID_ARG, "the input, pos_table and output must be 16-byte aligned");
   if (B < 1 || B > h->max_B) return fail(IPK_ERR_INVALID_ARG, "B=%d outside [1, max_batch=%d]", B, h->max_B);
   if (T < 1 || T > h->max_T) return fail(IPK_ERR_INVALID_ARG, "T=%d outside [1, max_T=%d]", T, h->max_T);
+  if (!pos_table && T > h->pcache_T)
+    return fail(IPK_ERR_INVALID_ARG,
+                h->pcache_T ? "pos_table is NULL and the kept projection covers T <= %d only" :
+                              "pos_table is NULL and no position projection is kept (T_table %d)",
+                h->pcache_T);
   Lengths lens;
   for (int b = 0; b < B; ++b) {
     const int L = lengths ? lengths[b] : T;
@@ -251,24 +274,147 @@ extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const 
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
     return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
-  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d, p_base_row(T)};
+  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d, p_base_row(T), p_rows(t_aligned(T))};
+  Workspace ws = h->ws;
+  if (!pos_table) {
+    // table row r of this T is row r + T_table - T of the kept one, whose relative
+    // position 0 sits at a 16-row boundary for every T
+    ws.p = h->pcache;
+    rs.p_rows = h->pcache_rows;
+    rs.p_base = p_base_row(h->pcache_T) + h->pcache_T - T;
+  }
   hipStream_t st = (hipStream_t)stream;
   const bool rec = h->stages_pending;
   h->stages_pending = false;
-  // stage events ride on the kernel dispatches: event i is stamped when kernel i
+  // stage events ride on the kernel dispatches: event i is stamped when stage i
   // starts, event 3 when the last kernel ends (no separate event packets)
   LaunchEv ev[3];
   if (rec) {
     for (int i = 0; i < 3; ++i) ev[i].start = h->stage_ev[i];
     ev[2].stop = h->stage_ev[3];
   }
+  hipError_t e = hipSuccess;
+  if (z1) {
+    e = launch_layernorm(rs, h->res, z1, ws.xln, st, ev[0]);
+    x = ws.xln;
+    ev[0] = LaunchEv{};
+  }
   // the projections also produce the V sums the core reads
-  hipError_t e = launch_projections(rs, h->w, h->ws, x, pos_table, st, ev[0]);
-  if (e == hipSuccess) e = launch_attention(rs, h->w, h->sc, h->ws, lens, st, ev[1]);
-  if (e == hipSuccess) e = launch_out_projection(rs, h->w, h->ws, y, st, ev[2]);
+  if (e == hipSuccess) e = launch_projections(rs, h->w, ws, x, pos_table, st, ev[0]);
+  if (e == hipSuccess) e = launch_attention(rs, h->w, h->sc, ws, lens, st, ev[1]);
+  if (e == hipSuccess) e = launch_out_projection(rs, h->w, ws, y, st, ev[2], z1 ? &h->res : nullptr, z1);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;
+  h->last_p = ws.p;
   h->has_run = true;
+  h->last_was_residual = z1 != nullptr;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
+                                   const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!x || !y) return fail(IPK_ERR_INVALID_ARG, "x and y must be non-NULL");
+  return enqueue_run(h, x, pos_table, lengths, B, T, y, stream, nullptr);
+}
+
+extern "C" int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* pos_table,
+                                     const int32_t* lengths, int32_t B, int32_t T, int8_t* z2, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!z1 || !z2) return fail(IPK_ERR_INVALID_ARG, "z1 and z2 must be non-NULL");
+  if (!h->has_res) return fail(IPK_ERR_INVALID_ARG, "no LayerNorm / residual constants set (ipk_mhsa_residual_set)");
+  if (B >= 1 && T >= 1 && z1 != z2) {
+    const size_t n = (size_t)B * T * h->d;
+    const uintptr_t a = (uintptr_t)z1, b = (uintptr_t)z2;
+    if (a < b + n && b < a + n) return fail(IPK_ERR_INVALID_ARG, "z1 and z2 overlap without being equal");
+  }
+  return enqueue_run(h, z1, pos_table, lengths, B, T, z2, stream, z1);
+}
+
+extern "C" int ipk_mhsa_residual_set(ipk_relpos_attn_t* h, const ipk_mhsa_residual_desc* r) {
+  if (!h || !r) return fail(IPK_ERR_INVALID_ARG, "handle and desc must be non-NULL");
+  if (!r->ln_mult || !r->ln_bias) return fail(IPK_ERR_INVALID_ARG, "ln_mult and ln_bias must be non-NULL");
+  if (r->ln_shift < 1 || r->ln_shift > 62) return fail(IPK_ERR_INVALID_ARG, "ln_shift=%d outside [1, 62]", r->ln_shift);
+  if (!mult_ok(r->m_z) || !mult_ok(r->m_y))
+    return fail(IPK_ERR_INVALID_ARG, "m_z=%d, m_y=%d must be in [0, 2^23)", r->m_z, r->m_y);
+  if (!shift_ok(r->shift_r)) return fail(IPK_ERR_INVALID_ARG, "shift_r=%d outside [1, 40]", r->shift_r);
+  const int d = h->d;
+  std::vector<int64_t> cb(d);
+  for (int k = 0; k < d; ++k) {
+    if (r->ln_mult[k] <= -(1 << 24) || r->ln_mult[k] >= (1 << 24))
+      return fail(IPK_ERR_INVALID_ARG, "ln_mult[%d]=%d outside (-2^24, 2^24)", k, r->ln_mult[k]);
+    if (r->ln_bias[k] <= -((int64_t)1 << 56) || r->ln_bias[k] >= ((int64_t)1 << 56))
+      return fail(IPK_ERR_INVALID_ARG, "ln_bias[%d] outside (-2^56, 2^56)", k);
+    cb[k] = r->ln_bias[k] + ((int64_t)1 << (r->ln_shift - 1));
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t x) {
+    if (e == hipSuccess) e = x;
+  };
+  if (!h->ws.xln) {
+    int32_t* g = nullptr;
+    int64_t* c = nullptr;
+    int8_t* xln = nullptr;
+    chk(dev_alloc(h, &g, d));
+    chk(dev_alloc(h, &c, d));
+    chk(dev_alloc(h, &xln, (size_t)h->max_B * h->max_T * d));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
+                  hipGetErrorString(e));
+    }
+    h->res.ln_mult = g;
+    h->res.ln_bias = c;
+    h->ws.xln = xln;
+  }
+  // stream-ordered after every run already enqueued on the handle's device
+  chk(hipDeviceSynchronize());
+  chk(hipMemcpy((void*)h->res.ln_mult, r->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
+  chk(hipMemcpy((void*)h->res.ln_bias, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice));
+  chk(hipDeviceSynchronize());
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(IPK_ERR_HIP, "copying the LayerNorm constants failed: %s", hipGetErrorString(e));
+  }
+  h->res.ln_shift = r->ln_shift;
+  h->res.m_z = r->m_z;
+  h->res.m_y = r->m_y;
+  h->res.shift_r = r->shift_r;
+  h->has_res = true;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_cache_positions(ipk_relpos_attn_t* h, const int8_t* pos_table, int32_t T_table,
+                                               void* stream) {
+  if (!h || !pos_table) return fail(IPK_ERR_INVALID_ARG, "handle and pos_table must be non-NULL");
+  if ((uintptr_t)pos_table & 15) return fail(IPK_ERR_INVALID_ARG, "pos_table must be 16-byte aligned");
+  if (T_table < 1 || T_table > h->max_T)
+    return fail(IPK_ERR_INVALID_ARG, "T_table=%d outside [1, max_T=%d]", T_table, h->max_T);
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  // rows per head: the table at its 16-aligned base (at most P_PADLO + 15) plus the
+  // padding the attention core's windows reach past either end, sized for max_T
+  const int rows = P_PADLO + 16 + 2 * t_aligned(h->max_T) + P_PADHI;
+  if (!h->pcache) {
+    int8_t* p = nullptr;
+    hipError_t e = dev_alloc(h, &p, (size_t)h->H * rows * h->DK);
+    if (e == hipSuccess) e = hipMemset(p, 0, (size_t)h->H * rows * h->DK);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
+                  hipGetErrorString(e));
+    }
+    h->pcache = p;
+    h->pcache_rows = rows;
+  }
+  RunShape rs{1, T_table, t_aligned(T_table), h->H, h->DK, h->d, p_base_row(T_table), rows};
+  hipError_t e = launch_pos_projection(rs, h->w, h->pcache, pos_table, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  h->pcache_T = T_table;
   return IPK_OK;
 }
 
@@ -276,11 +422,15 @@ extern "C" int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which,
                                             void* stream) {
   if (!h || !dst) return fail(IPK_ERR_INVALID_ARG, "handle and dst must be non-NULL");
   if (!h->has_run) return fail(IPK_ERR_INVALID_ARG, "no run yet");
-  if (which < IPK_INTER_Q || which > IPK_INTER_CTX) return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
+  if (which < IPK_INTER_Q || which > IPK_INTER_XLN) return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
+  if (which == IPK_INTER_XLN && !h->last_was_residual)
+    return fail(IPK_ERR_INVALID_ARG, "the last run was not an MHSA module run: no LayerNorm output");
   const RunShape& rs = h->last;
   const int64_t need = (which == IPK_INTER_P ? (int64_t)(2 * rs.T - 1) : (int64_t)rs.B * rs.T) * rs.d;
   if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
-  hipError_t e = launch_gather_intermediate(rs, h->ws, which, (int8_t*)dst, (hipStream_t)stream);
+  Workspace ws = h->ws;
+  ws.p = h->last_p;
+  hipError_t e = launch_gather_intermediate(rs, ws, which, (int8_t*)dst, (hipStream_t)stream);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "gather failed: %s", hipGetErrorString(e));
   return IPK_OK;
 }

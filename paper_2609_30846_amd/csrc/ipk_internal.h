@@ -55,6 +55,15 @@ __host__ __device__ inline size_t vt_index(int t, int kk, int DK) {
 struct Workspace {
   int8_t *q, *k, *vt, *p, *ctx;
   int32_t* vsum;
+  int8_t* xln;  // LayerNorm output [B][T][d] of the MHSA module's runs
+};
+
+// LayerNorm and residual constants of the MHSA module (Eq. 2) on the device.
+struct Residual {
+  const int32_t* ln_mult;  // [d]
+  const int64_t* ln_bias;  // [d]: ln_bias + 2^(ln_shift - 1), the rounding term folded in
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
 };
 
 // Fragment order of a weight matrix W [N][K] (N, K multiples of 32) for the A operand of
@@ -98,6 +107,7 @@ struct Lengths {
 struct RunShape {
   int B, T, T_al, H, DK, d;
   int p_base;  // workspace row of relative-position table row 0
+  int p_rows;  // rows per head of the projected table's buffer
 };
 
 // Optional timing events of one kernel launch, carried by the dispatch itself
@@ -117,12 +127,21 @@ inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem,
 }
 
 // Enqueue the kernels of one run; return the first HIP error.
+// pos_table == nullptr: Q|K|V only (the projected table is already in ws.p)
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev = {});
 hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars& sc, const Workspace& ws,
                             const Lengths& lens, hipStream_t st, const LaunchEv& ev = {});
+// res != nullptr: the epilogue adds the residual, y := clamp8(RS(m_z z1 + m_y y, 1, shift_r))
 hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Workspace& ws, int8_t* y,
-                                 hipStream_t st, const LaunchEv& ev = {});
+                                 hipStream_t st, const LaunchEv& ev = {}, const Residual* res = nullptr,
+                                 const int8_t* z1 = nullptr);
+// The position projection alone, of a table of T_table rows, into `p` (rs.p_base, rs.p_rows).
+hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p, const int8_t* pos_table,
+                                 hipStream_t st);
+// Integer LayerNorm of rows [B][T][d] of z into ws.xln.
+hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st,
+                            const LaunchEv& ev = {});
 // Workgroup shapes of the attention core for a run: the first shape's nqb1 query
 // blocks per (utterance, head), then (c2.ksplit != 0) the second shape's nqb2 blocks
 // for the remaining queries.  c1.ksplit == 0 when T_al does not fit LDS.

@@ -25,7 +25,7 @@ IPK_ERR_OUT_OF_MEMORY = -3
 IPK_ERR_HIP = -4
 IPK_MAX_BATCH = 256
 IPK_MAX_T = 8192
-IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX = range(5)
+IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN = range(6)
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p
@@ -35,6 +35,9 @@ SIGNATURES = [
     ("ipk_relpos_attn_destroy", C.c_int, [_vp]),
     ("ipk_relpos_attn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_relpos_attn_record_stages", C.c_int, [_vp, _vp]),
+    ("ipk_relpos_attn_cache_positions", C.c_int, [_vp, _vp, C.c_int32, _vp]),
+    ("ipk_mhsa_residual_set", C.c_int, [_vp, _vp]),
+    ("ipk_mhsa_residual_run", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
     ("ipk_status_string", C.c_char_p, [C.c_int]),
     ("ipk_last_error", C.c_char_p, []),
     ("ipk_abi_version", C.c_int, []),
@@ -62,6 +65,15 @@ class Desc(C.Structure):
         ("m_o", C.c_int32), ("shift_o", C.c_int32),
         ("q_ln2", C.c_int32), ("q_b", C.c_int32), ("q_c", C.c_int32),
         ("zp_x", C.c_int32), ("zp_y", C.c_int32),
+    ]
+
+
+class ResidualDesc(C.Structure):
+    """Mirror of ipk_mhsa_residual_desc."""
+
+    _fields_ = [
+        ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
+        ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
     ]
 
 
@@ -132,6 +144,24 @@ def ipk_relpos_attn_run(h: int, x, pos_table, lengths: Optional[Sequence[int]], 
     lp = lens.ctypes.data if lens is not None else None
     _check(load().ipk_relpos_attn_run(h, _ptr(x), _ptr(pos_table), lp, int(B), int(T), _ptr(y),
                                       _stream_ptr(stream)))
+
+
+def ipk_relpos_attn_cache_positions(h: int, pos_table, T_table: int, stream=None) -> None:
+    _check(load().ipk_relpos_attn_cache_positions(h, _ptr(pos_table), int(T_table), _stream_ptr(stream)))
+
+
+def ipk_mhsa_residual_set(h: int, desc: ResidualDesc) -> None:
+    _check(load().ipk_mhsa_residual_set(h, C.byref(desc)))
+
+
+def ipk_mhsa_residual_run(h: int, z1, pos_table, lengths: Optional[Sequence[int]], B: int, T: int, z2,
+                          stream=None) -> None:
+    lens = None
+    if lengths is not None:
+        lens = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    lp = lens.ctypes.data if lens is not None else None
+    _check(load().ipk_mhsa_residual_run(h, _ptr(z1), _ptr(pos_table), lp, int(B), int(T), _ptr(z2),
+                                        _stream_ptr(stream)))
 
 
 def ipk_relpos_attn_destroy(h: Optional[int]) -> None:
@@ -208,6 +238,33 @@ class RelPosAttn:
             y = torch.empty_like(x)
         ipk_relpos_attn_run(self.handle, x, pos_table, lengths, B, T, y, stream)
         return y
+
+    def cache_positions(self, pos_table, stream=None):
+        """Projects ``pos_table`` ([2 T_table - 1][d] int8 on the device) once; later
+        calls with ``pos_table=None`` use it for any T <= T_table."""
+        T_table = (pos_table.shape[0] + 1) // 2
+        ipk_relpos_attn_cache_positions(self.handle, pos_table, T_table, stream)
+
+    def set_residual(self, ln_mult, ln_bias, ln_shift: int, m_z: int, m_y: int, shift_r: int):
+        """LayerNorm and residual constants of the MHSA module (host arrays)."""
+        g = np.ascontiguousarray(ln_mult, dtype=np.int32)
+        c = np.ascontiguousarray(ln_bias, dtype=np.int64)
+        desc = ResidualDesc(g.ctypes.data, c.ctypes.data, int(ln_shift), int(m_z), int(m_y), int(shift_r))
+        ipk_mhsa_residual_set(self.handle, desc)
+
+    def set_residual_from(self, res):
+        """``res``: a workloads Residual (ln_mult, ln_bias, ln_shift, m_z, m_y, shift_r)."""
+        self.set_residual(res.ln_mult, res.ln_bias, res.ln_shift, res.m_z, res.m_y, res.shift_r)
+
+    def residual(self, z1, pos_table, lengths=None, z2=None, stream=None):
+        """z2 = z1 + MHSA(LN(z1)); ``z2`` may be ``z1`` (in place)."""
+        import torch
+
+        B, T, d = z1.shape
+        if z2 is None:
+            z2 = torch.empty_like(z1)
+        ipk_mhsa_residual_run(self.handle, z1, pos_table, lengths, B, T, z2, stream)
+        return z2
 
     def intermediate(self, which: int, shape, stream=None):
         import torch

@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert ipk.abi_version() == 1
+    assert ipk.abi_version() == 2
     assert ipk.status_name(0) == "IPK_OK"
     assert ipk.status_name(-1) == "IPK_ERR_INVALID_ARG"
     assert ipk.status_name(-2) == "IPK_ERR_UNSUPPORTED"
@@ -50,6 +50,13 @@ def test_descriptor_struct_matches_header_field_order():
     body = re.search(r"typedef struct ipk_relpos_attn_desc \{(.*?)\}", text, flags=re.S).group(1)
     names = re.findall(r"\*?(\w+)\s*[,;]", body)
     assert names == [f[0] for f in ipk.Desc._fields_]
+
+
+def test_residual_descriptor_struct_matches_header_field_order():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct ipk_mhsa_residual_desc \{(.*?)\}", text, flags=re.S).group(1)
+    names = re.findall(r"\*?(\w+)\s*[,;]", body)
+    assert names == [f[0] for f in ipk.ResidualDesc._fields_]
 
 
 def _valid_desc():
