@@ -43,6 +43,18 @@ class OracleTrace(C.Structure):
     _fields_ = [("q", i8p), ("k", i8p), ("v", i8p), ("p", i8p), ("s", i8p), ("a", u8p), ("ctx", i8p)]
 
 
+class OracleFfnDesc(C.Structure):
+    _fields_ = [
+        ("d_model", C.c_int32), ("d_ff", C.c_int32),
+        ("w1", i8p), ("w2", i8p), ("mult1", i32p), ("mult2", i32p),
+        ("shift1", C.c_int32), ("shift2", C.c_int32),
+        ("sw_qc", C.c_int64), ("sw_q1", C.c_int64),
+        ("m_sw", C.c_int32), ("shift_sw", C.c_int32),
+        ("ln_mult", i32p), ("ln_bias", i64p), ("ln_shift", C.c_int32),
+        ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
+    ]
+
+
 def lib():
     global _lib
     with _lock:
@@ -74,6 +86,10 @@ def lib():
             L.ipk_oracle_mhsa_residual.restype = C.c_int
             L.ipk_oracle_mhsa_residual.argtypes = [C.POINTER(OracleDesc), i32p, i64p, C.c_int32, C.c_int32, C.c_int32,
                                                    C.c_int32, i8p, i8p, i32p, C.c_int32, C.c_int32, i8p, i8p, i8p]
+            L.ipk_oracle_int_swish.restype = C.c_int64
+            L.ipk_oracle_int_swish.argtypes = [C.c_int64, C.c_int64, C.c_int64]
+            L.ipk_oracle_ffn_module.restype = C.c_int
+            L.ipk_oracle_ffn_module.argtypes = [C.POINTER(OracleFfnDesc), i8p, C.c_int64, i8p, i8p, i8p, i8p, i8p]
             L.ipk_oracle_relpos_attn.restype = C.c_int
             L.ipk_oracle_relpos_attn.argtypes = [C.POINTER(OracleDesc), i8p, i8p, i32p, C.c_int32, C.c_int32,
                                                  i8p, C.POINTER(OracleTrace)]
@@ -253,3 +269,46 @@ def mhsa_residual(blk, res, z1: Optional[np.ndarray] = None, lengths: Optional[n
     if rc != 0:
         raise ValueError(f"oracle rejected its arguments (status {rc})")
     return (z2, {"x": x, "y": y}) if trace else z2
+
+
+# ---- the feed-forward module of Eq. 1 (LayerNorm, W1, integer Swish, W2, residual)
+
+
+def int_swish(q: int, q_c: int, q_1: int) -> int:
+    """The integer Swish of Eq. 12 on one value (the C oracle's routine)."""
+    return int(lib().ipk_oracle_int_swish(int(q), int(q_c), int(q_1)))
+
+
+def ffn_module(ffn, z: np.ndarray, trace: bool = False):
+    """z_out = z + 0.5 FFN(LN(z)) on host memory (rows of d_model int8 values); with
+    trace, also returns the LayerNorm output x, h = W1 x, the Swish output o and
+    y = W2 o."""
+    z = np.ascontiguousarray(z, dtype=np.int8)
+    d, f = ffn.d_model, ffn.d_ff
+    flat = z.reshape(-1, d)
+    rows = flat.shape[0]
+    keep = []
+
+    def arr(a, dt, t):
+        a = np.ascontiguousarray(a, dtype=dt)
+        keep.append(a)
+        return _p(a, t)
+
+    D = OracleFfnDesc()
+    D.d_model, D.d_ff = d, f
+    D.w1, D.w2 = arr(ffn.w1, np.int8, i8p), arr(ffn.w2, np.int8, i8p)
+    D.mult1, D.mult2 = arr(ffn.mult1, np.int32, i32p), arr(ffn.mult2, np.int32, i32p)
+    D.shift1, D.shift2 = int(ffn.shift1), int(ffn.shift2)
+    D.sw_qc, D.sw_q1 = int(ffn.sw_qc), int(ffn.sw_q1)
+    D.m_sw, D.shift_sw = int(ffn.m_sw), int(ffn.shift_sw)
+    D.ln_mult, D.ln_bias, D.ln_shift = arr(ffn.ln_mult, np.int32, i32p), arr(ffn.ln_bias, np.int64, i64p), int(ffn.ln_shift)
+    D.m_z, D.m_y, D.shift_r = int(ffn.m_z), int(ffn.m_y), int(ffn.shift_r)
+    out = np.empty_like(flat)
+    tr = {k: np.empty((rows, n), dtype=np.int8) for k, n in (("x", d), ("h", f), ("o", f), ("y", d))} if trace else {}
+    rc = lib().ipk_oracle_ffn_module(C.byref(D), _p(flat, i8p), rows, _p(out, i8p),
+                                     *[_p(tr[k], i8p) if trace else None for k in ("x", "h", "o", "y")])
+    del keep
+    if rc != 0:
+        raise ValueError(f"oracle rejected its arguments (status {rc})")
+    out = out.reshape(z.shape)
+    return (out, {k: v.reshape(z.shape[:-1] + (v.shape[-1],)) for k, v in tr.items()}) if trace else out

@@ -312,3 +312,73 @@ int ipk_oracle_mhsa_residual(const oracle_desc* D, const int32_t* ln_g, const in
   free(y);
   return rc;
 }
+
+/* ------------------------------------------------------------------------------
+ * The feed-forward module of Eq. 1, Z1 = X + 0.5 FFN(LN(X)) with FFN = W2 Swish(W1 .),
+ * on integer grids.  Steps (this oracle's reading, kept with the design notes):
+ *  - x = LN(z) as above;
+ *  - h = clamp8(RS(x W1^T, mult1[c], shift1))            (Eq. 7, per channel, int8);
+ *  - the Swish of Sec. 3.2 on h's grid S: with u = x/2 on S_u = S/2, Eq. 12 gives
+ *    |tanh^| on the grid a S_u^2 as L = (min(|h|, q_c) - q_c)^2 + q_1 with
+ *    q_c = floor(c / S_u) and q_1 = floor(1 / (a S_u^2)), and since
+ *    sw^(x) = x (1 + sgn(x) |tanh^|) / 2 = (x + |x| |tanh^|) / 2,
+ *    q_sw = -(|h| L + h q_1) on the grid -a S_u^2 S / 2 (positive: a < 0);
+ *  - o = clamp8(RS(q_sw, m_sw, shift_sw)), FFN2's int8 input grid;
+ *  - y = clamp8(RS(o W2^T, mult2[c], shift2))             (Eq. 7);
+ *  - z_out = clamp8(RS(m_z z + m_y y, 1, shift_r)), the 0.5 of Eq. 1 folded into m_y.
+ * ------------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t d_model, d_ff;
+  const int8_t *w1, *w2;         /* [d_ff][d_model], [d_model][d_ff] */
+  const int32_t *mult1, *mult2;  /* [d_ff], [d_model] */
+  int32_t shift1, shift2;
+  int64_t sw_qc, sw_q1;
+  int32_t m_sw, shift_sw;
+  const int32_t* ln_mult;
+  const int64_t* ln_bias;
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
+} oracle_ffn_desc;
+
+/* The integer Swish of one value q on its grid (Eq. 12 as described above). */
+int64_t ipk_oracle_int_swish(int64_t q, int64_t q_c, int64_t q_1) {
+  const int64_t aq = q < 0 ? -q : q;
+  const int64_t t = (aq < q_c ? aq : q_c) - q_c;
+  const int64_t L = t * t + q_1;
+  return -(aq * L + q * q_1);
+}
+
+/* The module on `rows` rows of d_model int8 values.  x_out [rows][d_model], h_out and
+ * o_out [rows][d_ff], y_out [rows][d_model] receive the intermediates (each may be
+ * NULL).  Returns 0, or -1 on an invalid argument. */
+int ipk_oracle_ffn_module(const oracle_ffn_desc* D, const int8_t* z, int64_t rows, int8_t* z_out, int8_t* x_out,
+                          int8_t* h_out, int8_t* o_out, int8_t* y_out) {
+  if (!D || !z || !z_out || rows < 1 || D->d_model < 1 || D->d_ff < 1 || D->ln_shift < 1 || D->ln_shift > 62 ||
+      D->shift1 < 1 || D->shift1 > 40 || D->shift2 < 1 || D->shift2 > 40 || D->shift_sw < 1 || D->shift_sw > 40 ||
+      D->shift_r < 1 || D->shift_r > 40 || D->sw_qc < 0)
+    return -1;
+  const int32_t d = D->d_model, f = D->d_ff;
+  int8_t* x = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* h = (int8_t*)malloc((size_t)(rows * f));
+  int8_t* o = (int8_t*)malloc((size_t)(rows * f));
+  int8_t* y = (int8_t*)malloc((size_t)(rows * d));
+  if (!x || !h || !o || !y) {
+    free(x); free(h); free(o); free(y);
+    return -1;
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) ipk_oracle_layernorm_row(z + r * d, d, D->ln_mult, D->ln_bias, D->ln_shift, x + r * d);
+  ipk_oracle_linear(x, rows, d, D->w1, f, D->mult1, D->shift1, h);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < rows * f; ++i)
+    o[i] = (int8_t)ipk_oracle_clamp8(ipk_oracle_rs(ipk_oracle_int_swish(h[i], D->sw_qc, D->sw_q1), D->m_sw, D->shift_sw));
+  ipk_oracle_linear(o, rows, f, D->w2, d, D->mult2, D->shift2, y);
+  for (int64_t i = 0; i < rows * d; ++i) z_out[i] = (int8_t)ipk_oracle_residual(z[i], y[i], D->m_z, D->m_y, D->shift_r);
+  if (x_out) memcpy(x_out, x, (size_t)(rows * d));
+  if (h_out) memcpy(h_out, h, (size_t)(rows * f));
+  if (o_out) memcpy(o_out, o, (size_t)(rows * f));
+  if (y_out) memcpy(y_out, y, (size_t)(rows * d));
+  free(x); free(h); free(o); free(y);
+  return 0;
+}

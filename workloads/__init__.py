@@ -10,10 +10,12 @@ score, softmax or requantization of data).
 from .generate import (  # noqa: F401
     CONFIGS,
     Block,
+    Ffn,
     Residual,
     Workload,
     config_by_name,
     make_block,
+    make_ffn,
     make_residual,
     make_workload,
     sinusoid_table,

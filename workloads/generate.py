@@ -351,3 +351,113 @@ def make_residual(blk: Block, regime: str, seed: int) -> Residual:
                     m_z=fixed_point(_dec(S_z1) / _dec(S_z2)), m_y=fixed_point(_dec(S_y) / _dec(S_z2)),
                     shift_r=SHIFT_N,
                     scales={"S_z1": S_z1, "S_z2": S_z2, "S_x": S_x, "S_y": S_y, "gamma": gamma, "beta": beta})
+
+
+# ---------------------------------------------------------------------------------
+# The feed-forward module of Eq. 1, Z1 = X + 0.5 FFN(LN(X)), FFN = W2 Swish(W1 .),
+# with d_ff = 4 d (Parakeet's Conformer blocks).  W1, W2 are int8 uniform in
+# [-127, 127] with per-channel scales; LayerNorm's gamma ~ U[0.5, 1.5] and
+# beta ~ U[-0.25, 0.25] per channel.  Literal regime: every grid (S_x of the
+# LayerNorm output, S_h of W1's output, S_o of the Swish output, S_y, S_z2) and every
+# per-channel weight scale ~ U[2^-8, 2^-4]; calibrated: the LayerNorm output has unit
+# variance, the weights Xavier scale, and each grid covers +-4 standard deviations of
+# its tensor, estimated from those distributions (no data pass).
+SWISH_A, SWISH_C = -0.1240, 2.4632  # Eq. 13's minimax (a*, c*)
+FFN_MULT = 4
+
+
+@dataclasses.dataclass
+class Ffn:
+    """Integer parameters of the feed-forward module and the real values they came from."""
+
+    d_model: int
+    d_ff: int
+    w1: np.ndarray  # int8 [d_ff][d_model]
+    w2: np.ndarray  # int8 [d_model][d_ff]
+    mult1: np.ndarray  # int32 [d_ff]
+    shift1: int
+    mult2: np.ndarray  # int32 [d_model]
+    shift2: int
+    sw_qc: int  # floor(c* / S_u), S_u = S_h / 2
+    sw_q1: int  # floor(1 / (a* S_u^2))
+    m_sw: int  # Swish output grid -a* S_u^2 S_h / 2 -> S_o
+    shift_sw: int
+    ln_mult: np.ndarray
+    ln_bias: np.ndarray
+    ln_shift: int
+    m_z: int  # round(2^n S_z / S_z2)
+    m_y: int  # round(2^n 0.5 S_y / S_z2)
+    shift_r: int
+    scales: Dict[str, object]
+
+
+def fixed_point_fine(ratio, n_max: int = 40):
+    """(m, n) with m = round(2^n ratio) < 2^23 for the largest n <= n_max: a multiplier
+    with as many significant bits as the range allows (for ratios far below 1)."""
+    r = _dec(ratio)
+    for n in range(n_max, 0, -1):
+        m = _round_dec((Decimal(2) ** n) * r)
+        if m < (1 << 23):
+            return m, n
+    raise ValueError(f"ratio {ratio} needs a multiplier of 2^23 or more even at n = 1")
+
+
+def _ln_consts(d: int, gamma, beta, S_x: float):
+    two_n = Decimal(2) ** LN_SHIFT
+    unit = Decimal(2) ** LN_UNIT
+    sqrt_d = Decimal(d).sqrt()
+    sx = _dec(S_x)
+    g = np.array([_round_dec(two_n * sqrt_d * _dec(gm) / (unit * sx)) for gm in gamma], dtype=np.int64)
+    c = np.array([_round_dec(two_n * _dec(bt) / sx) for bt in beta], dtype=np.int64)
+    if np.any(np.abs(g) >= (1 << 24)):
+        raise ValueError("LayerNorm multiplier outside (-2^24, 2^24)")
+    return g.astype(np.int32), c
+
+
+def swish_constants(S_h: float, a: float = SWISH_A, c: float = SWISH_C):
+    """Integer constants of Eq. 12 on an input grid S_h, and the output grid."""
+    S_u = _dec(S_h) / 2
+    A = Decimal(str(a))
+    q_c = int((Decimal(str(c)) / S_u).to_integral_value(rounding=ROUND_FLOOR))
+    q_1 = int((1 / (A * S_u * S_u)).to_integral_value(rounding=ROUND_FLOOR))
+    S_sw = -A * S_u * S_u * _dec(S_h) / 2
+    return q_c, q_1, S_sw
+
+
+def make_ffn(d_model: int, regime: str, seed: int, S_z: float, d_ff: Optional[int] = None) -> Ffn:
+    """Draws one feed-forward module for inputs on grid S_z (a generator of its own)."""
+    rng = np.random.default_rng(seed)
+    d = d_model
+    f = d_ff or FFN_MULT * d
+    w1 = _uniform_i8(rng, (f, d))
+    w2 = _uniform_i8(rng, (d, f))
+    gamma = rng.uniform(0.5, 1.5, size=d)
+    beta = rng.uniform(-0.25, 0.25, size=d)
+    if regime == "literal":
+        u = lambda size=None: rng.uniform(SCALE_LO, SCALE_HI, size=size)  # noqa: E731
+        S_W1, S_W2 = u(f), u(d)
+        S_x, S_h, S_o, S_y, S_z2 = (float(u()) for _ in range(5))
+    elif regime == "calibrated":
+        kcov = 4.0
+        S_x = kcov * 1.5 / 127.0  # LayerNorm output: unit variance times gamma <= 1.5
+        S_W1 = rng.uniform(0.75, 1.0, size=f) / (SIGMA_W * math.sqrt(d))
+        S_W2 = rng.uniform(0.75, 1.0, size=d) / (SIGMA_W * math.sqrt(f))
+        S_h = kcov / 127.0  # W1's output: about unit variance
+        S_o = kcov * 0.6 / 127.0  # Swish of a unit normal: rms about 0.6
+        S_y = kcov * 0.6 / 127.0
+        sz = S_z * 127.0 / 4.0  # the input's grid covers +-4 of its standard deviations
+        S_z2 = 4.0 * math.sqrt(sz * sz + (0.5 * 0.6) ** 2) / 127.0
+    else:
+        raise ValueError(regime)
+    n = SHIFT_N
+    mult1 = np.array([fixed_point(_dec(S_x) * _dec(s) / _dec(S_h), n) for s in S_W1], dtype=np.int32)
+    mult2 = np.array([fixed_point(_dec(S_o) * _dec(s) / _dec(S_y), n) for s in S_W2], dtype=np.int32)
+    q_c, q_1, S_sw = swish_constants(S_h)
+    m_sw, shift_sw = fixed_point_fine(S_sw / _dec(S_o))
+    g, c = _ln_consts(d, gamma, beta, S_x)
+    return Ffn(d_model=d, d_ff=f, w1=w1, w2=w2, mult1=mult1, shift1=n, mult2=mult2, shift2=n,
+               sw_qc=q_c, sw_q1=q_1, m_sw=m_sw, shift_sw=shift_sw, ln_mult=g, ln_bias=c, ln_shift=LN_SHIFT,
+               m_z=fixed_point(_dec(S_z) / _dec(S_z2)), m_y=fixed_point(Decimal("0.5") * _dec(S_y) / _dec(S_z2)),
+               shift_r=SHIFT_N,
+               scales={"S_z": S_z, "S_x": S_x, "S_W1": S_W1, "S_h": S_h, "S_sw": float(S_sw), "S_o": S_o,
+                       "S_W2": S_W2, "S_y": S_y, "S_z2": S_z2, "gamma": gamma, "beta": beta})
