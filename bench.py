@@ -109,7 +109,7 @@ def main():
         return
 
     from paper_2609_30846_amd import ipk
-    from workloads import make_residual, make_workload
+    from workloads import make_ffn, make_residual, make_workload
 
     ipk.load()  # fails loudly when the HIP library is missing
     wl = make_workload(args.workload, args.regime)
@@ -189,6 +189,14 @@ def main():
         mod.set_residual_from(make_residual(blk, args.regime, seed=wl.seed + 1))
         ms_module = timed(lambda: mod.residual(x, pe, lengths=lengths, z2=z2, stream=stream), n_stage)
         y_kept_matches = bool(torch.equal(y_kept, y))
+        # the feed-forward module of Eq. 1 (LayerNorm, W1 with the integer Swish, W2
+        # with the half-step residual) on the same rows, d_ff = 4 d
+        ffn_par = make_ffn(d, args.regime, seed=wl.seed + 2, S_z=blk.scales["S_x"])
+        ffn = ipk.FeedForward(ffn_par, max_rows=B * T, device=dev)
+        z_ffn = torch.empty_like(x)
+        ms_ffn = timed(lambda: ffn(x, z_out=z_ffn, stream=stream), n_stage)
+        ffn_ops = 2 * 2 * B * T * d * ffn_par.d_ff
+        ffn.close()
 
     proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
     ops = 2 * (proj + pos + attn)
@@ -232,6 +240,13 @@ def main():
             "mhsa_module_layernorm_residual": {
                 "ms_per_step": round(ms_module, 5),
                 "frames_per_s": round(float(np.sum(lengths)) / (ms_module * 1e-3), 1),
+            },
+            "ffn_module_minimax_swish": {
+                "ms_per_step": round(ms_ffn, 5),
+                "rows": B * T,
+                "d_ff": ffn_par.d_ff,
+                "tops": round(ffn_ops / (ms_ffn * 1e-3) / 1e12, 3),
+                "pct_int8_peak": round(100.0 * ffn_ops / (ms_ffn * 1e-3) / 1e12 / INT8_PEAK_TOPS, 3),
             },
             "timing": f"{n_stage} steps each between two HIP events, after 5 warm-up steps",
         },

@@ -225,6 +225,66 @@ int ipk_mhsa_residual_set(ipk_relpos_attn_t* h, const ipk_mhsa_residual_desc* r)
 int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* pos_table, const int32_t* lengths,
                           int32_t B, int32_t T, int8_t* z2, void* stream);
 
+/*
+ * The feed-forward module of the Conformer block (Eq. 1) on integer grids:
+ *   x  = LN(z)                                   the LayerNorm above, on ln_mult/ln_bias/ln_shift
+ *   h  = clamp8(RS(x W1^T, mult1[c], shift1))    Eq. 7, d_ff outputs per row
+ *   q  = -(|h| L + h sw_q1),  L = (min(|h|, sw_qc) - sw_qc)^2 + sw_q1
+ *                                                the minimax integer Swish (Sec. 3.2, Eq. 12
+ *                                                with Eq. 13's (a*, c*)) on h's grid S:
+ *                                                sw_qc = floor(c* / (S/2)),
+ *                                                sw_q1 = floor(1 / (a* (S/2)^2)) (negative)
+ *   o  = clamp8(RS(q, m_sw, shift_sw))           to W2's input grid
+ *   y  = clamp8(RS(o W2^T, mult2[c], shift2))    Eq. 7, d_model outputs per row
+ *   z' = clamp8(RS(m_z z + m_y y, 1, shift_r))   the half-step residual (the 0.5 of Eq. 1 in m_y)
+ * Shapes: d_model and d_ff multiples of 64, d_model <= 16384, d_ff <= 65536;
+ * max_rows >= 1 with max_rows * d_ff < 2^31.
+ * Weights (DEVICE, int8, row-major, y = x W^T): w1 [d_ff][d_model], w2 [d_model][d_ff].
+ * Multipliers (HOST, int32): mult1 [d_ff], mult2 [d_model], each in [0, 2^23).
+ * LayerNorm constants (HOST): as ipk_mhsa_residual_desc.
+ * Ranges: shifts in [1, 40] (ln_shift in [1, 62]); 0 <= m_sw, m_z, m_y < 2^23;
+ * 0 <= sw_qc < 2^20; and |q m_sw| + 2^(shift_sw - 1) < 2^62 for every int8 h
+ * (IPK_ERR_UNSUPPORTED otherwise).
+ */
+typedef struct ipk_ffn_desc {
+  int32_t d_model, d_ff, max_rows;
+  const int8_t *w1, *w2;
+  const int32_t *mult1, *mult2;
+  int32_t shift1, shift2;
+  int32_t sw_qc, sw_q1;
+  int32_t m_sw, shift_sw;
+  const int32_t* ln_mult;
+  const int64_t* ln_bias;
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
+} ipk_ffn_desc;
+
+typedef struct ipk_ffn ipk_ffn_t;
+
+/* Validates `desc`, allocates the handle and its workspace for max_rows rows and
+ * keeps device copies of the weights (in MFMA fragment order), the multipliers and
+ * the Swish of every int8 input (a 256-entry table, computed on the device).
+ * Synchronizes its own copies.  Returns IPK_OK and sets *out, or a negative status
+ * with *out = NULL and nothing leaked. */
+int ipk_ffn_create(const ipk_ffn_desc* desc, ipk_ffn_t** out);
+
+/* Runs the module on `stream` over `rows` rows: z DEVICE int8 [rows][d_model] ->
+ * z_out DEVICE int8 [rows][d_model], both 16-byte aligned; z_out may be z itself (in
+ * place) but may not overlap it otherwise.  Asynchronous; calls on one handle must be
+ * ordered on one stream.  Errors: IPK_ERR_INVALID_ARG (null handle or pointer,
+ * misalignment, partial overlap, rows outside [1, max_rows]), IPK_ERR_HIP. */
+int ipk_ffn_run(ipk_ffn_t* h, const int8_t* z, int32_t rows, int8_t* z_out, void* stream);
+
+/* Copies an intermediate of the last run into `dst` (DEVICE, `bytes` bytes), on
+ * `stream`: IPK_FFN_X the LayerNorm output int8 [rows][d_model], IPK_FFN_O the Swish
+ * output int8 [rows][d_ff].  Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`,
+ * bytes too small, null), IPK_ERR_HIP. */
+enum { IPK_FFN_X = 0, IPK_FFN_O = 1 };
+int ipk_ffn_intermediate(ipk_ffn_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
+
+/* Frees the handle after synchronizing the device; NULL is a no-op. */
+int ipk_ffn_destroy(ipk_ffn_t* h);
+
 /* Human-readable name of a status code (static storage). */
 const char* ipk_status_string(int status);
 

@@ -46,6 +46,10 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 enum OutMode { OUT_QKV = 0, OUT_POS = 1, OUT_ROWMAJOR = 2 };
+// Epilogues of row-major outputs: the requantized int8 values themselves, the residual
+// add of Eq. 2 (with z1 laid out as the output), or the integer Swish of Eq. 12 and
+// its requantization, applied through a 256-entry table indexed by the biased code.
+enum Epilogue { EPI_PLAIN = 0, EPI_RESID = 1, EPI_SWISH = 2 };
 
 struct GemmProblem {
   const int8_t* x;      // [nb][rows][K] activations
@@ -71,6 +75,7 @@ struct GemmArgs {
   // m_y y, 1, shift_r)) with z1 laid out as y
   const int8_t* z1;
   int m_z, m_y, shift_r;
+  const uint8_t* swtab;  // EPI_SWISH: output byte of each biased code h + 128
 };
 
 constexpr int BK = 128;  // bytes of K per step
@@ -101,7 +106,10 @@ __device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2,
 // statement, so independent values overlap instead of running as one long chain.
 // v_cvt_i32_f64 truncates and saturates to the int32 range; truncation equals the
 // floor wherever the clamp to [1, 255] does not decide the result (t >= 1).
-__device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16], uint32_t (&D)[4]) {
+// With SW, each code goes through the Swish table `stab` (LDS) instead.
+template <bool SW = false>
+__device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16], uint32_t (&D)[4],
+                                          const uint8_t* stab = nullptr) {
   double t[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) t[e] = __builtin_fma((double)a[e], sc[e], 128.5);
@@ -112,9 +120,17 @@ __device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16],
         : "=&v"(v[4 * g]), "=&v"(v[4 * g + 1]), "=&v"(v[4 * g + 2]), "=&v"(v[4 * g + 3])
         : "v"(t[4 * g]), "v"(t[4 * g + 1]), "v"(t[4 * g + 2]), "v"(t[4 * g + 3]));
 #pragma unroll
-  for (int g = 0; g < 4; ++g)
-    D[g] = pack4((uint32_t)min(max(v[4 * g], 1), 255), (uint32_t)min(max(v[4 * g + 1], 1), 255),
-                 (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
+  for (int g = 0; g < 4; ++g) {
+    if constexpr (SW) {
+      uint32_t o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = stab[min(max(v[4 * g + e], 1), 255)];
+      D[g] = o[0] | (o[1] << 8) | (o[2] << 16) | (o[3] << 24);
+    } else {
+      D[g] = pack4((uint32_t)min(max(v[4 * g], 1), 255), (uint32_t)min(max(v[4 * g + 1], 1), 255),
+                   (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
+    }
+  }
 }
 
 // The residual add of Eq. 2 on 16 int8 pairs: clamp8(floor((m_z z + m_y y + 2^(n-1)) / 2^n)).
@@ -140,8 +156,8 @@ __device__ __forceinline__ v4i residual16(const v4i& y, const v4i& z, int m_z, i
 // WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  The weights
 // come pre-packed in MFMA fragment order (wfrag_index): each wave streams its own
 // fragments from memory straight into registers, one K step ahead, and only the token
-// tile goes through LDS.  RESID: row-major outputs with the residual add fused.
-template <int TN, int TM, int NWAVE, int WN, bool RESID>
+// tile goes through LDS.  EPI: the epilogue of row-major outputs.
+template <int TN, int TM, int NWAVE, int WN, int EPI>
 __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 64 * NWAVE;
   constexpr int WM = NWAVE / WN;            // waves along M
@@ -157,6 +173,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   // two LDS buffers: the next K step is stored while the current one is multiplied
   __shared__ __align__(16) int8_t sx[2][TM * BK];
   __shared__ double ssc[TN];
+  __shared__ uint32_t stab32[EPI == EPI_SWISH ? 64 : 1];  // the Swish table (read after the K loop)
 
   // XCD-aware deal: workgroup i runs on XCD i % 8; XCD x owns logical tiles
   // [x * per_xcd, (x + 1) * per_xcd)
@@ -187,6 +204,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   const int wn = wave % WN, wm = wave / WN;
 
   if (tid < TN) ssc[tid] = P.scale[min(n0 + tid, N - 1)];
+  if (EPI == EPI_SWISH && tid < 64) stab32[tid] = ((const uint32_t*)args.swtab)[tid];
 
   // thread -> (row, chunk) of the fetch: 8 threads cover one 128-byte row segment.
   // Raw buffer loads: rows past the end of the operand (their whole offset is in the
@@ -383,7 +401,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       uint32_t D[4];
-      requant16(acc[i][j], sc, D);
+      requant16<EPI == EPI_SWISH>(acc[i][j], sc, D, (const uint8_t*)stab32);
       const auto x02 = __builtin_amdgcn_permlane32_swap(D[0], D[2], false, false);
       const auto x13 = __builtin_amdgcn_permlane32_swap(D[1], D[3], false, false);
       v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
@@ -393,7 +411,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       // channels of one token
       const uint32_t joff = vwave ? ((uint32_t)(j >> 1) << (dks + 6)) + (uint32_t)(j & 1) * 512u : (uint32_t)j * jstep;
       if (tl + j * 32 < tmax) {
-        if (RESID)
+        if (EPI == EPI_RESID)
           out = residual16(out, *(const v4i*)(zsrc + (off0 + joff)), args.m_z, args.m_y, args.shift_r);
         *(v4i*)(dst + (off0 + joff)) = out;
       }
@@ -457,11 +475,11 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWAVE, int WN, bool RESID = false>
+template <int TN, int TM, int NWAVE, int WN, int EPI = EPI_PLAIN>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, RESID>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
+  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
                        a);
 }
 
@@ -511,8 +529,57 @@ hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Wor
   constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  if (res) return launch_gemm<TN, TM, NWAVE, WN, true>(a, tiles, st, ev);
+  if (res) return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, ev);
   return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
+}
+
+// ---------------------------------------------------------------------------
+// The feed-forward module of Eq. 1: W1 with the integer Swish in its epilogue, W2
+// with the residual add in its epilogue.
+
+// The integer Swish of Eq. 12 and its requantization to FFN2's input grid, for every
+// int8 input h (one thread per biased code h + 128; code 0 is never looked up):
+//   L = (min(|h|, q_c) - q_c)^2 + q_1,  q = -(|h| L + h q_1),  o = clamp8(RS(q, m, n)).
+// The host checks that |q m| + 2^(n-1) stays below 2^62 for every h.
+__global__ __launch_bounds__(256) void swish_table(uint8_t* tab, long long q_c, long long q_1, long long m,
+                                                   int shift) {
+  const long long h = (long long)threadIdx.x - 128;
+  const long long ah = h < 0 ? -h : h;
+  const long long t = (ah < q_c ? ah : q_c) - q_c;
+  const long long L = t * t + q_1;
+  const long long q = -(ah * L + h * q_1);
+  const long long o = (q * m + (1ll << (shift - 1))) >> shift;
+  tab[threadIdx.x] = (uint8_t)(int)(o < -127 ? -127 : (o > 127 ? 127 : o));
+}
+
+hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st) {
+  hipLaunchKernelGGL(swish_table, dim3(1), dim3(256), 0, st, tab, q_c, q_1, m, shift);
+  return hipGetLastError();
+}
+
+hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
+                         const uint8_t* swtab, int8_t* o, hipStream_t st) {
+  GemmArgs a{};
+  a.y = o;
+  a.swtab = swtab;
+  constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
+  const int tiles = add_problem(a, 0, x, w1, scale1, 1, rows, d_ff, d, OUT_ROWMAJOR, 0, TN, TM);
+  a.nprob = 1;
+  return launch_gemm<TN, TM, NWAVE, WN, EPI_SWISH>(a, tiles, st, LaunchEv{});
+}
+
+hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int8_t* w2, const double* scale2,
+                           const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st) {
+  GemmArgs a{};
+  a.y = z_out;
+  a.z1 = z;
+  a.m_z = m_z;
+  a.m_y = m_y;
+  a.shift_r = shift_r;
+  constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
+  const int tiles = add_problem(a, 0, o, w2, scale2, 1, rows, d, d_ff, OUT_ROWMAJOR, 0, TN, TM);
+  a.nprob = 1;
+  return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, LaunchEv{});
 }
 
 // one thread per 16-byte piece of the destination

@@ -2,7 +2,8 @@
 // workspace, and the per-run launch sequence
 //   projections (Q|K|V and the position table) -> rank-1 bias terms and V prefix
 //   sums -> attention core -> output projection; for the MHSA module of Eq. 2 an
-//   integer LayerNorm first and the residual add in the output projection's epilogue.
+//   integer LayerNorm first and the residual add in the output projection's epilogue;
+//   and the feed-forward module of Eq. 1 (LayerNorm, W1 + integer Swish, W2 + residual).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdarg.h>
@@ -455,6 +456,195 @@ extern "C" int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h) {
   (void)hipSetDevice(h->device);
   hipError_t e = hipDeviceSynchronize();
   free_handle(h);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The feed-forward module of Eq. 1.
+
+struct ipk_ffn {
+  int device;
+  int d, f, max_rows;
+  int8_t *w1, *w2;            // fragment order (wfrag_index)
+  double *scale1, *scale2;    // m 2^-n per output channel
+  uint8_t* swtab;             // 256 bytes: Swish output of each biased code h + 128
+  int8_t *x, *o;              // LayerNorm output [max_rows][d], Swish output [max_rows][f]
+  Residual res;
+  int last_rows;
+  std::vector<void*> allocs;
+};
+
+static void free_ffn(ipk_ffn* h) {
+  if (!h) return;
+  for (void* p : h->allocs) (void)hipFree(p);
+  delete h;
+}
+
+template <typename T>
+static hipError_t ffn_alloc(ipk_ffn* h, T** p, size_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
+  if (e != hipSuccess) return e;
+  h->allocs.push_back(q);
+  *p = (T*)q;
+  return hipSuccess;
+}
+
+static int validate_ffn(const ipk_ffn_desc* D) {
+  if (!D) return fail(IPK_ERR_INVALID_ARG, "desc is NULL");
+  if (D->d_model < 64 || D->d_model % 64 || D->d_model > 16384)
+    return fail(IPK_ERR_INVALID_ARG, "d_model=%d must be a multiple of 64 in [64, 16384]", D->d_model);
+  if (D->d_ff < 64 || D->d_ff % 64 || D->d_ff > 65536)
+    return fail(IPK_ERR_INVALID_ARG, "d_ff=%d must be a multiple of 64 in [64, 65536]", D->d_ff);
+  if (D->max_rows < 1 || (int64_t)D->max_rows * D->d_ff >= ((int64_t)1 << 31))
+    return fail(IPK_ERR_INVALID_ARG, "max_rows=%d outside [1, 2^31 / d_ff)", D->max_rows);
+  if (!D->w1 || !D->w2 || !D->mult1 || !D->mult2 || !D->ln_mult || !D->ln_bias)
+    return fail(IPK_ERR_INVALID_ARG, "a weight, multiplier or LayerNorm pointer is NULL");
+  for (int c = 0; c < D->d_ff; ++c)
+    if (!mult_ok(D->mult1[c])) return fail(IPK_ERR_INVALID_ARG, "mult1[%d]=%d outside [0, 2^23)", c, D->mult1[c]);
+  for (int c = 0; c < D->d_model; ++c)
+    if (!mult_ok(D->mult2[c])) return fail(IPK_ERR_INVALID_ARG, "mult2[%d]=%d outside [0, 2^23)", c, D->mult2[c]);
+  if (!shift_ok(D->shift1) || !shift_ok(D->shift2) || !shift_ok(D->shift_sw) || !shift_ok(D->shift_r))
+    return fail(IPK_ERR_INVALID_ARG, "a shift is outside [1, 40]");
+  if (D->ln_shift < 1 || D->ln_shift > 62) return fail(IPK_ERR_INVALID_ARG, "ln_shift=%d outside [1, 62]", D->ln_shift);
+  if (!mult_ok(D->m_sw) || !mult_ok(D->m_z) || !mult_ok(D->m_y))
+    return fail(IPK_ERR_INVALID_ARG, "m_sw, m_z and m_y must be in [0, 2^23)");
+  for (int k = 0; k < D->d_model; ++k) {
+    if (D->ln_mult[k] <= -(1 << 24) || D->ln_mult[k] >= (1 << 24))
+      return fail(IPK_ERR_INVALID_ARG, "ln_mult[%d]=%d outside (-2^24, 2^24)", k, D->ln_mult[k]);
+    if (D->ln_bias[k] <= -((int64_t)1 << 56) || D->ln_bias[k] >= ((int64_t)1 << 56))
+      return fail(IPK_ERR_INVALID_ARG, "ln_bias[%d] outside (-2^56, 2^56)", k);
+  }
+  if (D->sw_qc < 0 || D->sw_qc >= (1 << 20)) return fail(IPK_ERR_INVALID_ARG, "sw_qc=%d outside [0, 2^20)", D->sw_qc);
+  // the Swish table kernel evaluates q m_sw + 2^(n-1) in 64 bits: bound it for every h
+  for (int hv = -127; hv <= 127; ++hv) {
+    const __int128 ah = hv < 0 ? -hv : hv;
+    const __int128 t = (ah < D->sw_qc ? ah : (__int128)D->sw_qc) - D->sw_qc;
+    const __int128 L = t * t + D->sw_q1;
+    __int128 q = -(ah * L + (__int128)hv * D->sw_q1);
+    if (q < 0) q = -q;
+    if (q * D->m_sw + ((__int128)1 << (D->shift_sw - 1)) >= ((__int128)1 << 62))
+      return fail(IPK_ERR_UNSUPPORTED, "integer Swish times m_sw reaches 2^62 at h=%d", hv);
+  }
+  return IPK_OK;
+}
+
+extern "C" int ipk_ffn_create(const ipk_ffn_desc* desc, ipk_ffn_t** out) {
+  g_last_error[0] = 0;
+  if (!out) return fail(IPK_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int st = validate_ffn(desc);
+  if (st != IPK_OK) return st;
+  ipk_ffn* h = new (std::nothrow) ipk_ffn();
+  if (!h) return fail(IPK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    free_ffn(h);
+    return fail(IPK_ERR_HIP, "hipGetDevice failed");
+  }
+  const size_t d = desc->d_model, f = desc->d_ff, R = desc->max_rows;
+  h->d = (int)d;
+  h->f = (int)f;
+  h->max_rows = (int)R;
+  h->last_rows = 0;
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+  };
+  int32_t* g = nullptr;
+  int64_t* c = nullptr;
+  int8_t* stage = nullptr;
+  chk(ffn_alloc(h, &h->w1, f * d));
+  chk(ffn_alloc(h, &h->w2, d * f));
+  chk(ffn_alloc(h, &h->scale1, f));
+  chk(ffn_alloc(h, &h->scale2, d));
+  chk(ffn_alloc(h, &h->swtab, 256));
+  chk(ffn_alloc(h, &h->x, R * d));
+  chk(ffn_alloc(h, &h->o, R * f));
+  chk(ffn_alloc(h, &g, d));
+  chk(ffn_alloc(h, &c, d));
+  chk(ffn_alloc(h, &stage, f * d));
+  if (e != hipSuccess) {
+    free_ffn(h);
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
+                hipGetErrorString(e));
+  }
+  chk(hipMemcpy(stage, desc->w1, f * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w1, (int)f, (int)d, nullptr));
+  chk(hipMemcpy(stage, desc->w2, d * f, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w2, (int)d, (int)f, nullptr));
+  std::vector<double> s1(f), s2(d);
+  for (size_t k = 0; k < f; ++k) s1[k] = ldexp((double)desc->mult1[k], -desc->shift1);
+  for (size_t k = 0; k < d; ++k) s2[k] = ldexp((double)desc->mult2[k], -desc->shift2);
+  chk(hipMemcpy(h->scale1, s1.data(), f * sizeof(double), hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->scale2, s2.data(), d * sizeof(double), hipMemcpyHostToDevice));
+  std::vector<int64_t> cb(d);
+  for (size_t k = 0; k < d; ++k) cb[k] = desc->ln_bias[k] + ((int64_t)1 << (desc->ln_shift - 1));
+  chk(hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
+  chk(hipMemcpy(c, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice));
+  chk(launch_swish_table(h->swtab, desc->sw_qc, desc->sw_q1, desc->m_sw, desc->shift_sw, nullptr));
+  chk(hipDeviceSynchronize());
+  if (e != hipSuccess) {
+    free_ffn(h);
+    (void)hipGetLastError();
+    return fail(IPK_ERR_HIP, "copying the weights failed: %s", hipGetErrorString(e));
+  }
+  h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), (void*)stage));
+  (void)hipFree(stage);
+  h->res.ln_mult = g;
+  h->res.ln_bias = c;
+  h->res.ln_shift = desc->ln_shift;
+  h->res.m_z = desc->m_z;
+  h->res.m_y = desc->m_y;
+  h->res.shift_r = desc->shift_r;
+  *out = h;
+  return IPK_OK;
+}
+
+extern "C" int ipk_ffn_run(ipk_ffn_t* h, const int8_t* z, int32_t rows, int8_t* z_out, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!z || !z_out) return fail(IPK_ERR_INVALID_ARG, "z and z_out must be non-NULL");
+  if (((uintptr_t)z | (uintptr_t)z_out) & 15) return fail(IPK_ERR_INVALID_ARG, "z and z_out must be 16-byte aligned");
+  if (rows < 1 || rows > h->max_rows) return fail(IPK_ERR_INVALID_ARG, "rows=%d outside [1, max_rows=%d]", rows, h->max_rows);
+  if (z != z_out) {
+    const size_t n = (size_t)rows * h->d;
+    const uintptr_t a = (uintptr_t)z, b = (uintptr_t)z_out;
+    if (a < b + n && b < a + n) return fail(IPK_ERR_INVALID_ARG, "z and z_out overlap without being equal");
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
+  if (e == hipSuccess) e = launch_ffn_up(h->x, rows, h->d, h->f, h->w1, h->scale1, h->swtab, h->o, st);
+  if (e == hipSuccess)
+    e = launch_ffn_down(h->o, rows, h->d, h->f, h->w2, h->scale2, z, h->res.m_z, h->res.m_y, h->res.shift_r, z_out, st);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  h->last_rows = rows;
+  return IPK_OK;
+}
+
+extern "C" int ipk_ffn_intermediate(ipk_ffn_t* h, int32_t which, void* dst, int64_t bytes, void* stream) {
+  if (!h || !dst) return fail(IPK_ERR_INVALID_ARG, "handle and dst must be non-NULL");
+  if (!h->last_rows) return fail(IPK_ERR_INVALID_ARG, "no run yet");
+  if (which != IPK_FFN_X && which != IPK_FFN_O) return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
+  const int64_t need = (int64_t)h->last_rows * (which == IPK_FFN_X ? h->d : h->f);
+  if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
+  hipError_t e = hipMemcpyAsync(dst, which == IPK_FFN_X ? h->x : h->o, (size_t)need, hipMemcpyDeviceToDevice,
+                                (hipStream_t)stream);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "copy failed: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+extern "C" int ipk_ffn_destroy(ipk_ffn_t* h) {
+  if (!h) return IPK_OK;
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(h->device);
+  hipError_t e = hipDeviceSynchronize();
+  free_ffn(h);
   if (prev >= 0) (void)hipSetDevice(prev);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
   return IPK_OK;

@@ -142,6 +142,16 @@ hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p
 // Integer LayerNorm of rows [B][T][d] of z into ws.xln.
 hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st,
                             const LaunchEv& ev = {});
+// The feed-forward module (Eq. 1): the Swish table of every int8 input, W1 with the
+// Swish in its epilogue (x [rows][d] -> o [rows][d_ff]), W2 with the residual add in
+// its epilogue (o -> z_out [rows][d]).
+hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st);
+hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
+                         const uint8_t* swtab, int8_t* o, hipStream_t st);
+hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int8_t* w2, const double* scale2,
+                           const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st);
+hipError_t launch_layernorm_rows(long rows, int d, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st);
+
 // Workgroup shapes of the attention core for a run: the first shape's nqb1 query
 // blocks per (utterance, head), then (c2.ksplit != 0) the second shape's nqb2 blocks
 // for the remaining queries.  c1.ksplit == 0 when T_al does not fit LDS.

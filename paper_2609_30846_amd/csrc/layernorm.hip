@@ -77,6 +77,9 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
   if ((sg + 1) * (sg + 1) <= var) ++sg;
   if (sg < 1) sg = 1;
   const long long F = (1ll << 31) / sg;
+  // u = floor(y F / 2) for y = z - mu, in 32 bits: with F = 2 Fh + Fo,
+  // u = y Fh + Fo floor(y / 2), and |y Fh| <= |y| F / 2 <= 2^30 since |y| <= sigma
+  const int Fh = (int)(F >> 1), Fo = (F & 1) ? -1 : 0;
   const int shift = a.shift;
   const int m = (int)mu;
 #pragma unroll
@@ -92,9 +95,9 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int zb = (zv[k][w] << (24 - 8 * b)) >> 24;
-        // |z - mu| <= sigma, so |u| <= 2^30
-        const long long u = ((long long)(zb - m) * F) >> 1;
-        const long long t = (u * gv[b] + a.c[c0 + 4 * w + b]) >> shift;
+        const int y = zb - m;
+        const int u = y * Fh + ((y >> 1) & Fo);
+        const long long t = ((long long)u * gv[b] + a.c[c0 + 4 * w + b]) >> shift;
         o |= ((uint32_t)(int)min(max(t, -127ll), 127ll) & 0xFFu) << (8 * b);
       }
       out[w] = (int)o;
@@ -103,25 +106,34 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
   }
 }
 
-hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st,
+static hipError_t launch_ln(long rows, int d, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st,
                             const LaunchEv& ev) {
   LnArgs a{};
   a.z = z;
   a.x = out;
   a.g = r.ln_mult;
   a.c = r.ln_bias;
-  a.rows = (long)rs.B * rs.T;
-  a.d = rs.d;
+  a.rows = rows;
+  a.d = d;
   a.shift = r.ln_shift;
   const dim3 grid((unsigned)((a.rows + LN_WAVES - 1) / LN_WAVES)), block(64 * LN_WAVES);
-  const int np = (rs.d + 1023) / 1024;
-  if (rs.d % 16) return hipErrorInvalidValue;
+  const int np = (d + 1023) / 1024;
+  if (d % 16) return hipErrorInvalidValue;
   if (np <= 1) return launch_kernel(layernorm_i8<1>, grid, block, 0, st, ev, a);
   if (np <= 2) return launch_kernel(layernorm_i8<2>, grid, block, 0, st, ev, a);
   if (np <= 4) return launch_kernel(layernorm_i8<4>, grid, block, 0, st, ev, a);
   if (np <= 8) return launch_kernel(layernorm_i8<8>, grid, block, 0, st, ev, a);
   if (np <= 16) return launch_kernel(layernorm_i8<16>, grid, block, 0, st, ev, a);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st,
+                            const LaunchEv& ev) {
+  return launch_ln((long)rs.B * rs.T, rs.d, r, z, out, st, ev);
+}
+
+hipError_t launch_layernorm_rows(long rows, int d, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st) {
+  return launch_ln(rows, d, r, z, out, st, LaunchEv{});
 }
 
 }  // namespace ipk

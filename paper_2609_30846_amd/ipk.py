@@ -26,6 +26,7 @@ IPK_ERR_HIP = -4
 IPK_MAX_BATCH = 256
 IPK_MAX_T = 8192
 IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN = range(6)
+IPK_FFN_X, IPK_FFN_O = range(2)
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p
@@ -38,6 +39,10 @@ SIGNATURES = [
     ("ipk_relpos_attn_cache_positions", C.c_int, [_vp, _vp, C.c_int32, _vp]),
     ("ipk_mhsa_residual_set", C.c_int, [_vp, _vp]),
     ("ipk_mhsa_residual_run", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
+    ("ipk_ffn_create", C.c_int, [_vp, C.POINTER(_vp)]),
+    ("ipk_ffn_run", C.c_int, [_vp, _vp, C.c_int32, _vp, _vp]),
+    ("ipk_ffn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
+    ("ipk_ffn_destroy", C.c_int, [_vp]),
     ("ipk_status_string", C.c_char_p, [C.c_int]),
     ("ipk_last_error", C.c_char_p, []),
     ("ipk_abi_version", C.c_int, []),
@@ -72,6 +77,20 @@ class ResidualDesc(C.Structure):
     """Mirror of ipk_mhsa_residual_desc."""
 
     _fields_ = [
+        ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
+        ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
+    ]
+
+
+class FfnDesc(C.Structure):
+    """Mirror of ipk_ffn_desc."""
+
+    _fields_ = [
+        ("d_model", C.c_int32), ("d_ff", C.c_int32), ("max_rows", C.c_int32),
+        ("w1", _vp), ("w2", _vp), ("mult1", _vp), ("mult2", _vp),
+        ("shift1", C.c_int32), ("shift2", C.c_int32),
+        ("sw_qc", C.c_int32), ("sw_q1", C.c_int32),
+        ("m_sw", C.c_int32), ("shift_sw", C.c_int32),
         ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
         ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
     ]
@@ -276,6 +295,81 @@ class RelPosAttn:
     def close(self):
         if getattr(self, "handle", None):
             ipk_relpos_attn_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ipk_ffn_create(desc: FfnDesc) -> int:
+    h = _vp()
+    _check(load().ipk_ffn_create(C.byref(desc), C.byref(h)))
+    return h.value
+
+
+def ipk_ffn_run(h: int, z, rows: int, z_out, stream=None) -> None:
+    _check(load().ipk_ffn_run(h, _ptr(z), int(rows), _ptr(z_out), _stream_ptr(stream)))
+
+
+def ipk_ffn_intermediate(h: int, which: int, dst, stream=None) -> None:
+    _check(load().ipk_ffn_intermediate(h, int(which), _ptr(dst), int(dst.numel() * dst.element_size()),
+                                       _stream_ptr(stream)))
+
+
+def ipk_ffn_destroy(h: Optional[int]) -> None:
+    _check(load().ipk_ffn_destroy(h))
+
+
+class FeedForward:
+    """Owns one feed-forward module handle (Eq. 1), built from host arrays: ``ffn``
+    carries w1, w2, mult1, mult2, the shifts, the Swish constants sw_qc, sw_q1, m_sw,
+    shift_sw, the LayerNorm constants and the residual multipliers."""
+
+    def __init__(self, ffn, max_rows: int, device=None):
+        import torch
+
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        keep = {}
+        desc = FfnDesc()
+        desc.d_model, desc.d_ff, desc.max_rows = int(ffn.d_model), int(ffn.d_ff), int(max_rows)
+        for k in ("w1", "w2"):
+            t = torch.as_tensor(np.ascontiguousarray(getattr(ffn, k), dtype=np.int8)).to(dev)
+            keep[k] = t
+            setattr(desc, k, t.data_ptr())
+        for k, dt in (("mult1", np.int32), ("mult2", np.int32), ("ln_mult", np.int32), ("ln_bias", np.int64)):
+            a = np.ascontiguousarray(getattr(ffn, k), dtype=dt)
+            keep[k] = a
+            setattr(desc, k, a.ctypes.data)
+        for k in ("shift1", "shift2", "sw_qc", "sw_q1", "m_sw", "shift_sw", "ln_shift", "m_z", "m_y", "shift_r"):
+            setattr(desc, k, int(getattr(ffn, k)))
+        with torch.cuda.device(dev):
+            self.handle = ipk_ffn_create(desc)
+        self.device = dev
+        self.d_model, self.d_ff, self.max_rows = int(ffn.d_model), int(ffn.d_ff), int(max_rows)
+
+    def __call__(self, z, z_out=None, stream=None):
+        import torch
+
+        rows = z.numel() // self.d_model
+        if z_out is None:
+            z_out = torch.empty_like(z)
+        ipk_ffn_run(self.handle, z, rows, z_out, stream)
+        return z_out
+
+    def intermediate(self, which: int, rows: int, stream=None):
+        import torch
+
+        dst = torch.empty((rows, self.d_model if which == IPK_FFN_X else self.d_ff), dtype=torch.int8,
+                          device=self.device)
+        ipk_ffn_intermediate(self.handle, which, dst, stream)
+        return dst
+
+    def close(self):
+        if getattr(self, "handle", None):
+            ipk_ffn_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -59,6 +59,13 @@ def test_residual_descriptor_struct_matches_header_field_order():
     assert names == [f[0] for f in ipk.ResidualDesc._fields_]
 
 
+def test_ffn_descriptor_struct_matches_header_field_order():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct ipk_ffn_desc \{(.*?)\}", text, flags=re.S).group(1)
+    names = re.findall(r"\*?(\w+)\s*[,;]", body)
+    assert names == [f[0] for f in ipk.FfnDesc._fields_]
+
+
 def _valid_desc():
     """A descriptor that passes validation (weights point to dummy host memory)."""
     blk = make_workload("tiny", "calibrated").blocks[0]
@@ -160,3 +167,59 @@ def test_generated_constants_pass_validation_ranges():
             poly_max = max(q_b * q_b, (q_b - q_ln2 + 1) ** 2) + q_c
             assert q_ln2 >= 1 and 256 <= q_b * q_b + q_c and poly_max < (1 << 24)
             assert 8192 * poly_max < (1 << 32)
+
+
+def _valid_ffn_desc():
+    """A feed-forward descriptor that passes validation (weights: dummy host memory)."""
+    from workloads import make_ffn
+
+    f = make_ffn(256, "calibrated", seed=3, S_z=1.0 / 32)
+    keep = []
+    d = ipk.FfnDesc()
+    d.d_model, d.d_ff, d.max_rows = 256, 1024, 64
+    dummy = np.zeros(16, dtype=np.int8)
+    keep.append(dummy)
+    d.w1 = d.w2 = dummy.ctypes.data
+    for k, dt in (("mult1", np.int32), ("mult2", np.int32), ("ln_mult", np.int32), ("ln_bias", np.int64)):
+        a = np.ascontiguousarray(getattr(f, k), dtype=dt)
+        keep.append(a)
+        setattr(d, k, a.ctypes.data)
+    for k in ("shift1", "shift2", "sw_qc", "sw_q1", "m_sw", "shift_sw", "ln_shift", "m_z", "m_y", "shift_r"):
+        setattr(d, k, int(getattr(f, k)))
+    return d, keep
+
+
+BAD_FFN = [
+    ("d_model", 100, ipk.IPK_ERR_INVALID_ARG),
+    ("d_ff", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("max_rows", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("w2", None, ipk.IPK_ERR_INVALID_ARG),
+    ("ln_bias", None, ipk.IPK_ERR_INVALID_ARG),
+    ("shift_sw", 41, ipk.IPK_ERR_INVALID_ARG),
+    ("ln_shift", 63, ipk.IPK_ERR_INVALID_ARG),
+    ("m_sw", 1 << 23, ipk.IPK_ERR_INVALID_ARG),
+    ("sw_qc", -1, ipk.IPK_ERR_INVALID_ARG),
+    ("sw_qc", 1 << 20, ipk.IPK_ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("field,value,want", BAD_FFN)
+def test_ffn_create_rejects_invalid_descriptor(field, value, want):
+    d, keep = _valid_ffn_desc()
+    setattr(d, field, value)
+    h = C.c_void_p()
+    assert ipk.load().ipk_ffn_create(C.byref(d), C.byref(h)) == want
+    assert h.value is None
+    assert ipk.last_error() != ""
+
+
+def test_ffn_create_rejects_swish_overflow():
+    # a Swish whose q m_sw reaches 2^62 for some int8 input
+    d, keep = _valid_ffn_desc()
+    d.sw_qc, d.sw_q1, d.m_sw, d.shift_sw = (1 << 20) - 1, -(1 << 30), (1 << 23) - 1, 40
+    h = C.c_void_p()
+    assert ipk.load().ipk_ffn_create(C.byref(d), C.byref(h)) == ipk.IPK_ERR_UNSUPPORTED
+    lib = ipk.load()
+    assert lib.ipk_ffn_run(None, None, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_ffn_intermediate(None, 0, None, 0, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_ffn_destroy(None) == ipk.IPK_OK
