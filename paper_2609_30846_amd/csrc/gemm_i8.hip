@@ -483,23 +483,46 @@ static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const Laun
                        a);
 }
 
+// Token-tile height for a launch of `tiles_of(TM)` tiles: every tile of a launch runs at
+// once when the tiles fit the CUs, so a launch takes about (rounds over the CUs) x (one
+// tile's K loop, proportional to TM).  The smaller height wins only when it needs
+// fewer rounds x rows (ties keep the larger tile, which has less overhead per row).
+constexpr int kGemmCUs = 256;
+template <typename F>
+static int pick_tile_rows(int big, int small, F tiles_of) {
+  auto cost = [&](int tm) { return (long)((tiles_of(tm) + kGemmCUs - 1) / kGemmCUs) * tm; };
+  return cost(small) < cost(big) ? small : big;
+}
+
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
-  GemmArgs a{};
-  fill_dest(a, rs, ws, nullptr);
-  // 256 x 256 tiles of eight waves in a 4 x 2 grid (64 channels x 128 tokens each): per
-  // K step a workgroup moves 32 KB of token tile and 128 KB of token fragments through
-  // LDS and streams 64 KB of weight fragments (each wave's own, two waves per block)
-  constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
-  // the epilogue's V sums: a wave's tokens are whole 64-key chunks
-  static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
-  int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
-  a.nprob = 1;
-  if (pos_table) {
-    tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
-    a.nprob = 2;
-  }
-  return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
+  // 256-channel tiles of eight waves in a 4 x 2 grid (64 channels x TM/2 tokens each):
+  // with TM = 256, per K step a workgroup moves 32 KB of token tile and 128 KB of token
+  // fragments through LDS and streams 64 KB of weight fragments (each wave's own, two
+  // waves per block).  TM = 128 halves the tiles' height when that fills the CUs better
+  // (Q|K|V alone at T = 2500: 240 tiles in one round instead of 120 of twice the work).
+  constexpr int TN = 256, NWAVE = 8, WN = 4;
+  auto tiles_of = [&](int tm) {
+    long t = (long)rs.B * ((rs.T + tm - 1) / tm) * ((3 * rs.d + TN - 1) / TN);
+    if (pos_table) t += (long)((2 * rs.T - 1 + tm - 1) / tm) * ((rs.d + TN - 1) / TN);
+    return t;
+  };
+  const int TMr = pick_tile_rows(256, 128, tiles_of);
+  auto go = [&](auto tm_tag) {
+    constexpr int TM = decltype(tm_tag)::value;
+    // the epilogue's V sums: a wave's tokens are whole 64-key chunks
+    static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
+    GemmArgs a{};
+    fill_dest(a, rs, ws, nullptr);
+    int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
+    a.nprob = 1;
+    if (pos_table) {
+      tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
+      a.nprob = 2;
+    }
+    return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
+  };
+  return TMr == 128 ? go(std::integral_constant<int, 128>{}) : go(std::integral_constant<int, 256>{});
 }
 
 hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p, const int8_t* pos_table,
@@ -559,13 +582,21 @@ hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long l
 
 hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
                          const uint8_t* swtab, int8_t* o, hipStream_t st) {
-  GemmArgs a{};
-  a.y = o;
-  a.swtab = swtab;
-  constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
-  const int tiles = add_problem(a, 0, x, w1, scale1, 1, rows, d_ff, d, OUT_ROWMAJOR, 0, TN, TM);
-  a.nprob = 1;
-  return launch_gemm<TN, TM, NWAVE, WN, EPI_SWISH>(a, tiles, st, LaunchEv{});
+  // 256-channel tiles of eight waves; 192-token tiles when they need no more rounds
+  // over the CUs than 256-token ones (2500 rows: 224 tiles instead of 160 of 4/3 the work)
+  constexpr int TN = 256, NWAVE = 8, WN = 4;
+  auto tiles_of = [&](int tm) { return (long)((rows + tm - 1) / tm) * ((d_ff + TN - 1) / TN); };
+  auto go = [&](auto tm_tag) {
+    constexpr int TM = decltype(tm_tag)::value;
+    GemmArgs a{};
+    a.y = o;
+    a.swtab = swtab;
+    const int tiles = add_problem(a, 0, x, w1, scale1, 1, rows, d_ff, d, OUT_ROWMAJOR, 0, TN, TM);
+    a.nprob = 1;
+    return launch_gemm<TN, TM, NWAVE, WN, EPI_SWISH>(a, tiles, st, LaunchEv{});
+  };
+  return pick_tile_rows(256, 192, tiles_of) == 192 ? go(std::integral_constant<int, 192>{})
+                                                   : go(std::integral_constant<int, 256>{});
 }
 
 hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int8_t* w2, const double* scale2,
@@ -576,7 +607,10 @@ hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int
   a.m_z = m_z;
   a.m_y = m_y;
   a.shift_r = shift_r;
-  constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
+  // 128 x 128 tiles of eight waves (32 channels x 64 tokens each): K = d_ff is long, so
+  // the larger tile's operand reuse pays (measured against 64 x 64, 128 x 64, 128 x 96
+  // and 64 x 192 tiles at 2500 and 4000 rows)
+  constexpr int TN = 128, TM = 128, NWAVE = 8, WN = 4;
   const int tiles = add_problem(a, 0, o, w2, scale2, 1, rows, d, d_ff, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
   return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, LaunchEv{});
