@@ -156,8 +156,10 @@ __device__ __forceinline__ v4i residual16(const v4i& y, const v4i& z, int m_z, i
 // WN x WM waves (NWAVE = WN WM) each own a (TN/WN) x (TM/WM) sub-tile.  The weights
 // come pre-packed in MFMA fragment order (wfrag_index): each wave streams its own
 // fragments from memory straight into registers, one K step ahead, and only the token
-// tile goes through LDS.  EPI: the epilogue of row-major outputs.
-template <int TN, int TM, int NWAVE, int WN, int EPI>
+// tile goes through LDS.  EPI: the epilogue of row-major outputs.  TPF: register sets of
+// the token tile in flight (2 fetches each step's tile two steps before it is stored, for
+// long K loops whose operands come from beyond the L2).
+template <int TN, int TM, int NWAVE, int WN, int EPI, int TPF>
 __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 64 * NWAVE;
   constexpr int WM = NWAVE / WN;            // waves along M
@@ -216,7 +218,8 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   const int foff = frow * K + fchunk * 16;
 
   // the next step's token tile in registers
-  v4i rx[LX];
+  static_assert(TPF == 1 || TPF == 2, "token prefetch depth");
+  v4i rx[TPF][LX];
   // this wave's weight fragments of one K step (FN channel blocks x KSL slices, 1 KB
   // each, the slices of a block contiguous), two steps in registers.  A slice past K
   // (odd multiples of 64) meets zero tokens, so its contents do not matter; reads past
@@ -234,18 +237,19 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
     }
   };
   // K is a multiple of 64: the last step of an odd multiple fills its upper half with zeros
-  auto fetch = [&](int k0) {
+  auto fetch = [&](int k0, int set) {
     if (k0 + fchunk * 16 < K) {
 #pragma unroll
-      for (int r = 0; r < LX; ++r) rx[r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
+      for (int r = 0; r < LX; ++r)
+        rx[set][r] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(xres, foff + FROWS * r * K + k0, 0, 0);
     } else {
 #pragma unroll
-      for (int r = 0; r < LX; ++r) rx[r] = (v4i){};
+      for (int r = 0; r < LX; ++r) rx[set][r] = (v4i){};
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, int set) {
 #pragma unroll
-    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[r];
+    for (int r = 0; r < LX; ++r) *(v4i*)(sx[buf] + lds_off(frow + FROWS * r, fchunk)) = rx[set][r];
   };
 
   // waves whose channels are V produce the transposed product (tokens along MFMA rows)
@@ -282,15 +286,17 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       }
     };
     // step k is multiplied out of LDS buffer k % 2 (and weight set k % 2) while step
-    // k + 1 (fetched during step k - 1) is stored into the other buffer; one barrier
-    // per step orders both.  Unrolled twice so that the weight set is static.
+    // k + 1 (fetched into token set (k + 1) % TPF, TPF steps earlier) is stored into the
+    // other buffer; one barrier per step orders both.  Unrolled twice so that the weight
+    // and token sets are static.
     wfetch(0, std::integral_constant<int, 0>{});
-    fetch(0);
-    stash(0);
+    fetch(0, 0);
+    stash(0, 0);
     if (nk > 1) {
-      fetch(BK);
+      fetch(BK, 1 % TPF);
       wfetch(1, std::integral_constant<int, 1>{});
     }
+    if (TPF == 2 && nk > 2) fetch(2 * BK, 0);
     __syncthreads();
     for (int kt = 0; kt < nk; kt += 2) {
       static_for<2>([&](auto ph) {
@@ -298,11 +304,9 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
         if (kt + P2 < nk) {
           mma(P2, ph);
           if (kt + P2 + 1 < nk) {
-            stash(P2 ^ 1);
-            if (kt + P2 + 2 < nk) {
-              fetch((kt + P2 + 2) * BK);
-              wfetch(kt + P2 + 2, ph);
-            }
+            stash(P2 ^ 1, (P2 + 1) % TPF);
+            if (kt + P2 + 1 + TPF < nk) fetch((kt + P2 + 1 + TPF) * BK, (P2 + 1) % TPF);
+            if (kt + P2 + 2 < nk) wfetch(kt + P2 + 2, ph);
           }
           __syncthreads();
         }
@@ -475,11 +479,11 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.vsum = ws.vsum;
 }
 
-template <int TN, int TM, int NWAVE, int WN, int EPI = EPI_PLAIN>
+template <int TN, int TM, int NWAVE, int WN, int EPI = EPI_PLAIN, int TPF = 1>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
+  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI, TPF>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
                        a);
 }
 
@@ -552,8 +556,9 @@ hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Wor
   constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
   int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
-  if (res) return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, ev);
-  return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
+  // the token tile two steps ahead: 0.6 - 0.7 us less per call at T = 2500 (interleaved A/B)
+  if (res) return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID, 2>(a, tiles, st, ev);
+  return launch_gemm<TN, TM, NWAVE, WN, EPI_PLAIN, 2>(a, tiles, st, ev);
 }
 
 // ---------------------------------------------------------------------------
