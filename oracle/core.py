@@ -55,6 +55,19 @@ class OracleFfnDesc(C.Structure):
     ]
 
 
+class OracleConvDesc(C.Structure):
+    _fields_ = [
+        ("d_model", C.c_int32),
+        ("w_pw1", i8p), ("mult_pw1", i32p), ("shift_pw1", C.c_int32),
+        ("glu_qc", C.c_int64), ("glu_q1", C.c_int64), ("m_glu", C.c_int32), ("shift_glu", C.c_int32),
+        ("w_dw", i8p), ("bias_dw", i32p), ("mult_dw", i32p), ("shift_dw", C.c_int32),
+        ("sw_qc", C.c_int64), ("sw_q1", C.c_int64), ("m_sw", C.c_int32), ("shift_sw", C.c_int32),
+        ("w_pw2", i8p), ("mult_pw2", i32p), ("shift_pw2", C.c_int32),
+        ("ln_mult", i32p), ("ln_bias", i64p), ("ln_shift", C.c_int32),
+        ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
+    ]
+
+
 def lib():
     global _lib
     with _lock:
@@ -90,6 +103,11 @@ def lib():
             L.ipk_oracle_int_swish.argtypes = [C.c_int64, C.c_int64, C.c_int64]
             L.ipk_oracle_ffn_module.restype = C.c_int
             L.ipk_oracle_ffn_module.argtypes = [C.POINTER(OracleFfnDesc), i8p, C.c_int64, i8p, i8p, i8p, i8p, i8p]
+            L.ipk_oracle_int_sigmoid.restype = C.c_int64
+            L.ipk_oracle_int_sigmoid.argtypes = [C.c_int64, C.c_int64, C.c_int64]
+            L.ipk_oracle_conv_module.restype = C.c_int
+            L.ipk_oracle_conv_module.argtypes = [C.POINTER(OracleConvDesc), i8p, i32p, C.c_int32, C.c_int32, i8p,
+                                                 i8p, i8p, i8p, C.POINTER(C.c_int16), i8p, i8p]
             L.ipk_oracle_relpos_attn.restype = C.c_int
             L.ipk_oracle_relpos_attn.argtypes = [C.POINTER(OracleDesc), i8p, i8p, i32p, C.c_int32, C.c_int32,
                                                  i8p, C.POINTER(OracleTrace)]
@@ -312,3 +330,51 @@ def ffn_module(ffn, z: np.ndarray, trace: bool = False):
         raise ValueError(f"oracle rejected its arguments (status {rc})")
     out = out.reshape(z.shape)
     return (out, {k: v.reshape(z.shape[:-1] + (v.shape[-1],)) for k, v in tr.items()}) if trace else out
+
+
+# ---- the convolution module of Eq. 3 / Eq. 5 (LayerNorm, PW1, GLU, DW + BatchNorm on
+# an INT16 grid, Swish, PW2, residual)
+
+
+def int_sigmoid(q: int, q_c: int, q_1: int) -> int:
+    """The GLU's integer sigmoid (Eq. 12's tanh^ at x/2) on one value."""
+    return int(lib().ipk_oracle_int_sigmoid(int(q), int(q_c), int(q_1)))
+
+
+def conv_module(cv, z: np.ndarray, lengths: Optional[np.ndarray] = None, trace: bool = False):
+    """z_out = z + Conv(LN(z)) on host memory ([B][T][d] int8, frames t >= lengths[b]
+    masked); with trace, also the LayerNorm output x, PW1's output u [B][T][2d], the
+    GLU output g, the int16 BatchNorm output v, the Swish output o and y = PW2 o."""
+    z = np.ascontiguousarray(z, dtype=np.int8)
+    B, T, d = z.shape
+    lens = None if lengths is None else np.ascontiguousarray(lengths, dtype=np.int32)
+    keep = []
+
+    def arr(a, dt, t):
+        a = np.ascontiguousarray(a, dtype=dt)
+        keep.append(a)
+        return _p(a, t)
+
+    D = OracleConvDesc()
+    D.d_model = d
+    D.w_pw1, D.mult_pw1, D.shift_pw1 = arr(cv.w_pw1, np.int8, i8p), arr(cv.mult_pw1, np.int32, i32p), int(cv.shift_pw1)
+    D.glu_qc, D.glu_q1, D.m_glu, D.shift_glu = int(cv.glu_qc), int(cv.glu_q1), int(cv.m_glu), int(cv.shift_glu)
+    D.w_dw, D.bias_dw = arr(cv.w_dw, np.int8, i8p), arr(cv.bias_dw, np.int32, i32p)
+    D.mult_dw, D.shift_dw = arr(cv.mult_dw, np.int32, i32p), int(cv.shift_dw)
+    D.sw_qc, D.sw_q1, D.m_sw, D.shift_sw = int(cv.sw_qc), int(cv.sw_q1), int(cv.m_sw), int(cv.shift_sw)
+    D.w_pw2, D.mult_pw2, D.shift_pw2 = arr(cv.w_pw2, np.int8, i8p), arr(cv.mult_pw2, np.int32, i32p), int(cv.shift_pw2)
+    D.ln_mult, D.ln_bias, D.ln_shift = arr(cv.ln_mult, np.int32, i32p), arr(cv.ln_bias, np.int64, i64p), int(cv.ln_shift)
+    D.m_z, D.m_y, D.shift_r = int(cv.m_z), int(cv.m_y), int(cv.shift_r)
+    out = np.empty_like(z)
+    tr = {}
+    if trace:
+        tr = {"x": np.empty_like(z), "u": np.empty((B, T, 2 * d), dtype=np.int8), "g": np.empty_like(z),
+              "v": np.empty((B, T, d), dtype=np.int16), "o": np.empty_like(z), "y": np.empty_like(z)}
+    ptr = lambda k, t=i8p: _p(tr[k], t) if trace else None  # noqa: E731
+    rc = lib().ipk_oracle_conv_module(C.byref(D), _p(z, i8p), _p(lens, i32p) if lens is not None else None, B, T,
+                                      _p(out, i8p), ptr("x"), ptr("u"), ptr("g"), ptr("v", C.POINTER(C.c_int16)),
+                                      ptr("o"), ptr("y"))
+    del keep
+    if rc != 0:
+        raise ValueError(f"oracle rejected its arguments (status {rc})")
+    return (out, tr) if trace else out

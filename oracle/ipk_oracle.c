@@ -382,3 +382,142 @@ int ipk_oracle_ffn_module(const oracle_ffn_desc* D, const int8_t* z, int64_t row
   free(x); free(h); free(o); free(y);
   return 0;
 }
+
+/* ------------------------------------------------------------------------------
+ * The convolution module of Eq. 3 and Eq. 5, Z3 = Z2 + Conv(LN(Z2)) with
+ * Conv = PW2(Swish(BN(DW(GLU(PW1(.)))))), on integer grids (this oracle's reading,
+ * kept with the design notes):
+ *  - x = LN(z) as above;
+ *  - u = clamp8(RS(x W_pw1^T, mult_pw1[c], shift_pw1)) over 2 d channels: a = u[:, :d],
+ *    b = u[:, d:] (Eq. 7);
+ *  - GLU: a * sigmoid(b) with sigmoid(x) = (1 + tanh^(x/2)) / 2 and tanh^ of Eq. 12.
+ *    On b's grid S (u = x/2 on S/2), tanh^ = sgn(q) (a* (S/2)^2) L with
+ *    L = (min(|q|, q_c) - q_c)^2 + q_1, so sigmoid = -(q_1 + sgn(q) L) on the grid
+ *    -a* (S/2)^2 / 2; g = clamp8(RS(a * sigmoid, m_glu, shift_glu)), and g = 0 on
+ *    frames t >= L_b (the padding mask before the depthwise convolution);
+ *  - DW: depthwise convolution over time, K = 9 taps centred on t (zero outside
+ *    [0, T)), BatchNorm folded into its int8 weights and an int32 bias on the
+ *    accumulator grid; the result goes to the INT16 grid of the BatchNorm output:
+ *    v = clamp16(RS(sum_k w[c][k] g[t + k - 4][c] + bias[c], mult_dw[c], shift_dw));
+ *  - Swish of Eq. 12 on the int16 grid as in the feed-forward module, then
+ *    o = clamp8(RS(q_sw, m_sw, shift_sw)), o = 0 on frames t >= L_b;
+ *  - y = clamp8(RS(o W_pw2^T, mult_pw2[c], shift_pw2)) (Eq. 7);
+ *  - z_out = clamp8(RS(m_z z + m_y y, 1, shift_r)).
+ * The Swish and GLU products are formed in 128 bits here, so no intermediate can
+ * overflow whatever the constants.
+ * ------------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t d_model;
+  const int8_t* w_pw1; /* [2d][d] */
+  const int32_t* mult_pw1;
+  int32_t shift_pw1;
+  int64_t glu_qc, glu_q1;
+  int32_t m_glu, shift_glu;
+  const int8_t* w_dw; /* [d][9] */
+  const int32_t* bias_dw;
+  const int32_t* mult_dw;
+  int32_t shift_dw;
+  int64_t sw_qc, sw_q1;
+  int32_t m_sw, shift_sw;
+  const int8_t* w_pw2; /* [d][d] */
+  const int32_t* mult_pw2;
+  int32_t shift_pw2;
+  const int32_t* ln_mult;
+  const int64_t* ln_bias;
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
+} oracle_conv_desc;
+
+/* floor((a m + 2^(n-1)) / 2^n) in 128-bit arithmetic */
+static int64_t rs_wide(__int128 a, int64_t m, int32_t n) {
+  __int128 v = a * m + ((__int128)1 << (n - 1));
+  __int128 d = (__int128)1 << n;
+  __int128 q = v / d;
+  if (v % d != 0 && v < 0) q -= 1;
+  if (q > INT64_MAX / 2) return INT64_MAX / 2;
+  if (q < INT64_MIN / 2) return INT64_MIN / 2;
+  return (int64_t)q;
+}
+
+static int64_t clamp16(int64_t v) { return v < -32767 ? -32767 : (v > 32767 ? 32767 : v); }
+
+/* The sigmoid of GLU on one value q of its grid (as described above). */
+int64_t ipk_oracle_int_sigmoid(int64_t q, int64_t q_c, int64_t q_1) {
+  const int64_t aq = q < 0 ? -q : q;
+  const int64_t t = (aq < q_c ? aq : q_c) - q_c;
+  const int64_t L = t * t + q_1;
+  const int64_t sg = q > 0 ? 1 : (q < 0 ? -1 : 0);
+  return -(q_1 + sg * L);
+}
+
+/* The module on [B][T][d_model].  Intermediates (each may be NULL): x_out [B][T][d],
+ * u_out [B][T][2d], g_out [B][T][d] (GLU), v_out int16 [B][T][d] (BatchNorm output),
+ * o_out [B][T][d] (Swish), y_out [B][T][d].  Returns 0, or -1 on an invalid argument. */
+int ipk_oracle_conv_module(const oracle_conv_desc* D, const int8_t* z, const int32_t* lengths, int32_t B, int32_t T,
+                           int8_t* z_out, int8_t* x_out, int8_t* u_out, int8_t* g_out, int16_t* v_out, int8_t* o_out,
+                           int8_t* y_out) {
+  if (!D || !z || !z_out || B < 1 || T < 1 || D->d_model < 1 || D->ln_shift < 1 || D->ln_shift > 62 ||
+      D->shift_pw1 < 1 || D->shift_pw1 > 40 || D->shift_glu < 1 || D->shift_glu > 62 || D->shift_dw < 1 ||
+      D->shift_dw > 40 || D->shift_sw < 1 || D->shift_sw > 62 || D->shift_pw2 < 1 || D->shift_pw2 > 40 ||
+      D->shift_r < 1 || D->shift_r > 40 || D->glu_qc < 0 || D->sw_qc < 0)
+    return -1;
+  for (int32_t b = 0; b < B; ++b)
+    if (lengths && (lengths[b] < 1 || lengths[b] > T)) return -1;
+  const int32_t d = D->d_model;
+  const int64_t rows = (int64_t)B * T;
+  int8_t* x = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* u = (int8_t*)malloc((size_t)(rows * 2 * d));
+  int8_t* g = (int8_t*)malloc((size_t)(rows * d));
+  int16_t* v = (int16_t*)malloc((size_t)(rows * d) * sizeof(int16_t));
+  int8_t* o = (int8_t*)malloc((size_t)(rows * d));
+  int8_t* y = (int8_t*)malloc((size_t)(rows * d));
+  if (!x || !u || !g || !v || !o || !y) {
+    free(x); free(u); free(g); free(v); free(o); free(y);
+    return -1;
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) ipk_oracle_layernorm_row(z + r * d, d, D->ln_mult, D->ln_bias, D->ln_shift, x + r * d);
+  ipk_oracle_linear(x, rows, d, D->w_pw1, 2 * d, D->mult_pw1, D->shift_pw1, u);
+  for (int32_t bb = 0; bb < B; ++bb) {
+    const int32_t L = lengths ? lengths[bb] : T;
+#pragma omp parallel for schedule(static)
+    for (int32_t t = 0; t < T; ++t) {
+      const int64_t r = (int64_t)bb * T + t;
+      for (int32_t c = 0; c < d; ++c) {
+        int64_t gv = 0;
+        if (t < L) {
+          const int64_t sig = ipk_oracle_int_sigmoid(u[r * 2 * d + d + c], D->glu_qc, D->glu_q1);
+          gv = ipk_oracle_clamp8(rs_wide((__int128)u[r * 2 * d + c] * sig, D->m_glu, D->shift_glu));
+        }
+        g[r * d + c] = (int8_t)gv;
+      }
+    }
+#pragma omp parallel for schedule(static)
+    for (int32_t t = 0; t < T; ++t) {
+      const int64_t r = (int64_t)bb * T + t;
+      for (int32_t c = 0; c < d; ++c) {
+        int64_t acc = D->bias_dw[c];
+        for (int32_t k = 0; k < 9; ++k) {
+          const int32_t ts = t + k - 4;
+          if (ts >= 0 && ts < T) acc += (int64_t)D->w_dw[c * 9 + k] * g[((int64_t)bb * T + ts) * d + c];
+        }
+        const int64_t vv = clamp16(ipk_oracle_rs(acc, D->mult_dw[c], D->shift_dw));
+        v[r * d + c] = (int16_t)vv;
+        int64_t ov = 0;
+        if (t < L) ov = ipk_oracle_clamp8(rs_wide(ipk_oracle_int_swish(vv, D->sw_qc, D->sw_q1), D->m_sw, D->shift_sw));
+        o[r * d + c] = (int8_t)ov;
+      }
+    }
+  }
+  ipk_oracle_linear(o, rows, d, D->w_pw2, d, D->mult_pw2, D->shift_pw2, y);
+  for (int64_t i = 0; i < rows * d; ++i) z_out[i] = (int8_t)ipk_oracle_residual(z[i], y[i], D->m_z, D->m_y, D->shift_r);
+  if (x_out) memcpy(x_out, x, (size_t)(rows * d));
+  if (u_out) memcpy(u_out, u, (size_t)(rows * 2 * d));
+  if (g_out) memcpy(g_out, g, (size_t)(rows * d));
+  if (v_out) memcpy(v_out, v, (size_t)(rows * d) * sizeof(int16_t));
+  if (o_out) memcpy(o_out, o, (size_t)(rows * d));
+  if (y_out) memcpy(y_out, y, (size_t)(rows * d));
+  free(x); free(u); free(g); free(v); free(o); free(y);
+  return 0;
+}

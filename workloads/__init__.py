@@ -10,11 +10,13 @@ score, softmax or requantization of data).
 from .generate import (  # noqa: F401
     CONFIGS,
     Block,
+    Conv,
     Ffn,
     Residual,
     Workload,
     config_by_name,
     make_block,
+    make_conv,
     make_ffn,
     make_residual,
     make_workload,

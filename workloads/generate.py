@@ -461,3 +461,148 @@ def make_ffn(d_model: int, regime: str, seed: int, S_z: float, d_ff: Optional[in
                shift_r=SHIFT_N,
                scales={"S_z": S_z, "S_x": S_x, "S_W1": S_W1, "S_h": S_h, "S_sw": float(S_sw), "S_o": S_o,
                        "S_W2": S_W2, "S_y": S_y, "S_z2": S_z2, "gamma": gamma, "beta": beta})
+
+
+# ---------------------------------------------------------------------------------
+# The convolution module of Eq. 3 / Eq. 5, Z3 = Z2 + Conv(LN(Z2)) with
+# Conv = PW2(Swish(BN(DW(GLU(PW1(.)))))): PW1 int8 [2d][d], a depthwise kernel of 9
+# taps per channel with BatchNorm folded into it (gamma / sqrt(var + eps) into the int8
+# weights' per-channel scale, beta - gamma mean / sqrt(var + eps) into an int32 bias on
+# the accumulator grid), the BatchNorm output on an INT16 grid (the paper's remedy for
+# its range), PW2 int8 [d][d].  Literal regime: int8 grids and per-channel weight scales
+# ~ U[2^-8, 2^-4], the int16 grid ~ U[2^-16, 2^-12] (the same clip range over 32767
+# levels); calibrated: unit-variance tensors, Xavier-scaled weights, int8 grids covering
+# +-4 standard deviations and the int16 grid +-16.
+CONV_K = 9
+S16_LO, S16_HI = 2.0 ** -16, 2.0 ** -12
+
+
+@dataclasses.dataclass
+class Conv:
+    """Integer parameters of the convolution module and the real values they came from."""
+
+    d_model: int
+    w_pw1: np.ndarray  # int8 [2d][d]
+    mult_pw1: np.ndarray
+    shift_pw1: int
+    glu_qc: int
+    glu_q1: int
+    m_glu: int
+    shift_glu: int
+    w_dw: np.ndarray  # int8 [d][9]
+    bias_dw: np.ndarray  # int32 [d]
+    mult_dw: np.ndarray
+    shift_dw: int
+    sw_qc: int
+    sw_q1: int
+    m_sw: int
+    shift_sw: int
+    w_pw2: np.ndarray  # int8 [d][d]
+    mult_pw2: np.ndarray
+    shift_pw2: int
+    ln_mult: np.ndarray
+    ln_bias: np.ndarray
+    ln_shift: int
+    m_z: int
+    m_y: int
+    shift_r: int
+    scales: Dict[str, object]
+
+
+def fixed_point_bounded(ratio, max_abs_input: int, n_max: int = 62):
+    """(m, n), m = round(2^n ratio), for the largest n <= n_max with m < 2^23 and
+    m max_abs_input + 2^(n-1) < 2^62 (so the requantization fits 64-bit integers)."""
+    r = _dec(ratio)
+    for n in range(n_max, 0, -1):
+        m = _round_dec((Decimal(2) ** n) * r)
+        if m < (1 << 23) and m * max_abs_input + (1 << (n - 1)) < (1 << 62):
+            return m, n
+    raise ValueError(f"no fixed-point multiplier for ratio {ratio}")
+
+
+# The GLU's sigmoid (1 + tanh^(x/2)) / 2 with Eq. 12's polynomial family, (a, c) fitted by
+# Eq. 13's minimax criterion to the function it stands for, the sigmoid itself (the
+# Swish pair (a*, c*) leaves tanh^(0+) = 1 + a* c*^2 = 0.25, a sigmoid error of 0.12
+# at x = 0+, harmless inside x sigma(x) but not in a gate).  Solved numerically (dense
+# grid, Nelder-Mead): max |tanh^ - tanh| = 0.0348, so the sigmoid is within 0.0174.
+SIGMOID_A, SIGMOID_C = -0.2182, 2.1032
+
+
+def sigmoid_constants(S_b: float, a: float = SIGMOID_A, c: float = SIGMOID_C):
+    """Integer constants of the GLU sigmoid (1 + tanh^(x/2)) / 2 on grid S_b: q_c, q_1 as
+    for Eq. 12 with (a, c) = (SIGMOID_A, SIGMOID_C), output grid -a (S_b/2)^2 / 2."""
+    q_c, q_1, _ = swish_constants(S_b, a, c)
+    S_u = _dec(S_b) / 2
+    return q_c, q_1, -Decimal(str(a)) * S_u * S_u / 2
+
+
+def _max_abs_poly(q_max: int, q_c: int, q_1: int, sigmoid: bool) -> int:
+    """max over |q| <= q_max of |Swish(q)| (or |sigmoid(q)|) on the integer grids."""
+    best = 0
+    for q in range(-q_max, q_max + 1) if q_max <= 255 else np.unique(np.r_[np.arange(-q_max, -q_max + 300),
+                                                                            np.arange(-q_c - 2, q_c + 3),
+                                                                            np.arange(q_max - 300, q_max + 1)]):
+        q = int(q)
+        aq = abs(q)
+        t = min(aq, q_c) - q_c
+        L = t * t + q_1
+        v = -(q_1 + (1 if q > 0 else (-1 if q < 0 else 0)) * L) if sigmoid else -(aq * L + q * q_1)
+        best = max(best, abs(v))
+    return best
+
+
+def make_conv(d_model: int, regime: str, seed: int, S_z: float) -> Conv:
+    """Draws one convolution module for inputs on grid S_z (a generator of its own)."""
+    rng = np.random.default_rng(seed)
+    d = d_model
+    w_pw1 = _uniform_i8(rng, (2 * d, d))
+    w_dw = _uniform_i8(rng, (d, CONV_K))
+    w_pw2 = _uniform_i8(rng, (d, d))
+    gamma = rng.uniform(0.5, 1.5, size=d)
+    beta = rng.uniform(-0.25, 0.25, size=d)
+    bias_real = rng.uniform(-0.25, 0.25, size=d)  # folded BatchNorm shift
+    if regime == "literal":
+        u = lambda size=None: rng.uniform(SCALE_LO, SCALE_HI, size=size)  # noqa: E731
+        S_W1, S_dw, S_W2 = u(2 * d), u(d), u(d)
+        S_x, S_u8, S_g, S_o, S_y, S_z2 = (float(u()) for _ in range(6))
+        S_v = float(rng.uniform(S16_LO, S16_HI))
+    elif regime == "calibrated":
+        kcov = 4.0
+        S_x = kcov * 1.5 / 127.0
+        S_W1 = rng.uniform(0.75, 1.0, size=2 * d) / (SIGMA_W * math.sqrt(d))
+        S_u8 = kcov / 127.0  # PW1 output: about unit variance
+        S_g = kcov * 0.5 / 127.0  # a * sigmoid(b)
+        S_dw = rng.uniform(0.75, 1.0, size=d) / (SIGMA_W * math.sqrt(CONV_K) * 0.5)
+        S_v = 16.0 / 32767.0  # the int16 BatchNorm output covers +-16
+        S_o = kcov * 0.6 / 127.0
+        S_W2 = rng.uniform(0.75, 1.0, size=d) / (SIGMA_W * math.sqrt(d))
+        S_y = kcov * 0.6 / 127.0
+        sz = S_z * 127.0 / 4.0
+        S_z2 = 4.0 * math.sqrt(sz * sz + 0.6 ** 2) / 127.0
+    else:
+        raise ValueError(regime)
+    n = SHIFT_N
+    mult_pw1 = np.array([fixed_point(_dec(S_x) * _dec(s) / _dec(S_u8), n) for s in S_W1], dtype=np.int32)
+    glu_qc, glu_q1, S_sig = sigmoid_constants(S_u8)
+    m_glu, shift_glu = fixed_point_bounded(_dec(S_u8) * S_sig / _dec(S_g),
+                                           127 * _max_abs_poly(127, glu_qc, glu_q1, True))
+    bias_dw = np.array([int(round(b / (S_g * s))) for b, s in zip(bias_real, S_dw)], dtype=np.int64)
+    bias_dw = np.clip(bias_dw, -(1 << 30), (1 << 30)).astype(np.int32)
+    # per-channel multipliers of the int16 BatchNorm output; n chosen so every m < 2^23
+    ratios = [_dec(S_g) * _dec(s) / _dec(S_v) for s in S_dw]
+    shift_dw = n
+    while max(_round_dec((Decimal(2) ** shift_dw) * r) for r in ratios) >= (1 << 23):
+        shift_dw -= 1
+    mult_dw = np.array([_round_dec((Decimal(2) ** shift_dw) * r) for r in ratios], dtype=np.int32)
+    sw_qc, sw_q1, S_sw = swish_constants(S_v)
+    m_sw, shift_sw = fixed_point_bounded(S_sw / _dec(S_o), _max_abs_poly(32767, sw_qc, sw_q1, False))
+    mult_pw2 = np.array([fixed_point(_dec(S_o) * _dec(s) / _dec(S_y), n) for s in S_W2], dtype=np.int32)
+    g, c = _ln_consts(d, gamma, beta, S_x)
+    return Conv(d_model=d, w_pw1=w_pw1, mult_pw1=mult_pw1, shift_pw1=n, glu_qc=glu_qc, glu_q1=glu_q1, m_glu=m_glu,
+                shift_glu=shift_glu, w_dw=w_dw, bias_dw=bias_dw, mult_dw=mult_dw, shift_dw=shift_dw, sw_qc=sw_qc,
+                sw_q1=sw_q1, m_sw=m_sw, shift_sw=shift_sw, w_pw2=w_pw2, mult_pw2=mult_pw2, shift_pw2=n, ln_mult=g,
+                ln_bias=c, ln_shift=LN_SHIFT, m_z=fixed_point(_dec(S_z) / _dec(S_z2)),
+                m_y=fixed_point(_dec(S_y) / _dec(S_z2)), shift_r=SHIFT_N,
+                scales={"S_z": S_z, "S_x": S_x, "S_W1": S_W1, "S_u": S_u8, "S_sig": float(S_sig), "S_g": S_g,
+                        "S_dw": S_dw, "bias": bias_real, "S_v": S_v, "S_sw": float(S_sw), "S_o": S_o, "S_W2": S_W2,
+                        "S_y": S_y, "S_z2": S_z2, "gamma": gamma, "beta": beta})
