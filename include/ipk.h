@@ -243,7 +243,7 @@ int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* 
  * Multipliers (HOST, int32): mult1 [d_ff], mult2 [d_model], each in [0, 2^23).
  * LayerNorm constants (HOST): as ipk_mhsa_residual_desc.
  * Ranges: shifts in [1, 40] (ln_shift in [1, 62]); 0 <= m_sw, m_z, m_y < 2^23;
- * 0 <= sw_qc < 2^20; and |q m_sw| + 2^(shift_sw - 1) < 2^62 for every int8 h
+ * 0 <= sw_qc < 2^20; |sw_q1| < 2^45; and |q m_sw| + 2^(shift_sw - 1) < 2^62 for every int8 h
  * (IPK_ERR_UNSUPPORTED otherwise).
  */
 typedef struct ipk_ffn_desc {
@@ -251,7 +251,8 @@ typedef struct ipk_ffn_desc {
   const int8_t *w1, *w2;
   const int32_t *mult1, *mult2;
   int32_t shift1, shift2;
-  int32_t sw_qc, sw_q1;
+  int32_t sw_qc;
+  int64_t sw_q1;
   int32_t m_sw, shift_sw;
   const int32_t* ln_mult;
   const int64_t* ln_bias;
@@ -284,6 +285,85 @@ int ipk_ffn_intermediate(ipk_ffn_t* h, int32_t which, void* dst, int64_t bytes, 
 
 /* Frees the handle after synchronizing the device; NULL is a no-op. */
 int ipk_ffn_destroy(ipk_ffn_t* h);
+
+/*
+ * The convolution module of the Conformer block (Eq. 3 and Eq. 5) on integer grids,
+ * z' = z + Conv(LN(z)) with Conv = PW2(Swish(BN(DW(GLU(PW1(.)))))):
+ *   x  = LN(z)                                      the LayerNorm above
+ *   u  = clamp8(RS(x W_pw1^T, mult_pw1[c], shift_pw1))   2 d channels: a = u[:, :d], b = u[:, d:]
+ *   g  = clamp8(RS(a s, m_glu, shift_glu)),  s = -(glu_q1 + sgn(b) L_g(b)),
+ *        L_g(q) = (min(|q|, glu_qc) - glu_qc)^2 + glu_q1
+ *                                                   GLU with the sigmoid (1 + tanh^(x/2)) / 2 of
+ *                                                   Eq. 12's polynomial; g = 0 on frames t >= L_b
+ *   v  = clamp16(RS(bias_dw[c] + sum_k w_dw[c][k] g[t + k - 4], mult_dw[c], shift_dw))
+ *                                                   depthwise convolution over time (9 taps,
+ *                                                   zero outside [0, T)) with BatchNorm folded
+ *                                                   into w_dw and bias_dw; v on the INT16 grid
+ *                                                   of the BatchNorm output ([-32767, 32767])
+ *   o  = clamp8(RS(-(|v| L_s(v) + v sw_q1), m_sw, shift_sw)) for t < L_b, else 0,
+ *        L_s(q) = (min(|q|, sw_qc) - sw_qc)^2 + sw_q1    Eq. 12's Swish on v's grid
+ *   y  = clamp8(RS(o W_pw2^T, mult_pw2[c], shift_pw2))
+ *   z' = clamp8(RS(m_z z + m_y y, 1, shift_r))
+ * Shapes: d_model a multiple of 64 in [64, 16384]; max_batch in [1, IPK_MAX_BATCH],
+ * max_T in [1, IPK_MAX_T] size the workspace.
+ * Weights (DEVICE, int8, row-major): w_pw1 [2 d][d], w_dw [d][9], w_pw2 [d][d].
+ * Per-channel constants (HOST, int32): mult_pw1 [2 d], bias_dw [d], mult_dw [d], mult_pw2 [d].
+ * Ranges: multipliers in [0, 2^23); |bias_dw| < 2^30; shift_pw1, shift_dw, shift_pw2,
+ * shift_r in [1, 40]; shift_glu, shift_sw in [1, 62]; 0 <= glu_qc, sw_qc < 2^20;
+ * |glu_q1|, |sw_q1| < 2^45 (an int16 grid puts q_1 far beyond 32 bits); and for
+ * every int8 a, b: |a s| m_glu + 2^(shift_glu - 1) < 2^62, for every int16 v:
+ * |Swish(v)| m_sw + 2^(shift_sw - 1) < 2^62 (IPK_ERR_UNSUPPORTED otherwise).
+ * LayerNorm and residual constants as ipk_mhsa_residual_desc.
+ */
+typedef struct ipk_conv_desc {
+  int32_t d_model, max_batch, max_T;
+  const int8_t* w_pw1;
+  const int32_t* mult_pw1;
+  int32_t shift_pw1;
+  int32_t glu_qc;
+  int64_t glu_q1;
+  int32_t m_glu, shift_glu;
+  const int8_t* w_dw;
+  const int32_t *bias_dw, *mult_dw;
+  int32_t shift_dw;
+  int32_t sw_qc;
+  int64_t sw_q1;
+  int32_t m_sw, shift_sw;
+  const int8_t* w_pw2;
+  const int32_t* mult_pw2;
+  int32_t shift_pw2;
+  const int32_t* ln_mult;
+  const int64_t* ln_bias;
+  int32_t ln_shift;
+  int32_t m_z, m_y, shift_r;
+} ipk_conv_desc;
+
+typedef struct ipk_conv ipk_conv_t;
+
+/* Validates `desc`, allocates the handle and its workspace and keeps device copies of
+ * the weights and constants.  Synchronizes its own copies.  Returns IPK_OK and sets
+ * *out, or a negative status with *out = NULL and nothing leaked. */
+int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out);
+
+/* Runs the module on `stream`: z DEVICE int8 [B][T][d_model] -> z_out (same layout),
+ * both 16-byte aligned; z_out may be z itself but may not overlap it otherwise.
+ * lengths: HOST int32 [B] valid frames in [1, T] (NULL: all T), captured at the call.
+ * Asynchronous; calls on one handle must be ordered on one stream.
+ * Errors: IPK_ERR_INVALID_ARG (null handle or pointer, misalignment, partial overlap,
+ * B or T outside the handle's limits, a length outside [1, T]), IPK_ERR_HIP. */
+int ipk_conv_run(ipk_conv_t* h, const int8_t* z, const int32_t* lengths, int32_t B, int32_t T, int8_t* z_out,
+                 void* stream);
+
+/* Copies an intermediate of the last run into `dst` (DEVICE, `bytes` bytes) on
+ * `stream`: IPK_CONV_X the LayerNorm output int8 [B][T][d], IPK_CONV_U PW1's output int8
+ * [B][T][2 d], IPK_CONV_V the BatchNorm output int16 [B][T][d], IPK_CONV_O the Swish
+ * output int8 [B][T][d].  Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`,
+ * bytes too small, null), IPK_ERR_HIP. */
+enum { IPK_CONV_X = 0, IPK_CONV_U = 1, IPK_CONV_V = 2, IPK_CONV_O = 3 };
+int ipk_conv_intermediate(ipk_conv_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
+
+/* Frees the handle after synchronizing the device; NULL is a no-op. */
+int ipk_conv_destroy(ipk_conv_t* h);
 
 /* Human-readable name of a status code (static storage). */
 const char* ipk_status_string(int status);

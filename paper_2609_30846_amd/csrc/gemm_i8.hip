@@ -604,21 +604,40 @@ hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_
                                                    : go(std::integral_constant<int, 256>{});
 }
 
-hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int8_t* w2, const double* scale2,
-                           const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st) {
+hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const double* scale,
+                               const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st) {
   GemmArgs a{};
   a.y = z_out;
   a.z1 = z;
   a.m_z = m_z;
   a.m_y = m_y;
   a.shift_r = shift_r;
-  // 128 x 128 tiles of eight waves (32 channels x 64 tokens each): K = d_ff is long, so
-  // the larger tile's operand reuse pays (measured against 64 x 64, 128 x 64, 128 x 96
-  // and 64 x 192 tiles at 2500 and 4000 rows)
+  // 128 x 128 tiles of eight waves (32 channels x 64 tokens each): for the feed-forward
+  // module's W2 (K = d_ff) measured against 64 x 64, 128 x 64, 128 x 96, 64 x 192,
+  // 256 x 128 and 128 x 256 tiles at 2500 and 4000 rows
   constexpr int TN = 128, TM = 128, NWAVE = 8, WN = 4;
-  const int tiles = add_problem(a, 0, o, w2, scale2, 1, rows, d, d_ff, OUT_ROWMAJOR, 0, TN, TM);
+  const int tiles = add_problem(a, 0, x, w, scale, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
   return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, LaunchEv{});
+}
+
+hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const double* scale, int8_t* y,
+                         hipStream_t st) {
+  constexpr int TN = 256, NWAVE = 8, WN = 4;
+  auto tiles_of = [&](int tm) { return (long)((rows + tm - 1) / tm) * ((N + TN - 1) / TN); };
+  int TMr = pick_tile_rows(256, 192, tiles_of);
+  TMr = pick_tile_rows(TMr, 128, tiles_of);
+  auto go = [&](auto tm_tag) {
+    constexpr int TM = decltype(tm_tag)::value;
+    GemmArgs a{};
+    a.y = y;
+    const int tiles = add_problem(a, 0, x, w, scale, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
+    a.nprob = 1;
+    return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, LaunchEv{});
+  };
+  if (TMr == 128) return go(std::integral_constant<int, 128>{});
+  if (TMr == 192) return go(std::integral_constant<int, 192>{});
+  return go(std::integral_constant<int, 256>{});
 }
 
 // one thread per 16-byte piece of the destination

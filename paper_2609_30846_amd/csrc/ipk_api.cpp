@@ -3,7 +3,9 @@
 //   projections (Q|K|V and the position table) -> rank-1 bias terms and V prefix
 //   sums -> attention core -> output projection; for the MHSA module of Eq. 2 an
 //   integer LayerNorm first and the residual add in the output projection's epilogue;
-//   and the feed-forward module of Eq. 1 (LayerNorm, W1 + integer Swish, W2 + residual).
+//   the feed-forward module of Eq. 1 (LayerNorm, W1 + integer Swish, W2 + residual); and
+//   the convolution module of Eq. 5 (LayerNorm, PW1, GLU + depthwise + INT16 BatchNorm
+//   + Swish, PW2 + residual).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdarg.h>
@@ -518,6 +520,8 @@ static int validate_ffn(const ipk_ffn_desc* D) {
       return fail(IPK_ERR_INVALID_ARG, "ln_bias[%d] outside (-2^56, 2^56)", k);
   }
   if (D->sw_qc < 0 || D->sw_qc >= (1 << 20)) return fail(IPK_ERR_INVALID_ARG, "sw_qc=%d outside [0, 2^20)", D->sw_qc);
+  if (D->sw_q1 <= -((int64_t)1 << 45) || D->sw_q1 >= ((int64_t)1 << 45))
+    return fail(IPK_ERR_INVALID_ARG, "sw_q1 outside (-2^45, 2^45)");
   // the Swish table kernel evaluates q m_sw + 2^(n-1) in 64 bits: bound it for every h
   for (int hv = -127; hv <= 127; ++hv) {
     const __int128 ah = hv < 0 ? -hv : hv;
@@ -620,7 +624,8 @@ extern "C" int ipk_ffn_run(ipk_ffn_t* h, const int8_t* z, int32_t rows, int8_t* 
   hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
   if (e == hipSuccess) e = launch_ffn_up(h->x, rows, h->d, h->f, h->w1, h->scale1, h->swtab, h->o, st);
   if (e == hipSuccess)
-    e = launch_ffn_down(h->o, rows, h->d, h->f, h->w2, h->scale2, z, h->res.m_z, h->res.m_y, h->res.shift_r, z_out, st);
+    e = launch_linear_resid(h->o, rows, h->d, h->f, h->w2, h->scale2, z, h->res.m_z, h->res.m_y, h->res.shift_r, z_out,
+                            st);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last_rows = rows;
   return IPK_OK;
@@ -645,6 +650,258 @@ extern "C" int ipk_ffn_destroy(ipk_ffn_t* h) {
   (void)hipSetDevice(h->device);
   hipError_t e = hipDeviceSynchronize();
   free_ffn(h);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The convolution module of Eq. 3 and Eq. 5.
+
+struct ipk_conv {
+  int device;
+  int d, max_B, max_T;
+  int8_t *w_pw1, *w_pw2;        // fragment order (wfrag_index)
+  double *scale_pw1, *scale_pw2;
+  ConvMiddle mid;               // depthwise weights and constants (device copies)
+  int8_t *x, *u, *o;            // LayerNorm output, PW1 output [.][2 d], Swish output
+  int16_t* v;                   // int16 BatchNorm output
+  Residual res;
+  int last_B, last_T;
+  std::vector<void*> allocs;
+};
+
+static void free_conv(ipk_conv* h) {
+  if (!h) return;
+  for (void* p : h->allocs) (void)hipFree(p);
+  delete h;
+}
+
+template <typename T>
+static hipError_t conv_alloc(ipk_conv* h, T** p, size_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
+  if (e != hipSuccess) return e;
+  h->allocs.push_back(q);
+  *p = (T*)q;
+  return hipSuccess;
+}
+
+static __int128 poly_l128(__int128 aq, __int128 q_c, __int128 q_1) {
+  const __int128 t = (aq < q_c ? aq : q_c) - q_c;
+  return t * t + q_1;
+}
+
+static int validate_conv(const ipk_conv_desc* D) {
+  if (!D) return fail(IPK_ERR_INVALID_ARG, "desc is NULL");
+  if (D->d_model < 64 || D->d_model % 64 || D->d_model > 16384)
+    return fail(IPK_ERR_INVALID_ARG, "d_model=%d must be a multiple of 64 in [64, 16384]", D->d_model);
+  if (D->max_batch < 1 || D->max_batch > IPK_MAX_BATCH)
+    return fail(IPK_ERR_INVALID_ARG, "max_batch=%d outside [1, %d]", D->max_batch, IPK_MAX_BATCH);
+  if (D->max_T < 1 || D->max_T > IPK_MAX_T) return fail(IPK_ERR_INVALID_ARG, "max_T=%d outside [1, %d]", D->max_T, IPK_MAX_T);
+  if ((int64_t)D->max_batch * D->max_T * 2 * D->d_model >= ((int64_t)1 << 31))
+    return fail(IPK_ERR_UNSUPPORTED, "max_batch * max_T * 2 d_model reaches 2^31");
+  if (!D->w_pw1 || !D->w_dw || !D->w_pw2 || !D->mult_pw1 || !D->bias_dw || !D->mult_dw || !D->mult_pw2 ||
+      !D->ln_mult || !D->ln_bias)
+    return fail(IPK_ERR_INVALID_ARG, "a weight, multiplier, bias or LayerNorm pointer is NULL");
+  const int d = D->d_model;
+  for (int c = 0; c < 2 * d; ++c)
+    if (!mult_ok(D->mult_pw1[c])) return fail(IPK_ERR_INVALID_ARG, "mult_pw1[%d]=%d outside [0, 2^23)", c, D->mult_pw1[c]);
+  for (int c = 0; c < d; ++c) {
+    if (!mult_ok(D->mult_dw[c])) return fail(IPK_ERR_INVALID_ARG, "mult_dw[%d]=%d outside [0, 2^23)", c, D->mult_dw[c]);
+    if (!mult_ok(D->mult_pw2[c])) return fail(IPK_ERR_INVALID_ARG, "mult_pw2[%d]=%d outside [0, 2^23)", c, D->mult_pw2[c]);
+    if (D->bias_dw[c] <= -(1 << 30) || D->bias_dw[c] >= (1 << 30))
+      return fail(IPK_ERR_INVALID_ARG, "bias_dw[%d]=%d outside (-2^30, 2^30)", c, D->bias_dw[c]);
+    if (D->ln_mult[c] <= -(1 << 24) || D->ln_mult[c] >= (1 << 24))
+      return fail(IPK_ERR_INVALID_ARG, "ln_mult[%d]=%d outside (-2^24, 2^24)", c, D->ln_mult[c]);
+    if (D->ln_bias[c] <= -((int64_t)1 << 56) || D->ln_bias[c] >= ((int64_t)1 << 56))
+      return fail(IPK_ERR_INVALID_ARG, "ln_bias[%d] outside (-2^56, 2^56)", c);
+  }
+  if (!shift_ok(D->shift_pw1) || !shift_ok(D->shift_dw) || !shift_ok(D->shift_pw2) || !shift_ok(D->shift_r))
+    return fail(IPK_ERR_INVALID_ARG, "shift_pw1, shift_dw, shift_pw2 and shift_r must be in [1, 40]");
+  if (D->shift_glu < 1 || D->shift_glu > 62 || D->shift_sw < 1 || D->shift_sw > 62)
+    return fail(IPK_ERR_INVALID_ARG, "shift_glu and shift_sw must be in [1, 62]");
+  if (D->ln_shift < 1 || D->ln_shift > 62) return fail(IPK_ERR_INVALID_ARG, "ln_shift=%d outside [1, 62]", D->ln_shift);
+  if (!mult_ok(D->m_glu) || !mult_ok(D->m_sw) || !mult_ok(D->m_z) || !mult_ok(D->m_y))
+    return fail(IPK_ERR_INVALID_ARG, "m_glu, m_sw, m_z and m_y must be in [0, 2^23)");
+  if (D->glu_qc < 0 || D->glu_qc >= (1 << 20) || D->sw_qc < 0 || D->sw_qc >= (1 << 20))
+    return fail(IPK_ERR_INVALID_ARG, "glu_qc and sw_qc must be in [0, 2^20)");
+  const int64_t q1lim = (int64_t)1 << 45;
+  if (D->glu_q1 <= -q1lim || D->glu_q1 >= q1lim || D->sw_q1 <= -q1lim || D->sw_q1 >= q1lim)
+    return fail(IPK_ERR_INVALID_ARG, "glu_q1 and sw_q1 must be in (-2^45, 2^45)");
+  // the kernel's 64-bit products: GLU over every int8 (a, b), Swish over every int16 v
+  const __int128 lim = (__int128)1 << 62;
+  __int128 smax = 0;
+  for (int b = -127; b <= 127; ++b) {
+    const __int128 ab = b < 0 ? -b : b, sg = b > 0 ? 1 : (b < 0 ? -1 : 0);
+    __int128 sgm = -((__int128)D->glu_q1 + sg * poly_l128(ab, D->glu_qc, D->glu_q1));
+    if (sgm < 0) sgm = -sgm;
+    if (sgm > smax) smax = sgm;
+  }
+  if (smax * 128 * D->m_glu + ((__int128)1 << (D->shift_glu - 1)) >= lim)
+    return fail(IPK_ERR_UNSUPPORTED, "GLU product times m_glu reaches 2^62");
+  for (int vv = -32767; vv <= 32767; ++vv) {
+    const __int128 av = vv < 0 ? -vv : vv;
+    __int128 q = -(av * poly_l128(av, D->sw_qc, D->sw_q1) + (__int128)vv * D->sw_q1);
+    if (q < 0) q = -q;
+    if (q * D->m_sw + ((__int128)1 << (D->shift_sw - 1)) >= lim)
+      return fail(IPK_ERR_UNSUPPORTED, "Swish of the int16 value %d times m_sw reaches 2^62", vv);
+  }
+  return IPK_OK;
+}
+
+extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
+  g_last_error[0] = 0;
+  if (!out) return fail(IPK_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int st = validate_conv(desc);
+  if (st != IPK_OK) return st;
+  ipk_conv* h = new (std::nothrow) ipk_conv();
+  if (!h) return fail(IPK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    free_conv(h);
+    return fail(IPK_ERR_HIP, "hipGetDevice failed");
+  }
+  const size_t d = desc->d_model, R = (size_t)desc->max_batch * desc->max_T;
+  h->d = (int)d;
+  h->max_B = desc->max_batch;
+  h->max_T = desc->max_T;
+  h->last_B = h->last_T = 0;
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+  };
+  int8_t *wdw = nullptr, *stage = nullptr;
+  int32_t *bias = nullptr, *mdw = nullptr, *g = nullptr;
+  int64_t* c = nullptr;
+  chk(conv_alloc(h, &h->w_pw1, 2 * d * d));
+  chk(conv_alloc(h, &h->w_pw2, d * d));
+  chk(conv_alloc(h, &h->scale_pw1, 2 * d));
+  chk(conv_alloc(h, &h->scale_pw2, d));
+  chk(conv_alloc(h, &wdw, d * 9));
+  chk(conv_alloc(h, &bias, d));
+  chk(conv_alloc(h, &mdw, d));
+  chk(conv_alloc(h, &g, d));
+  chk(conv_alloc(h, &c, d));
+  chk(conv_alloc(h, &h->x, R * d));
+  chk(conv_alloc(h, &h->u, R * 2 * d));
+  chk(conv_alloc(h, &h->o, R * d));
+  chk(conv_alloc(h, &h->v, R * d));
+  chk(conv_alloc(h, &stage, 2 * d * d));
+  if (e != hipSuccess) {
+    free_conv(h);
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device allocation failed: %s",
+                hipGetErrorString(e));
+  }
+  chk(hipMemcpy(stage, desc->w_pw1, 2 * d * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w_pw1, 2 * (int)d, (int)d, nullptr));
+  chk(hipMemcpy(stage, desc->w_pw2, d * d, hipMemcpyDefault));
+  chk(pack_weight_fragments(stage, h->w_pw2, (int)d, (int)d, nullptr));
+  chk(hipMemcpy(wdw, desc->w_dw, d * 9, hipMemcpyDefault));
+  std::vector<double> s1(2 * d), s2(d);
+  for (size_t k = 0; k < 2 * d; ++k) s1[k] = ldexp((double)desc->mult_pw1[k], -desc->shift_pw1);
+  for (size_t k = 0; k < d; ++k) s2[k] = ldexp((double)desc->mult_pw2[k], -desc->shift_pw2);
+  chk(hipMemcpy(h->scale_pw1, s1.data(), 2 * d * sizeof(double), hipMemcpyHostToDevice));
+  chk(hipMemcpy(h->scale_pw2, s2.data(), d * sizeof(double), hipMemcpyHostToDevice));
+  chk(hipMemcpy(bias, desc->bias_dw, d * sizeof(int32_t), hipMemcpyHostToDevice));
+  chk(hipMemcpy(mdw, desc->mult_dw, d * sizeof(int32_t), hipMemcpyHostToDevice));
+  std::vector<int64_t> cb(d);
+  for (size_t k = 0; k < d; ++k) cb[k] = desc->ln_bias[k] + ((int64_t)1 << (desc->ln_shift - 1));
+  chk(hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
+  chk(hipMemcpy(c, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice));
+  chk(hipDeviceSynchronize());
+  if (e != hipSuccess) {
+    free_conv(h);
+    (void)hipGetLastError();
+    return fail(IPK_ERR_HIP, "copying the weights failed: %s", hipGetErrorString(e));
+  }
+  h->allocs.erase(std::find(h->allocs.begin(), h->allocs.end(), (void*)stage));
+  (void)hipFree(stage);
+  h->mid.w_dw = wdw;
+  h->mid.bias_dw = bias;
+  h->mid.mult_dw = mdw;
+  h->mid.shift_dw = desc->shift_dw;
+  h->mid.glu_qc = desc->glu_qc;
+  h->mid.glu_q1 = desc->glu_q1;
+  h->mid.m_glu = desc->m_glu;
+  h->mid.shift_glu = desc->shift_glu;
+  h->mid.sw_qc = desc->sw_qc;
+  h->mid.sw_q1 = desc->sw_q1;
+  h->mid.m_sw = desc->m_sw;
+  h->mid.shift_sw = desc->shift_sw;
+  h->res.ln_mult = g;
+  h->res.ln_bias = c;
+  h->res.ln_shift = desc->ln_shift;
+  h->res.m_z = desc->m_z;
+  h->res.m_y = desc->m_y;
+  h->res.shift_r = desc->shift_r;
+  *out = h;
+  return IPK_OK;
+}
+
+extern "C" int ipk_conv_run(ipk_conv_t* h, const int8_t* z, const int32_t* lengths, int32_t B, int32_t T, int8_t* z_out,
+                            void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!z || !z_out) return fail(IPK_ERR_INVALID_ARG, "z and z_out must be non-NULL");
+  if (((uintptr_t)z | (uintptr_t)z_out) & 15) return fail(IPK_ERR_INVALID_ARG, "z and z_out must be 16-byte aligned");
+  if (B < 1 || B > h->max_B) return fail(IPK_ERR_INVALID_ARG, "B=%d outside [1, max_batch=%d]", B, h->max_B);
+  if (T < 1 || T > h->max_T) return fail(IPK_ERR_INVALID_ARG, "T=%d outside [1, max_T=%d]", T, h->max_T);
+  Lengths lens;
+  for (int b = 0; b < B; ++b) {
+    const int L = lengths ? lengths[b] : T;
+    if (L < 1 || L > T) return fail(IPK_ERR_INVALID_ARG, "lengths[%d]=%d outside [1, T=%d]", b, L, T);
+    lens.len[b] = L;
+  }
+  for (int b = B; b < IPK_MAX_BATCH; ++b) lens.len[b] = 0;
+  const size_t n = (size_t)B * T * h->d;
+  if (z != z_out) {
+    const uintptr_t a = (uintptr_t)z, b = (uintptr_t)z_out;
+    if (a < b + n && b < a + n) return fail(IPK_ERR_INVALID_ARG, "z and z_out overlap without being equal");
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  hipStream_t st = (hipStream_t)stream;
+  const int rows = B * T;
+  hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
+  if (e == hipSuccess) e = launch_linear(h->x, rows, h->d, 2 * h->d, h->w_pw1, h->scale_pw1, h->u, st);
+  if (e == hipSuccess) e = launch_conv_middle(h->mid, h->u, lens, B, T, h->d, h->o, h->v, st);
+  if (e == hipSuccess)
+    e = launch_linear_resid(h->o, rows, h->d, h->d, h->w_pw2, h->scale_pw2, z, h->res.m_z, h->res.m_y,
+                            h->res.shift_r, z_out, st);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  h->last_B = B;
+  h->last_T = T;
+  return IPK_OK;
+}
+
+extern "C" int ipk_conv_intermediate(ipk_conv_t* h, int32_t which, void* dst, int64_t bytes, void* stream) {
+  if (!h || !dst) return fail(IPK_ERR_INVALID_ARG, "handle and dst must be non-NULL");
+  if (!h->last_B) return fail(IPK_ERR_INVALID_ARG, "no run yet");
+  const int64_t rows = (int64_t)h->last_B * h->last_T;
+  const void* src = nullptr;
+  int64_t need = 0;
+  switch (which) {
+    case IPK_CONV_X: src = h->x; need = rows * h->d; break;
+    case IPK_CONV_U: src = h->u; need = rows * 2 * h->d; break;
+    case IPK_CONV_V: src = h->v; need = rows * h->d * 2; break;
+    case IPK_CONV_O: src = h->o; need = rows * h->d; break;
+    default: return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
+  }
+  if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
+  hipError_t e = hipMemcpyAsync(dst, src, (size_t)need, hipMemcpyDeviceToDevice, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "copy failed: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+extern "C" int ipk_conv_destroy(ipk_conv_t* h) {
+  if (!h) return IPK_OK;
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(h->device);
+  hipError_t e = hipDeviceSynchronize();
+  free_conv(h);
   if (prev >= 0) (void)hipSetDevice(prev);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
   return IPK_OK;

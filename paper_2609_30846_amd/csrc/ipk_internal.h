@@ -148,8 +148,27 @@ hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t*
 hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st);
 hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
                          const uint8_t* swtab, int8_t* o, hipStream_t st);
-hipError_t launch_ffn_down(const int8_t* o, int rows, int d, int d_ff, const int8_t* w2, const double* scale2,
-                           const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st);
+// A row-major linear layer y = clamp8(RS(x W^T)) of `rows` rows (K -> N), and one with the
+// residual add z_out = clamp8(RS(m_z z + m_y y, 1, shift_r)) in its epilogue.
+hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const double* scale, int8_t* y,
+                         hipStream_t st);
+hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const double* scale,
+                               const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st);
+
+// The middle of the convolution module (Eq. 5): GLU, depthwise convolution with folded
+// BatchNorm to the INT16 grid, Swish, requantization to PW2's int8 input.
+struct ConvMiddle {
+  const int8_t* w_dw;     // [d][9]
+  const int32_t* bias_dw;  // [d]
+  const int32_t* mult_dw;  // [d]
+  int shift_dw;
+  long long glu_qc, glu_q1, m_glu;
+  int shift_glu;
+  long long sw_qc, sw_q1, m_sw;
+  int shift_sw;
+};
+hipError_t launch_conv_middle(const ConvMiddle& m, const int8_t* u, const Lengths& lens, int B, int T, int d,
+                              int8_t* o, int16_t* v, hipStream_t st);
 hipError_t launch_layernorm_rows(long rows, int d, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st);
 
 // Workgroup shapes of the attention core for a run: the first shape's nqb1 query

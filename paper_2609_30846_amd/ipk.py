@@ -27,6 +27,7 @@ IPK_MAX_BATCH = 256
 IPK_MAX_T = 8192
 IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN = range(6)
 IPK_FFN_X, IPK_FFN_O = range(2)
+IPK_CONV_X, IPK_CONV_U, IPK_CONV_V, IPK_CONV_O = range(4)
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p
@@ -43,6 +44,10 @@ SIGNATURES = [
     ("ipk_ffn_run", C.c_int, [_vp, _vp, C.c_int32, _vp, _vp]),
     ("ipk_ffn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_ffn_destroy", C.c_int, [_vp]),
+    ("ipk_conv_create", C.c_int, [_vp, C.POINTER(_vp)]),
+    ("ipk_conv_run", C.c_int, [_vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
+    ("ipk_conv_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
+    ("ipk_conv_destroy", C.c_int, [_vp]),
     ("ipk_status_string", C.c_char_p, [C.c_int]),
     ("ipk_last_error", C.c_char_p, []),
     ("ipk_abi_version", C.c_int, []),
@@ -89,8 +94,23 @@ class FfnDesc(C.Structure):
         ("d_model", C.c_int32), ("d_ff", C.c_int32), ("max_rows", C.c_int32),
         ("w1", _vp), ("w2", _vp), ("mult1", _vp), ("mult2", _vp),
         ("shift1", C.c_int32), ("shift2", C.c_int32),
-        ("sw_qc", C.c_int32), ("sw_q1", C.c_int32),
+        ("sw_qc", C.c_int32), ("sw_q1", C.c_int64),
         ("m_sw", C.c_int32), ("shift_sw", C.c_int32),
+        ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
+        ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
+    ]
+
+
+class ConvDesc(C.Structure):
+    """Mirror of ipk_conv_desc."""
+
+    _fields_ = [
+        ("d_model", C.c_int32), ("max_batch", C.c_int32), ("max_T", C.c_int32),
+        ("w_pw1", _vp), ("mult_pw1", _vp), ("shift_pw1", C.c_int32),
+        ("glu_qc", C.c_int32), ("glu_q1", C.c_int64), ("m_glu", C.c_int32), ("shift_glu", C.c_int32),
+        ("w_dw", _vp), ("bias_dw", _vp), ("mult_dw", _vp), ("shift_dw", C.c_int32),
+        ("sw_qc", C.c_int32), ("sw_q1", C.c_int64), ("m_sw", C.c_int32), ("shift_sw", C.c_int32),
+        ("w_pw2", _vp), ("mult_pw2", _vp), ("shift_pw2", C.c_int32),
         ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
         ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
     ]
@@ -370,6 +390,89 @@ class FeedForward:
     def close(self):
         if getattr(self, "handle", None):
             ipk_ffn_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ipk_conv_create(desc: ConvDesc) -> int:
+    h = _vp()
+    _check(load().ipk_conv_create(C.byref(desc), C.byref(h)))
+    return h.value
+
+
+def ipk_conv_run(h: int, z, lengths: Optional[Sequence[int]], B: int, T: int, z_out, stream=None) -> None:
+    lens = None
+    if lengths is not None:
+        lens = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    lp = lens.ctypes.data if lens is not None else None
+    _check(load().ipk_conv_run(h, _ptr(z), lp, int(B), int(T), _ptr(z_out), _stream_ptr(stream)))
+
+
+def ipk_conv_intermediate(h: int, which: int, dst, stream=None) -> None:
+    _check(load().ipk_conv_intermediate(h, int(which), _ptr(dst), int(dst.numel() * dst.element_size()),
+                                        _stream_ptr(stream)))
+
+
+def ipk_conv_destroy(h: Optional[int]) -> None:
+    _check(load().ipk_conv_destroy(h))
+
+
+class ConvModule:
+    """Owns one convolution module handle (Eq. 3 / Eq. 5), built from host arrays: ``cv``
+    carries w_pw1, w_dw, w_pw2, the multipliers, bias_dw, the shifts, the GLU and Swish
+    constants, the LayerNorm constants and the residual multipliers."""
+
+    def __init__(self, cv, max_batch: int, max_T: int, device=None):
+        import torch
+
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        keep = {}
+        desc = ConvDesc()
+        desc.d_model, desc.max_batch, desc.max_T = int(cv.d_model), int(max_batch), int(max_T)
+        for k in ("w_pw1", "w_dw", "w_pw2"):
+            t = torch.as_tensor(np.ascontiguousarray(getattr(cv, k), dtype=np.int8)).to(dev)
+            keep[k] = t
+            setattr(desc, k, t.data_ptr())
+        for k, dt in (("mult_pw1", np.int32), ("bias_dw", np.int32), ("mult_dw", np.int32), ("mult_pw2", np.int32),
+                      ("ln_mult", np.int32), ("ln_bias", np.int64)):
+            a = np.ascontiguousarray(getattr(cv, k), dtype=dt)
+            keep[k] = a
+            setattr(desc, k, a.ctypes.data)
+        for k in ("shift_pw1", "glu_qc", "glu_q1", "m_glu", "shift_glu", "shift_dw", "sw_qc", "sw_q1", "m_sw",
+                  "shift_sw", "shift_pw2", "ln_shift", "m_z", "m_y", "shift_r"):
+            setattr(desc, k, int(getattr(cv, k)))
+        with torch.cuda.device(dev):
+            self.handle = ipk_conv_create(desc)
+        self.device = dev
+        self.d_model = int(cv.d_model)
+
+    def __call__(self, z, lengths=None, z_out=None, stream=None):
+        import torch
+
+        B, T, d = z.shape
+        if z_out is None:
+            z_out = torch.empty_like(z)
+        ipk_conv_run(self.handle, z, lengths, B, T, z_out, stream)
+        return z_out
+
+    def intermediate(self, which: int, B: int, T: int, stream=None):
+        import torch
+
+        d = self.d_model
+        shape, dt = {IPK_CONV_X: ((B, T, d), torch.int8), IPK_CONV_U: ((B, T, 2 * d), torch.int8),
+                     IPK_CONV_V: ((B, T, d), torch.int16), IPK_CONV_O: ((B, T, d), torch.int8)}[which]
+        dst = torch.empty(shape, dtype=dt, device=self.device)
+        ipk_conv_intermediate(self.handle, which, dst, stream)
+        return dst
+
+    def close(self):
+        if getattr(self, "handle", None):
+            ipk_conv_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -200,6 +200,7 @@ BAD_FFN = [
     ("m_sw", 1 << 23, ipk.IPK_ERR_INVALID_ARG),
     ("sw_qc", -1, ipk.IPK_ERR_INVALID_ARG),
     ("sw_qc", 1 << 20, ipk.IPK_ERR_INVALID_ARG),
+    ("sw_q1", 1 << 45, ipk.IPK_ERR_INVALID_ARG),
 ]
 
 
@@ -223,3 +224,60 @@ def test_ffn_create_rejects_swish_overflow():
     assert lib.ipk_ffn_run(None, None, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_ffn_intermediate(None, 0, None, 0, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_ffn_destroy(None) == ipk.IPK_OK
+
+
+
+def test_conv_descriptor_struct_matches_header_field_order():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct ipk_conv_desc \{(.*?)\}", text, flags=re.S).group(1)
+    names = re.findall(r"\*?(\w+)\s*[,;]", body)
+    assert names == [f[0] for f in ipk.ConvDesc._fields_]
+
+
+def _valid_conv_desc():
+    from workloads import make_conv
+
+    cv = make_conv(256, "calibrated", seed=3, S_z=1.0 / 32)
+    keep = []
+    d = ipk.ConvDesc()
+    d.d_model, d.max_batch, d.max_T = 256, 2, 64
+    dummy = np.zeros(16, dtype=np.int8)
+    keep.append(dummy)
+    d.w_pw1 = d.w_dw = d.w_pw2 = dummy.ctypes.data
+    for k, dt in (("mult_pw1", np.int32), ("bias_dw", np.int32), ("mult_dw", np.int32), ("mult_pw2", np.int32),
+                  ("ln_mult", np.int32), ("ln_bias", np.int64)):
+        a = np.ascontiguousarray(getattr(cv, k), dtype=dt)
+        keep.append(a)
+        setattr(d, k, a.ctypes.data)
+    for k in ("shift_pw1", "glu_qc", "glu_q1", "m_glu", "shift_glu", "shift_dw", "sw_qc", "sw_q1", "m_sw",
+              "shift_sw", "shift_pw2", "ln_shift", "m_z", "m_y", "shift_r"):
+        setattr(d, k, int(getattr(cv, k)))
+    return d, keep
+
+
+BAD_CONV = [
+    ("d_model", 96, ipk.IPK_ERR_INVALID_ARG),
+    ("max_batch", 0, ipk.IPK_ERR_INVALID_ARG),
+    ("max_T", 8193, ipk.IPK_ERR_INVALID_ARG),
+    ("w_dw", None, ipk.IPK_ERR_INVALID_ARG),
+    ("bias_dw", None, ipk.IPK_ERR_INVALID_ARG),
+    ("shift_dw", 41, ipk.IPK_ERR_INVALID_ARG),
+    ("shift_sw", 63, ipk.IPK_ERR_INVALID_ARG),
+    ("m_glu", 1 << 23, ipk.IPK_ERR_INVALID_ARG),
+    ("glu_qc", 1 << 20, ipk.IPK_ERR_INVALID_ARG),
+    ("sw_q1", -(1 << 45), ipk.IPK_ERR_INVALID_ARG),
+    ("m_sw", (1 << 23) - 1, ipk.IPK_ERR_UNSUPPORTED),  # Swish of some int16 v times m_sw reaches 2^62
+]
+
+
+@pytest.mark.parametrize("field,value,want", BAD_CONV)
+def test_conv_create_rejects_invalid_descriptor(field, value, want):
+    d, keep = _valid_conv_desc()
+    setattr(d, field, value)
+    h = C.c_void_p()
+    assert ipk.load().ipk_conv_create(C.byref(d), C.byref(h)) == want
+    assert h.value is None
+    assert ipk.last_error() != ""
+    lib = ipk.load()
+    assert lib.ipk_conv_run(None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_conv_destroy(None) == ipk.IPK_OK
