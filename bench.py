@@ -109,7 +109,7 @@ def main():
         return
 
     from paper_2609_30846_amd import ipk
-    from workloads import make_ffn, make_residual, make_workload
+    from workloads import make_conv, make_ffn, make_residual, make_workload
 
     ipk.load()  # fails loudly when the HIP library is missing
     wl = make_workload(args.workload, args.regime)
@@ -197,6 +197,14 @@ def main():
         ms_ffn = timed(lambda: ffn(x, z_out=z_ffn, stream=stream), n_stage)
         ffn_ops = 2 * 2 * B * T * d * ffn_par.d_ff
         ffn.close()
+        # the convolution module of Eq. 3 / Eq. 5 (LayerNorm, PW1, GLU + depthwise + INT16
+        # BatchNorm + Swish, PW2 with the residual) on the same utterances
+        conv_par = make_conv(d, args.regime, seed=wl.seed + 3, S_z=blk.scales["S_x"])
+        conv = ipk.ConvModule(conv_par, max_batch=B, max_T=T, device=dev)
+        z_conv = torch.empty_like(x)
+        ms_conv = timed(lambda: conv(x, lengths=lengths, z_out=z_conv, stream=stream), n_stage)
+        conv_ops = 2 * B * T * d * (2 * d + d) + 2 * 9 * B * T * d
+        conv.close()
 
     proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
     ops = 2 * (proj + pos + attn)
@@ -247,6 +255,11 @@ def main():
                 "d_ff": ffn_par.d_ff,
                 "tops": round(ffn_ops / (ms_ffn * 1e-3) / 1e12, 3),
                 "pct_int8_peak": round(100.0 * ffn_ops / (ms_ffn * 1e-3) / 1e12 / INT8_PEAK_TOPS, 3),
+            },
+            "conv_module_int16_batchnorm": {
+                "ms_per_step": round(ms_conv, 5),
+                "frames_per_s": round(float(np.sum(lengths)) / (ms_conv * 1e-3), 1),
+                "tops": round(conv_ops / (ms_conv * 1e-3) / 1e12, 3),
             },
             "timing": f"{n_stage} steps each between two HIP events, after 5 warm-up steps",
         },

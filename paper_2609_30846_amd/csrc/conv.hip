@@ -10,20 +10,23 @@
 // Every product fits 64 bits: the host proves |a sigma| m_glu and |swish(v)| m_sw below
 // 2^62 for every int8 pair and every int16 v before it accepts the constants.
 //
-// One thread per channel, a workgroup per (utterance, 256 channels, 64 frames): the
-// thread computes the GLU of its channel over the 72 frames the window needs into its
-// own LDS column (no other thread reads it, so no barrier), then slides the 9 taps.
-// Loads and stores of a frame are 256 consecutive bytes across the workgroup.  The
-// work is a few hundred bytes per frame and channel of integer arithmetic: the kernel
-// is bound by its VALU work and the HBM traffic of PW1's output (2 d bytes per frame
-// in, d + 2 d bytes out with the int16 BatchNorm output).
+// One thread per channel, a workgroup per (utterance, 256 channels, 16 frames): the
+// thread computes the GLU of its channel over the 24 frames the window needs, in
+// registers, then slides the 9 taps over them.  The GLU's sigmoid of every int8 input
+// sits in LDS (256 values, computed by the workgroup), and the Swish of every int16
+// value and its requantization in a 64 KB table computed once per handle
+// (`swish16_table`), so an output costs its nine multiply-adds, one requantization
+// and one table load.  Loads and stores of a frame are 256 consecutive elements across
+// the workgroup.  Per frame and channel the kernel moves 2 bytes of PW1's output in and
+// 3 bytes out (the int8 Swish output and the int16 BatchNorm output).
 #include "ipk_internal.h"
 
 namespace ipk {
 
 constexpr int CONV_TAPS = 9, CONV_HALF = 4;
-constexpr int CONV_FRAMES = 64;   // output frames per workgroup
+constexpr int CONV_FRAMES = 16;   // output frames per workgroup (the window: 24 frames in registers)
 constexpr int CONV_CH = 256;      // channels per workgroup (one per thread)
+constexpr int CONV_WIN = CONV_FRAMES + 2 * CONV_HALF;
 
 struct ConvArgs {
   const int8_t* u;  // [B][T][2 d] PW1 output: a = channels [0, d), b = [d, 2 d)
@@ -32,12 +35,11 @@ struct ConvArgs {
   const int8_t* w;  // [d][9]
   const int32_t* bias;
   const int32_t* mult;
-  Lengths lens;  // valid frames per utterance
+  const int8_t* swtab16;  // [65535]: Swish output of each int16 v, at v + 32767
+  Lengths lens;           // valid frames per utterance
   int T, d, shift_dw;
   long long glu_qc, glu_q1, m_glu;
   int shift_glu;
-  long long sw_qc, sw_q1, m_sw;
-  int shift_sw;
 };
 
 __device__ __forceinline__ long long rs64(long long a, long long m, int n) {
@@ -49,54 +51,73 @@ __device__ __forceinline__ long long poly_l(long long aq, long long q_c, long lo
   return t * t + q_1;
 }
 
+// The Swish of Eq. 12 on every int16 input and its requantization to PW2's int8 grid,
+// one thread per value (computed once per handle; the middle kernel looks it up).
+__global__ __launch_bounds__(256) void swish16_table(int8_t* tab, long long q_c, long long q_1, long long m,
+                                                     int shift) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= 65535) return;
+  const long long v = (long long)i - 32767;
+  const long long av = v < 0 ? -v : v;
+  const long long q = -(av * poly_l(av, q_c, q_1) + v * q_1);
+  const long long o = rs64(q, m, shift);
+  tab[i] = (int8_t)(o < -127 ? -127 : (o > 127 ? 127 : o));
+}
+
 __global__ __launch_bounds__(CONV_CH) void conv_glu_dw_swish(ConvArgs a) {
-  __shared__ int8_t gcol[CONV_FRAMES + 2 * CONV_HALF][CONV_CH];
+  // the GLU sigmoid of every int8 b, at b + 128
+  __shared__ long long sig[256];
   const int tid = threadIdx.x;
+  {
+    const long long bv = (long long)tid - 128;
+    const long long ab = bv < 0 ? -bv : bv;
+    const long long sg = bv > 0 ? 1 : (bv < 0 ? -1 : 0);
+    sig[tid] = -(a.glu_q1 + sg * poly_l(ab, a.glu_qc, a.glu_q1));
+  }
+  __syncthreads();
   const int c = blockIdx.y * CONV_CH + tid;
   const int b = blockIdx.z;
   const int t0 = blockIdx.x * CONV_FRAMES;
   const int T = a.T, d = a.d;
   if (c >= d) return;
   const int L = a.lens.len[b];
-  const int8_t* ub = a.u + (size_t)b * T * 2 * d;
-  // GLU over the window of frames t0 - 4 .. t0 + 64 + 3
-  for (int f = 0; f < CONV_FRAMES + 2 * CONV_HALF; ++f) {
+  const int8_t* ub = a.u + (size_t)b * T * 2 * d + c;
+  // GLU over the window t0 - 4 .. t0 + 19, in registers (static indices)
+  int g[CONV_WIN];
+#pragma unroll
+  for (int f = 0; f < CONV_WIN; ++f) {
     const int t = t0 - CONV_HALF + f;
-    long long gv = 0;
+    int gv = 0;
     if (t >= 0 && t < L) {
-      const long long av = ub[(size_t)t * 2 * d + c], bv = ub[(size_t)t * 2 * d + d + c];
-      const long long ab = bv < 0 ? -bv : bv;
-      const long long sg = bv > 0 ? 1 : (bv < 0 ? -1 : 0);
-      const long long sig = -(a.glu_q1 + sg * poly_l(ab, a.glu_qc, a.glu_q1));
-      gv = rs64(av * sig, a.m_glu, a.shift_glu);
-      gv = gv < -127 ? -127 : (gv > 127 ? 127 : gv);
+      const long long av = ub[(size_t)t * 2 * d], bi = ub[(size_t)t * 2 * d + d];
+      long long r = rs64(av * sig[bi + 128], a.m_glu, a.shift_glu);
+      gv = (int)(r < -127 ? -127 : (r > 127 ? 127 : r));
     }
-    gcol[f][tid] = (int8_t)gv;
+    g[f] = gv;
   }
   int w[CONV_TAPS];
 #pragma unroll
   for (int k = 0; k < CONV_TAPS; ++k) w[k] = a.w[c * CONV_TAPS + k];
   const int bias = a.bias[c];
   const long long mdw = a.mult[c];
-  const int tend = min(t0 + CONV_FRAMES, T);
-  for (int t = t0; t < tend; ++t) {
-    const int f = t - t0;
+#pragma unroll
+  for (int f = 0; f < CONV_FRAMES; ++f) {
+    const int t = t0 + f;
+    if (t >= T) break;
     int acc = bias;
 #pragma unroll
-    for (int k = 0; k < CONV_TAPS; ++k) acc += w[k] * (int)gcol[f + k][tid];
+    for (int k = 0; k < CONV_TAPS; ++k) acc += w[k] * g[f + k];
     long long vv = rs64(acc, mdw, a.shift_dw);
     vv = vv < -32767 ? -32767 : (vv > 32767 ? 32767 : vv);
     const size_t idx = ((size_t)b * T + t) * d + c;
     a.v[idx] = (int16_t)vv;
-    long long ov = 0;
-    if (t < L) {
-      const long long av = vv < 0 ? -vv : vv;
-      const long long q = -(av * poly_l(av, a.sw_qc, a.sw_q1) + vv * a.sw_q1);
-      ov = rs64(q, a.m_sw, a.shift_sw);
-      ov = ov < -127 ? -127 : (ov > 127 ? 127 : ov);
-    }
-    a.o[idx] = (int8_t)ov;
+    a.o[idx] = t < L ? a.swtab16[vv + 32767] : (int8_t)0;
   }
+}
+
+hipError_t launch_swish16_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st) {
+  hipLaunchKernelGGL(swish16_table, dim3((65535 + 255) / 256), dim3(256), 0, st, tab, q_c, q_1, m, shift);
+  return hipGetLastError();
 }
 
 hipError_t launch_conv_middle(const ConvMiddle& m, const int8_t* u, const Lengths& lens, int B, int T, int d,
@@ -116,10 +137,7 @@ hipError_t launch_conv_middle(const ConvMiddle& m, const int8_t* u, const Length
   a.glu_q1 = m.glu_q1;
   a.m_glu = m.m_glu;
   a.shift_glu = m.shift_glu;
-  a.sw_qc = m.sw_qc;
-  a.sw_q1 = m.sw_q1;
-  a.m_sw = m.m_sw;
-  a.shift_sw = m.shift_sw;
+  a.swtab16 = m.swtab16;
   const dim3 grid((unsigned)((T + CONV_FRAMES - 1) / CONV_FRAMES), (unsigned)((d + CONV_CH - 1) / CONV_CH),
                   (unsigned)B);
   hipLaunchKernelGGL(conv_glu_dw_swish, grid, dim3(CONV_CH), 0, st, a);

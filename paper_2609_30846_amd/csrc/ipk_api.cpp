@@ -788,6 +788,8 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   chk(conv_alloc(h, &h->o, R * d));
   chk(conv_alloc(h, &h->v, R * d));
   chk(conv_alloc(h, &stage, 2 * d * d));
+  int8_t* sw16 = nullptr;
+  chk(conv_alloc(h, &sw16, 65535));
   if (e != hipSuccess) {
     free_conv(h);
     (void)hipGetLastError();
@@ -810,6 +812,7 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   for (size_t k = 0; k < d; ++k) cb[k] = desc->ln_bias[k] + ((int64_t)1 << (desc->ln_shift - 1));
   chk(hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
   chk(hipMemcpy(c, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice));
+  chk(launch_swish16_table(sw16, desc->sw_qc, desc->sw_q1, desc->m_sw, desc->shift_sw, nullptr));
   chk(hipDeviceSynchronize());
   if (e != hipSuccess) {
     free_conv(h);
@@ -826,10 +829,7 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   h->mid.glu_q1 = desc->glu_q1;
   h->mid.m_glu = desc->m_glu;
   h->mid.shift_glu = desc->shift_glu;
-  h->mid.sw_qc = desc->sw_qc;
-  h->mid.sw_q1 = desc->sw_q1;
-  h->mid.m_sw = desc->m_sw;
-  h->mid.shift_sw = desc->shift_sw;
+  h->mid.swtab16 = sw16;
   h->res.ln_mult = g;
   h->res.ln_bias = c;
   h->res.ln_shift = desc->ln_shift;

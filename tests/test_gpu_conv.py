@@ -101,3 +101,41 @@ def test_conv_argument_errors(gpu_lib):
         mod.intermediate(ipk.IPK_CONV_V, 2, 16)
     assert ei.value.status == ipk.IPK_ERR_INVALID_ARG
     mod.close()
+
+
+def test_conformer_modules_chained(gpu_lib):
+    """The four residual sub-modules of the Conformer block in order (Eq. 1 - 4: FFN,
+    MHSA, convolution, FFN), each on the previous one's int8 output, on the GPU and in
+    the oracle: byte-equal after every module."""
+    import torch
+
+    from workloads import make_ffn, make_residual
+
+    ipk = gpu_lib
+    blk = make_workload("parakeet", "calibrated").blocks[0]
+    B, T, d = blk.x.shape
+    f1 = make_ffn(d, "calibrated", seed=1, S_z=blk.scales["S_x"])
+    res = make_residual(blk, "calibrated", seed=2)
+    cv = make_conv(d, "calibrated", seed=3, S_z=blk.scales["S_x"])
+    f2 = make_ffn(d, "calibrated", seed=4, S_z=blk.scales["S_x"])
+    m_f1, m_f2 = ipk.FeedForward(f1, max_rows=B * T), ipk.FeedForward(f2, max_rows=B * T)
+    m_at = ipk.RelPosAttn.from_block(blk)
+    m_at.set_residual_from(res)
+    m_cv = ipk.ConvModule(cv, max_batch=B, max_T=T)
+    pe = torch.from_numpy(blk.pos_table).cuda()
+    z = torch.from_numpy(blk.x).cuda()
+    zr = blk.x
+    steps = [
+        ("ffn1", lambda t: m_f1(t), lambda a: core.ffn_module(f1, a)),
+        ("mhsa", lambda t: m_at.residual(t, pe, lengths=blk.lengths), lambda a: core.mhsa_residual(blk, res, z1=a)),
+        ("conv", lambda t: m_cv(t, lengths=blk.lengths), lambda a: core.conv_module(cv, a, lengths=blk.lengths)),
+        ("ffn2", lambda t: m_f2(t), lambda a: core.ffn_module(f2, a)),
+    ]
+    for name, gpu, ora in steps:
+        z = gpu(z)
+        torch.cuda.synchronize()
+        zr = ora(zr)
+        assert _first_mismatch(z.cpu().numpy(), zr) is None, name
+        print(f"[chain] {name} ok", flush=True)
+    for m in (m_f1, m_f2, m_at, m_cv):
+        m.close()
