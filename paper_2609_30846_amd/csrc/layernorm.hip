@@ -15,9 +15,9 @@
 // so the row is read once.  Both sums come from one pass: sum z and sum z^2 by
 // v_dot4 against ones and against z itself, and
 //   sum (z - mu)^2 = sum z^2 - 2 mu sum z + d mu^2
-// exactly in integers.  floor(sqrt(v)) is the correctly rounded double square root
-// truncated and then checked against v (v < 2^31, so the double is within one of
-// the root and one correction step suffices either way).
+// exactly in integers, and the wave sums are DPP adds.  floor(sqrt(v)) is the correctly
+// rounded double square root truncated and then checked against v (v < 2^31, so the
+// double is within one of the root and one correction step suffices either way).
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -35,10 +35,16 @@ struct LnArgs {
 
 constexpr int LN_WAVES = 4;  // rows per workgroup
 
+// Sum over the wave: DPP adds leave every lane of a 16-lane row with the row's sum
+// (quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror), and the four
+// row sums are read as scalars.  Integer adds, so the order does not matter.
 __device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) + __builtin_amdgcn_readlane(v, 32) +
+         __builtin_amdgcn_readlane(v, 48);
 }
 
 // floor(a / b) for b > 0
@@ -76,7 +82,10 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
   if (sg * sg > var) --sg;
   if ((sg + 1) * (sg + 1) <= var) ++sg;
   if (sg < 1) sg = 1;
-  const long long F = (1ll << 31) / sg;
+  // floor(2^31 / sigma) from the correctly rounded double quotient: unless sigma divides
+  // 2^31 the quotient lies at least 1 / sigma >= 2^-16 below the next integer, far more
+  // than its rounding error (2^31 2^-53), so truncating it gives the floor
+  const long long F = (long long)(2147483648.0 / (double)sg);
   // u = floor(y F / 2) for y = z - mu, in 32 bits: with F = 2 Fh + Fo,
   // u = y Fh + Fo floor(y / 2), and |y Fh| <= |y| F / 2 <= 2^30 since |y| <= sigma
   const int Fh = (int)(F >> 1), Fo = (F & 1) ? -1 : 0;
