@@ -205,6 +205,30 @@ def main():
         ms_conv = timed(lambda: conv(x, lengths=lengths, z_out=z_conv, stream=stream), n_stage)
         conv_ops = 2 * B * T * d * (2 * d + d) + 2 * 9 * B * T * d
         conv.close()
+        # the 24-block stack workload (B = 8, T = 500): each block's int8 output feeds the
+        # next block; encoder frames per second over whole 24-block passes
+        swl = make_workload("stack", args.regime)
+        sblk = swl.blocks
+        smods = [ipk.RelPosAttn.from_block(b_, device=dev) for b_ in sblk]
+        sx = torch.from_numpy(sblk[0].x).to(dev)
+        spe = torch.from_numpy(sblk[0].pos_table).to(dev)
+        sbuf = [torch.empty_like(sx), torch.empty_like(sx)]
+
+        def stack_pass():
+            cur = sx
+            for i_, (m_, b_) in enumerate(zip(smods, sblk)):
+                m_(cur, spe, lengths=b_.lengths, y=sbuf[i_ % 2], stream=stream)
+                cur = sbuf[i_ % 2]
+
+        n_stack = max(1, min(20, n_stage // 10))
+        ms_stack = timed(stack_pass, n_stack)
+        sB, sT = sblk[0].x.shape[0], sblk[0].T
+        s_ops = 0
+        for b_ in sblk:
+            p_, q_, r_ = algorithmic_macs(sB, sT, d, H, dk, b_.lengths)
+            s_ops += 2 * (p_ + q_ + r_)
+        for m_ in smods:
+            m_.close()
 
     proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
     ops = 2 * (proj + pos + attn)
@@ -260,6 +284,13 @@ def main():
                 "ms_per_step": round(ms_conv, 5),
                 "frames_per_s": round(float(np.sum(lengths)) / (ms_conv * 1e-3), 1),
                 "tops": round(conv_ops / (ms_conv * 1e-3) / 1e12, 3),
+            },
+            "stack_24_blocks": {
+                "workload": f"stack: 24 blocks, B={sB} T={sT} d_model={d} H={H}, {args.regime} scales, seed {swl.seed}",
+                "ms_per_pass": round(ms_stack, 4),
+                "encoder_frames_per_s": round(sB * sT / (ms_stack * 1e-3), 1),
+                "tops": round(s_ops / (ms_stack * 1e-3) / 1e12, 3),
+                "passes_timed": n_stack,
             },
             "timing": f"{n_stage} steps each between two HIP events, after 5 warm-up steps",
         },
