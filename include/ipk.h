@@ -365,6 +365,32 @@ int ipk_conv_intermediate(ipk_conv_t* h, int32_t which, void* dst, int64_t bytes
 /* Frees the handle after synchronizing the device; NULL is a no-op. */
 int ipk_conv_destroy(ipk_conv_t* h);
 
+/*
+ * The integer LayerNorm alone (the LN of Eq. 1 - 4, defined above under
+ * ipk_mhsa_residual_desc), for the block's final normalization H = LN(...) of Eq. 4.
+ * ln_mult HOST int32 [d_model], ln_bias HOST int64 [d_model]; ranges as for the MHSA
+ * module: |ln_mult| < 2^24, |ln_bias| < 2^56, ln_shift in [1, 62]; d_model a multiple of
+ * 16 in [16, 16384].  create copies them to the device (synchronously).
+ */
+typedef struct ipk_layernorm_desc {
+  int32_t d_model;
+  const int32_t* ln_mult;
+  const int64_t* ln_bias;
+  int32_t ln_shift;
+} ipk_layernorm_desc;
+
+typedef struct ipk_layernorm ipk_layernorm_t;
+
+int ipk_layernorm_create(const ipk_layernorm_desc* desc, ipk_layernorm_t** out);
+
+/* x = LN(z) row by row on `stream`: z, x DEVICE int8 [rows][d_model], 16-byte aligned,
+ * x may be z itself.  Errors: IPK_ERR_INVALID_ARG (null handle or pointer, misalignment,
+ * rows < 1, partial overlap), IPK_ERR_HIP. */
+int ipk_layernorm_run(ipk_layernorm_t* h, const int8_t* z, int64_t rows, int8_t* x, void* stream);
+
+/* Frees the handle after synchronizing the device; NULL is a no-op. */
+int ipk_layernorm_destroy(ipk_layernorm_t* h);
+
 /* Human-readable name of a status code (static storage). */
 const char* ipk_status_string(int status);
 

@@ -907,6 +907,93 @@ extern "C" int ipk_conv_destroy(ipk_conv_t* h) {
   return IPK_OK;
 }
 
+// ---------------------------------------------------------------------------
+// The integer LayerNorm alone (the final LN of Eq. 4).
+
+struct ipk_layernorm {
+  int device, d;
+  Residual res;  // only the LayerNorm fields are used
+  std::vector<void*> allocs;
+};
+
+static void free_ln(ipk_layernorm* h) {
+  if (!h) return;
+  for (void* p : h->allocs) (void)hipFree(p);
+  delete h;
+}
+
+extern "C" int ipk_layernorm_create(const ipk_layernorm_desc* desc, ipk_layernorm_t** out) {
+  g_last_error[0] = 0;
+  if (!out) return fail(IPK_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!desc) return fail(IPK_ERR_INVALID_ARG, "desc is NULL");
+  const int d = desc->d_model;
+  if (d < 16 || d % 16 || d > 16384) return fail(IPK_ERR_INVALID_ARG, "d_model=%d must be a multiple of 16 in [16, 16384]", d);
+  if (!desc->ln_mult || !desc->ln_bias) return fail(IPK_ERR_INVALID_ARG, "ln_mult and ln_bias must be non-NULL");
+  if (desc->ln_shift < 1 || desc->ln_shift > 62) return fail(IPK_ERR_INVALID_ARG, "ln_shift=%d outside [1, 62]", desc->ln_shift);
+  std::vector<int64_t> cb(d);
+  for (int k = 0; k < d; ++k) {
+    if (desc->ln_mult[k] <= -(1 << 24) || desc->ln_mult[k] >= (1 << 24))
+      return fail(IPK_ERR_INVALID_ARG, "ln_mult[%d]=%d outside (-2^24, 2^24)", k, desc->ln_mult[k]);
+    if (desc->ln_bias[k] <= -((int64_t)1 << 56) || desc->ln_bias[k] >= ((int64_t)1 << 56))
+      return fail(IPK_ERR_INVALID_ARG, "ln_bias[%d] outside (-2^56, 2^56)", k);
+    cb[k] = desc->ln_bias[k] + ((int64_t)1 << (desc->ln_shift - 1));
+  }
+  ipk_layernorm* h = new (std::nothrow) ipk_layernorm();
+  if (!h) return fail(IPK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  h->d = d;
+  hipError_t e = hipGetDevice(&h->device);
+  void *g = nullptr, *c = nullptr;
+  if (e == hipSuccess) e = hipMalloc(&g, d * sizeof(int32_t));
+  if (e == hipSuccess) h->allocs.push_back(g);
+  if (e == hipSuccess) e = hipMalloc(&c, d * sizeof(int64_t));
+  if (e == hipSuccess) h->allocs.push_back(c);
+  if (e == hipSuccess) e = hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(c, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    free_ln(h);
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? IPK_ERR_OUT_OF_MEMORY : IPK_ERR_HIP, "device setup failed: %s",
+                hipGetErrorString(e));
+  }
+  h->res.ln_mult = (const int32_t*)g;
+  h->res.ln_bias = (const int64_t*)c;
+  h->res.ln_shift = desc->ln_shift;
+  *out = h;
+  return IPK_OK;
+}
+
+extern "C" int ipk_layernorm_run(ipk_layernorm_t* h, const int8_t* z, int64_t rows, int8_t* x, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!z || !x) return fail(IPK_ERR_INVALID_ARG, "z and x must be non-NULL");
+  if (((uintptr_t)z | (uintptr_t)x) & 15) return fail(IPK_ERR_INVALID_ARG, "z and x must be 16-byte aligned");
+  if (rows < 1 || rows > ((int64_t)1 << 31) / h->d) return fail(IPK_ERR_INVALID_ARG, "rows=%lld outside [1, 2^31 / d)", (long long)rows);
+  if (z != x) {
+    const size_t n = (size_t)rows * h->d;
+    const uintptr_t a = (uintptr_t)z, b = (uintptr_t)x;
+    if (a < b + n && b < a + n) return fail(IPK_ERR_INVALID_ARG, "z and x overlap without being equal");
+  }
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  hipError_t e = launch_layernorm_rows((long)rows, h->d, h->res, z, x, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
+extern "C" int ipk_layernorm_destroy(ipk_layernorm_t* h) {
+  if (!h) return IPK_OK;
+  int prev = -1;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(h->device);
+  hipError_t e = hipDeviceSynchronize();
+  free_ln(h);
+  if (prev >= 0) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "device error at destroy: %s", hipGetErrorString(e));
+  return IPK_OK;
+}
+
 extern "C" const char* ipk_status_string(int status) {
   switch (status) {
     case IPK_OK: return "IPK_OK";

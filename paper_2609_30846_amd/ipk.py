@@ -48,6 +48,9 @@ SIGNATURES = [
     ("ipk_conv_run", C.c_int, [_vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
     ("ipk_conv_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_conv_destroy", C.c_int, [_vp]),
+    ("ipk_layernorm_create", C.c_int, [_vp, C.POINTER(_vp)]),
+    ("ipk_layernorm_run", C.c_int, [_vp, _vp, C.c_int64, _vp, _vp]),
+    ("ipk_layernorm_destroy", C.c_int, [_vp]),
     ("ipk_status_string", C.c_char_p, [C.c_int]),
     ("ipk_last_error", C.c_char_p, []),
     ("ipk_abi_version", C.c_int, []),
@@ -114,6 +117,12 @@ class ConvDesc(C.Structure):
         ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32),
         ("m_z", C.c_int32), ("m_y", C.c_int32), ("shift_r", C.c_int32),
     ]
+
+
+class LayerNormDesc(C.Structure):
+    """Mirror of ipk_layernorm_desc."""
+
+    _fields_ = [("d_model", C.c_int32), ("ln_mult", _vp), ("ln_bias", _vp), ("ln_shift", C.c_int32)]
 
 
 _lib = None
@@ -473,6 +482,54 @@ class ConvModule:
     def close(self):
         if getattr(self, "handle", None):
             ipk_conv_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ipk_layernorm_create(desc: LayerNormDesc) -> int:
+    h = _vp()
+    _check(load().ipk_layernorm_create(C.byref(desc), C.byref(h)))
+    return h.value
+
+
+def ipk_layernorm_run(h: int, z, rows: int, x, stream=None) -> None:
+    _check(load().ipk_layernorm_run(h, _ptr(z), int(rows), _ptr(x), _stream_ptr(stream)))
+
+
+def ipk_layernorm_destroy(h: Optional[int]) -> None:
+    _check(load().ipk_layernorm_destroy(h))
+
+
+class LayerNorm:
+    """Owns one integer LayerNorm handle; ``p`` carries ln_mult, ln_bias, ln_shift."""
+
+    def __init__(self, d_model: int, p, device=None):
+        import torch
+
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        g = np.ascontiguousarray(p.ln_mult, dtype=np.int32)
+        c = np.ascontiguousarray(p.ln_bias, dtype=np.int64)
+        desc = LayerNormDesc(int(d_model), g.ctypes.data, c.ctypes.data, int(p.ln_shift))
+        with torch.cuda.device(dev):
+            self.handle = ipk_layernorm_create(desc)
+        self.device, self.d_model = dev, int(d_model)
+
+    def __call__(self, z, x=None, stream=None):
+        import torch
+
+        if x is None:
+            x = torch.empty_like(z)
+        ipk_layernorm_run(self.handle, z, z.numel() // self.d_model, x, stream)
+        return x
+
+    def close(self):
+        if getattr(self, "handle", None):
+            ipk_layernorm_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

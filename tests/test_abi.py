@@ -281,3 +281,21 @@ def test_conv_create_rejects_invalid_descriptor(field, value, want):
     lib = ipk.load()
     assert lib.ipk_conv_run(None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_conv_destroy(None) == ipk.IPK_OK
+
+
+
+def test_layernorm_descriptor_and_validation():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct ipk_layernorm_desc \{(.*?)\}", text, flags=re.S).group(1)
+    assert re.findall(r"\*?(\w+)\s*[,;]", body) == [f[0] for f in ipk.LayerNormDesc._fields_]
+    lib = ipk.load()
+    g = np.zeros(256, dtype=np.int32)
+    c = np.zeros(256, dtype=np.int64)
+    for d_model, shift, gbad in ((100, 40, 0), (256, 0, 0), (256, 63, 0), (256, 40, 1 << 24)):
+        g[5] = gbad
+        desc = ipk.LayerNormDesc(d_model, g.ctypes.data, c.ctypes.data, shift)
+        h = C.c_void_p()
+        assert lib.ipk_layernorm_create(C.byref(desc), C.byref(h)) == ipk.IPK_ERR_INVALID_ARG
+        assert h.value is None
+    assert lib.ipk_layernorm_run(None, None, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_layernorm_destroy(None) == ipk.IPK_OK

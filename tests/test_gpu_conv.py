@@ -104,9 +104,9 @@ def test_conv_argument_errors(gpu_lib):
 
 
 def test_conformer_modules_chained(gpu_lib):
-    """The four residual sub-modules of the Conformer block in order (Eq. 1 - 4: FFN,
-    MHSA, convolution, FFN), each on the previous one's int8 output, on the GPU and in
-    the oracle: byte-equal after every module."""
+    """The whole Conformer block (Eq. 1 - 4): the four residual sub-modules in order
+    (FFN, MHSA, convolution, FFN) and the final LayerNorm, each on the previous one's
+    int8 output, on the GPU and in the oracle: byte-equal after every step."""
     import torch
 
     from workloads import make_ffn, make_residual
@@ -131,11 +131,21 @@ def test_conformer_modules_chained(gpu_lib):
         ("conv", lambda t: m_cv(t, lengths=blk.lengths), lambda a: core.conv_module(cv, a, lengths=blk.lengths)),
         ("ffn2", lambda t: m_f2(t), lambda a: core.ffn_module(f2, a)),
     ]
+    # Eq. 4 ends with a LayerNorm of its own: H = LN(Z3 + 0.5 FFN2(LN(Z3)))
+    ln_par = make_residual(blk, "calibrated", seed=5)
+    m_ln = ipk.LayerNorm(d, ln_par)
+    steps.append(("final LayerNorm", lambda t: m_ln(t), lambda a: core.layernorm(a, ln_par)))
     for name, gpu, ora in steps:
         z = gpu(z)
         torch.cuda.synchronize()
         zr = ora(zr)
         assert _first_mismatch(z.cpu().numpy(), zr) is None, name
         print(f"[chain] {name} ok", flush=True)
-    for m in (m_f1, m_f2, m_at, m_cv):
+    # in place, on rows not a multiple of the workgroup's four
+    zz = torch.from_numpy(np.ascontiguousarray(blk.x[0, :37])).cuda()
+    ref = core.layernorm(blk.x[0, :37], ln_par)
+    m_ln(zz, x=zz)
+    torch.cuda.synchronize()
+    assert _first_mismatch(zz.cpu().numpy(), ref) is None, "layernorm in place"
+    for m in (m_f1, m_f2, m_at, m_cv, m_ln):
         m.close()
