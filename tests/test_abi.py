@@ -299,3 +299,35 @@ def test_layernorm_descriptor_and_validation():
         assert h.value is None
     assert lib.ipk_layernorm_run(None, None, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_layernorm_destroy(None) == ipk.IPK_OK
+
+
+def test_generated_module_constants_pass_validation_ranges():
+    """Every generated feed-forward and convolution module (both regimes, the model
+    widths of the workloads) has integers inside the ranges create() accepts, including
+    the 64-bit product bounds of the Swish and GLU requantizations."""
+    from workloads import make_conv, make_ffn
+
+    for regime in ("literal", "calibrated"):
+        for d in (256, 1024):
+            for seed in (1, 2):
+                f = make_ffn(d, regime, seed=seed, S_z=1.0 / 32)
+                assert f.mult1.min() >= 0 and f.mult1.max() < (1 << 23) and 1 <= f.shift_sw <= 40
+                assert 0 <= f.sw_qc < (1 << 20) and abs(f.sw_q1) < (1 << 45) and 0 <= f.m_sw < (1 << 23)
+                for h in range(-127, 128):
+                    ah = abs(h)
+                    t = min(ah, f.sw_qc) - f.sw_qc
+                    q = -(ah * (t * t + f.sw_q1) + h * f.sw_q1)
+                    assert abs(q) * f.m_sw + (1 << (f.shift_sw - 1)) < (1 << 62)
+                cv = make_conv(d, regime, seed=seed, S_z=1.0 / 32)
+                assert cv.mult_dw.max() < (1 << 23) and 1 <= cv.shift_dw <= 40
+                assert 1 <= cv.shift_glu <= 62 and 1 <= cv.shift_sw <= 62
+                assert abs(cv.glu_q1) < (1 << 45) and abs(cv.sw_q1) < (1 << 45)
+                assert np.abs(cv.bias_dw.astype(np.int64)).max() < (1 << 30)
+                smax = max(abs(-(cv.glu_q1 + (1 if b > 0 else -1 if b < 0 else 0) *
+                                 ((min(abs(b), cv.glu_qc) - cv.glu_qc) ** 2 + cv.glu_q1))) for b in range(-127, 128))
+                assert smax * 128 * cv.m_glu + (1 << (cv.shift_glu - 1)) < (1 << 62)
+                v = np.arange(-32767, 32768, dtype=object)
+                av = np.abs(v)
+                t = np.minimum(av, cv.sw_qc) - cv.sw_qc
+                q = np.abs(-(av * (t * t + cv.sw_q1) + v * cv.sw_q1))
+                assert int(q.max()) * cv.m_sw + (1 << (cv.shift_sw - 1)) < (1 << 62)
