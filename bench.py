@@ -48,13 +48,14 @@ def algorithmic_macs(B, T, d, H, dk, lengths):
 
 
 def kernel_source_hash() -> str:
-    """Hash of the HIP sources the library is built from."""
+    """Hash of the kernel sources (the HIP files and their shared header; the C-ABI
+    glue in ipk_api.cpp does not change what a kernel reads or writes)."""
     import glob
     import hashlib
 
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_30846_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*"))):
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
         with open(f, "rb") as fh:
             h.update(os.path.basename(f).encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
