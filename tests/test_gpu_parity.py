@@ -195,3 +195,47 @@ def test_run_argument_errors(gpu_lib):
     with pytest.raises(gpu_lib.IpkError):
         gpu_lib.ipk_relpos_attn_run(mod.handle, None, pe, None, 1, 64, y)
     mod.close()
+
+
+def test_longest_supported_T(gpu_lib):
+    """The longest utterance the on-chip score rows allow (create rejects a longer
+    max_T with IPK_ERR_UNSUPPORTED), with a ragged second utterance, d_k = 64 and 128."""
+    import dataclasses
+
+    from workloads import generate
+
+    ipk = gpu_lib
+    for d, H in ((256, 4), (256, 2)):
+        shape = dataclasses.replace(generate.config_by_name("tiny"), B=2, d_model=d, n_heads=H, name="tiny")
+        probe = generate.make_block(dataclasses.replace(shape, B=1), 16, np.random.default_rng(1), "calibrated")
+        T_max = None
+        for T in range(4096, 0, -64):
+            try:
+                m = ipk.RelPosAttn.from_block(probe, max_batch=1, max_T=T)
+            except ipk.IpkError as e:
+                assert e.status == ipk.IPK_ERR_UNSUPPORTED
+                continue
+            m.close()
+            T_max = T
+            break
+        assert T_max is not None and T_max >= 2500
+        with pytest.raises(ipk.IpkError):
+            ipk.RelPosAttn.from_block(probe, max_batch=1, max_T=T_max + 64)
+        blk = generate.make_block(shape, T_max, np.random.default_rng(T_max + d + H), "calibrated",
+                                  lengths=[T_max, T_max - 37])
+        print(f"[parity] longest T={T_max} d_k={d // H}", flush=True)
+        g = _run_gpu(ipk, blk)
+        y = core.relpos_attn(blk)
+        assert _first_mismatch(g["y"], y) is None, (T_max, d // H, _first_mismatch(g["y"], y))
+
+
+@pytest.mark.parametrize("which", ["no_position", "no_scores"])
+def test_degenerate_score_scales(gpu_lib, which, score_path):
+    """m_p = 0 switches the position branch of Eq. 11 off; m_c = m_p = 0 makes every
+    score 0, so each row's softmax is uniform over its valid keys."""
+    blk = make_workload("batched", "calibrated", B=3).blocks[0]
+    blk.consts = dict(blk.consts)
+    blk.consts["m_p"] = 0
+    if which == "no_scores":
+        blk.consts["m_c"] = 0
+    _check_block(gpu_lib, blk, f"degenerate {which}")
