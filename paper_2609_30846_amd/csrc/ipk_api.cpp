@@ -131,8 +131,9 @@ static void free_handle(ipk_relpos_attn* h) {
   delete h;
 }
 
-template <typename T>
-static hipError_t dev_alloc(ipk_relpos_attn* h, T** p, size_t count) {
+// Device allocation recorded on any handle type with an `allocs` list (freed with it).
+template <typename H, typename T>
+static hipError_t dev_alloc(H* h, T** p, size_t count) {
   void* q = nullptr;
   hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
   if (e != hipSuccess) return e;
@@ -484,16 +485,6 @@ static void free_ffn(ipk_ffn* h) {
   delete h;
 }
 
-template <typename T>
-static hipError_t ffn_alloc(ipk_ffn* h, T** p, size_t count) {
-  void* q = nullptr;
-  hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
-  if (e != hipSuccess) return e;
-  h->allocs.push_back(q);
-  *p = (T*)q;
-  return hipSuccess;
-}
-
 static int validate_ffn(const ipk_ffn_desc* D) {
   if (!D) return fail(IPK_ERR_INVALID_ARG, "desc is NULL");
   if (D->d_model < 64 || D->d_model % 64 || D->d_model > 16384)
@@ -559,16 +550,16 @@ extern "C" int ipk_ffn_create(const ipk_ffn_desc* desc, ipk_ffn_t** out) {
   int32_t* g = nullptr;
   int64_t* c = nullptr;
   int8_t* stage = nullptr;
-  chk(ffn_alloc(h, &h->w1, f * d));
-  chk(ffn_alloc(h, &h->w2, d * f));
-  chk(ffn_alloc(h, &h->scale1, f));
-  chk(ffn_alloc(h, &h->scale2, d));
-  chk(ffn_alloc(h, &h->swtab, 256));
-  chk(ffn_alloc(h, &h->x, R * d));
-  chk(ffn_alloc(h, &h->o, R * f));
-  chk(ffn_alloc(h, &g, d));
-  chk(ffn_alloc(h, &c, d));
-  chk(ffn_alloc(h, &stage, f * d));
+  chk(dev_alloc(h, &h->w1, f * d));
+  chk(dev_alloc(h, &h->w2, d * f));
+  chk(dev_alloc(h, &h->scale1, f));
+  chk(dev_alloc(h, &h->scale2, d));
+  chk(dev_alloc(h, &h->swtab, 256));
+  chk(dev_alloc(h, &h->x, R * d));
+  chk(dev_alloc(h, &h->o, R * f));
+  chk(dev_alloc(h, &g, d));
+  chk(dev_alloc(h, &c, d));
+  chk(dev_alloc(h, &stage, f * d));
   if (e != hipSuccess) {
     free_ffn(h);
     (void)hipGetLastError();
@@ -677,16 +668,6 @@ static void free_conv(ipk_conv* h) {
   delete h;
 }
 
-template <typename T>
-static hipError_t conv_alloc(ipk_conv* h, T** p, size_t count) {
-  void* q = nullptr;
-  hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 1);
-  if (e != hipSuccess) return e;
-  h->allocs.push_back(q);
-  *p = (T*)q;
-  return hipSuccess;
-}
-
 static __int128 poly_l128(__int128 aq, __int128 q_c, __int128 q_1) {
   const __int128 t = (aq < q_c ? aq : q_c) - q_c;
   return t * t + q_1;
@@ -774,22 +755,22 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   int8_t *wdw = nullptr, *stage = nullptr;
   int32_t *bias = nullptr, *mdw = nullptr, *g = nullptr;
   int64_t* c = nullptr;
-  chk(conv_alloc(h, &h->w_pw1, 2 * d * d));
-  chk(conv_alloc(h, &h->w_pw2, d * d));
-  chk(conv_alloc(h, &h->scale_pw1, 2 * d));
-  chk(conv_alloc(h, &h->scale_pw2, d));
-  chk(conv_alloc(h, &wdw, d * 9));
-  chk(conv_alloc(h, &bias, d));
-  chk(conv_alloc(h, &mdw, d));
-  chk(conv_alloc(h, &g, d));
-  chk(conv_alloc(h, &c, d));
-  chk(conv_alloc(h, &h->x, R * d));
-  chk(conv_alloc(h, &h->u, R * 2 * d));
-  chk(conv_alloc(h, &h->o, R * d));
-  chk(conv_alloc(h, &h->v, R * d));
-  chk(conv_alloc(h, &stage, 2 * d * d));
+  chk(dev_alloc(h, &h->w_pw1, 2 * d * d));
+  chk(dev_alloc(h, &h->w_pw2, d * d));
+  chk(dev_alloc(h, &h->scale_pw1, 2 * d));
+  chk(dev_alloc(h, &h->scale_pw2, d));
+  chk(dev_alloc(h, &wdw, d * 9));
+  chk(dev_alloc(h, &bias, d));
+  chk(dev_alloc(h, &mdw, d));
+  chk(dev_alloc(h, &g, d));
+  chk(dev_alloc(h, &c, d));
+  chk(dev_alloc(h, &h->x, R * d));
+  chk(dev_alloc(h, &h->u, R * 2 * d));
+  chk(dev_alloc(h, &h->o, R * d));
+  chk(dev_alloc(h, &h->v, R * d));
+  chk(dev_alloc(h, &stage, 2 * d * d));
   int8_t* sw16 = nullptr;
-  chk(conv_alloc(h, &sw16, 65535));
+  chk(dev_alloc(h, &sw16, 65535));
   if (e != hipSuccess) {
     free_conv(h);
     (void)hipGetLastError();

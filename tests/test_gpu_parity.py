@@ -239,3 +239,58 @@ def test_degenerate_score_scales(gpu_lib, which, score_path):
     if which == "no_scores":
         blk.consts["m_c"] = 0
     _check_block(gpu_lib, blk, f"degenerate {which}")
+
+
+def test_graph_capture_replays_match_eager(gpu_lib):
+    """One block call captured in a HIP graph (the run enqueues kernels only: no
+    allocation, copy or memset) and replayed several times, with eager work on the same
+    buffers between the replays: every replay equals the eager result."""
+    import torch
+
+    ipk = gpu_lib
+    blk = make_workload("parakeet", "calibrated").blocks[0]
+    mod = ipk.RelPosAttn.from_block(blk)
+    x = torch.from_numpy(blk.x).cuda()
+    pe = torch.from_numpy(blk.pos_table).cuda()
+    y_eager = mod(x, pe, lengths=blk.lengths).clone()
+    torch.cuda.synchronize()
+    y = torch.empty_like(x)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        mod(x, pe, lengths=blk.lengths, y=y)
+    other = torch.from_numpy(np.ascontiguousarray(blk.x[:, ::-1])).cuda()
+    for k in range(4):
+        y.fill_(k + 1)
+        mod(other, pe, lengths=blk.lengths)  # eager work on the same handle between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), k
+    ref = core.relpos_attn(blk)
+    assert _first_mismatch(y.cpu().numpy(), ref) is None
+    del graph
+    mod.close()
+
+
+def test_two_handles_on_two_streams(gpu_lib):
+    """Two handles running at once on two streams (default priority) each match the
+    oracle: a handle's workspace is its own."""
+    import torch
+
+    ipk = gpu_lib
+    blks = [make_workload("batched", "calibrated", seed=s, B=2).blocks[0] for s in (31, 32)]
+    mods = [ipk.RelPosAttn.from_block(b) for b in blks]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ins = [(torch.from_numpy(b.x).cuda(), torch.from_numpy(b.pos_table).cuda()) for b in blks]
+    torch.cuda.synchronize()
+    outs = []
+    for m, b, (x, pe), st in zip(mods, blks, ins, streams):
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                y = m(x, pe, lengths=b.lengths, stream=st)
+        outs.append(y)
+    torch.cuda.synchronize()
+    for b, y in zip(blks, outs):
+        ref = core.relpos_attn(b)
+        assert _first_mismatch(y.cpu().numpy(), ref) is None
+    for m in mods:
+        m.close()
