@@ -331,3 +331,14 @@ def test_generated_module_constants_pass_validation_ranges():
                 t = np.minimum(av, cv.sw_qc) - cv.sw_qc
                 q = np.abs(-(av * (t * t + cv.sw_q1) + v * cv.sw_q1))
                 assert int(q.max()) * cv.m_sw + (1 << (cv.shift_sw - 1)) < (1 << 62)
+
+
+def test_create_rejects_max_T_beyond_the_score_rows():
+    """The attention core keeps every score row of a workgroup on chip: the longest
+    supported utterance is 3968 frames (62 chunks of 64) for d_k 64 and 128; one frame
+    more is IPK_ERR_UNSUPPORTED before any device call."""
+    for dk, H in ((64, 4), (128, 2)):
+        d, keep = _valid_desc()
+        d.d_k, d.n_heads, d.max_T = dk, H, 3969
+        assert _create_status(d) == ipk.IPK_ERR_UNSUPPORTED
+        assert "on-chip score rows" in ipk.last_error()
