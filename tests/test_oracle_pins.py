@@ -210,6 +210,39 @@ def test_minimax_swish_matches_table3():
     assert round(swish.sup_error(swish.sw, swish.hard_swish), 3) == g["maxerr_hard_swish"]
 
 
+def _fit(loss, start):
+    from scipy.optimize import minimize
+
+    r = minimize(loss, start, method="Nelder-Mead", options={"xatol": 1e-8, "fatol": 1e-14, "maxiter": 4000})
+    return r.x
+
+
+def test_table3_other_fits_reproduce_their_max_errors():
+    """Table 3's other three fits of Eq. 12's polynomial, solved here, give the Swish
+    output errors the table prints: the least-squares fit to the Swish output, and the
+    minimax and least-squares fits to tanh.  The minimax fit to tanh is the pair the
+    GLU's sigmoid uses, so this pins that pair against the paper too."""
+    g = _golden("paper_constants.txt")
+    x = np.linspace(-20.0, 20.0, 200001)
+    sw = swish.sw(x)
+
+    def sw_err(a, c):
+        return float(np.max(np.abs(swish.sw_hat(x, a, c) - sw)))
+
+    xs = np.linspace(-8.0, 8.0, 80001)
+    sws = swish.sw(xs)
+    a2, c2 = _fit(lambda p: np.mean((swish.sw_hat(xs, p[0], p[1]) - sws) ** 2), [-0.15, 2.4])
+    assert round(sw_err(a2, c2), 3) == g["maxerr_l2_swish"]
+    u = np.linspace(0.0, 6.0, 60001)
+    t = np.tanh(u)
+    ai, ci = _fit(lambda p: np.max(np.abs(p[0] * (np.minimum(u, p[1]) - p[1]) ** 2 + 1 - t)), [-0.25, 2.0])
+    assert round(sw_err(ai, ci), 3) == g["maxerr_linf_tanh"]
+    assert abs(ai - generate.SIGMOID_A) < 2e-4 and abs(ci - generate.SIGMOID_C) < 2e-4
+    assert round(sw_err(generate.SIGMOID_A, generate.SIGMOID_C), 3) == g["maxerr_linf_tanh"]
+    al, cl = _fit(lambda p: np.mean((p[0] * (np.minimum(u, p[1]) - p[1]) ** 2 + 1 - t) ** 2), [-0.25, 2.0])
+    assert round(sw_err(al, cl), 3) == g["maxerr_l2_tanh"]
+
+
 def test_minimax_swish_is_a_local_optimum_of_eq13():
     # Moving (a, c) off the printed optimum can only raise the max error (Eq. 13)
     base = swish.sup_error(swish.sw, swish.sw_hat)
