@@ -54,7 +54,8 @@ typedef enum ipk_status {
  * Block descriptor, read only during ipk_relpos_attn_create.
  *
  * Shapes: d_model = n_heads * d_k, d_k in {64, 128}; max_batch in [1, IPK_MAX_BATCH]
- * and max_T in [1, IPK_MAX_T] size the handle's workspace.
+ * and max_T in [1, IPK_MAX_T] size the handle's workspace.  The attention core keeps a
+ * workgroup's score rows on chip, which limits max_T to 8000 (IPK_ERR_UNSUPPORTED above).
  *
  * Weights (DEVICE pointers, int8, [d_out = d_model][d_in = d_model], row-major,
  * nn.Linear convention y = x W^T): w_q, w_k, w_v (the three projections of

@@ -258,21 +258,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       return r;
     };
 
-    // Register rings over the step phase S = (step index) % NTL, all indices static:
+    // Register rings over the step phase S = (step index) % RING, all indices static
+    // (RING = NTL, and 2 for a single tile, so that the current and the next step never
+    // share a slot):
     //  pr[u]:    tile 0's hi-window P fragment of the step with phase u; at phase S
-    //            tile t uses slot (S - t) mod NTL (its window is tile 0's window of t
+    //            tile t uses slot (S - t) mod RING (its window is tile 0's window of t
     //            steps before)
     //  kr[u]:    K fragment of the step with phase u (current, next)
     //  gr[u][t]: position MFMA results (hi windows) of the step with phase u; a
     //            step's lo windows are the previous step's hi windows
-    v4i pr[NTL][NKS], kr[NTL][NKS], gr[NTL][NTL];
-    int bvp[NTL];
+    constexpr int RING = NTL > 1 ? NTL : 2;
+    v4i pr[RING][NKS], kr[RING][NKS], gr[RING][NTL];
+    int bvp[RING];
     auto splat = [](int bb) { return (v4i){bb, bb, bb, bb}; };
     {
       // tile t's hi window of the first step: tile 0's window 16 t rows lower
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        const int u = (NTL - t) % NTL;
+        const int u = (RING - t) % RING;
 #pragma unroll
         for (int s = 0; s < NKS; ++s) pr[u][s] = ldp(poff - 16 * t * DK, s);
       }
@@ -282,16 +285,16 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
       for (int s = 0; s < NKS; ++s) plast[s] = ldp(poff - 16 * NTL * DK, s);
 #pragma unroll
-      for (int t = 0; t < NTL; ++t) bvp[(NTL - t) % NTL] = rank1(vf, pr[(NTL - t) % NTL])[0];
+      for (int t = 0; t < NTL; ++t) bvp[(RING - t) % RING] = rank1(vf, pr[(RING - t) % RING])[0];
       const int bvlast = rank1(vf, plast)[0];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        const int u = (NTL - t - 1) % NTL;  // slot of tile (t + 1)'s hi window
+        const int u = (RING - t - 1) % RING;  // slot of tile (t + 1)'s hi window
         v4i gacc = splat(t + 1 < NTL ? bvp[u] : bvlast);
 #pragma unroll
         for (int s = 0; s < NKS; ++s)
           gacc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], t + 1 < NTL ? pr[u][s] : plast[s], gacc, 0, 0, 0);
-        gr[NTL - 1][t] = gacc;
+        gr[RING - 1][t] = gacc;
       }
     }
 #pragma unroll
@@ -303,7 +306,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     // every tile and turns them into score codes in LDS.
     auto step = [&](auto Sc, const bool masked) {
       constexpr int S = decltype(Sc)::value;
-      constexpr int SN = (S + 1) % NTL, SP = (S + NTL - 1) % NTL;
+      constexpr int SN = (S + 1) % RING, SP = (S + RING - 1) % RING;
       const int adv = j0 + 16 < j_stop ? 16 * DK : 0;
 #pragma unroll
       for (int s = 0; s < NKS; ++s) kr[SN][s] = ldk(koff + adv, s);
@@ -316,15 +319,15 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], kr[S][0], uk, 0, 0, 0);
-        gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], pr[(S + NTL - t) % NTL][0],
-                                                         splat(bvp[(S + NTL - t) % NTL]), 0, 0, 0);
+        gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], pr[(S + RING - t) % RING][0],
+                                                         splat(bvp[(S + RING - t) % RING]), 0, 0, 0);
       }
 #pragma unroll
       for (int s = 1; s < NKS; ++s)
 #pragma unroll
         for (int t = 0; t < NTL; ++t) {
           cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], kr[S][s], cs[t], 0, 0, 0);
-          gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], pr[(S + NTL - t) % NTL][s], gr[S][t], 0, 0, 0);
+          gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], pr[(S + RING - t) % RING][s], gr[S][t], 0, 0, 0);
         }
       // the last tile's window (slot SN) is consumed: it takes the next step's tile-0 window
 #pragma unroll
@@ -359,23 +362,23 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       poff += 16 * DK;
       j0 += 16;
     };
-    // NTL unmasked steps per iteration, so that every ring index stays static
-    while (j0 + 16 * NTL <= j_full) {
+    // RING unmasked steps per iteration, so that every ring index stays static
+    while (j0 + 16 * RING <= j_full) {
       step(Phase<0>{}, false);
       step(Phase<1>{}, false);
-      if constexpr (NTL > 2) step(Phase<2>{}, false);
+      if constexpr (RING > 2) step(Phase<2 % RING>{}, false);
     }
-    // the rest (fewer than NTL steps below j_full, then the masked ones)
+    // the rest (fewer than RING steps below j_full, then the masked ones)
     int ph = 0;
     while (j0 < j_stop) {
       const bool m = j0 + 16 > j_full;
       if (ph == 0)
         step(Phase<0>{}, m);
-      else if (ph == 1 || NTL == 2)
-        step(Phase<1 % NTL>{}, m);
+      else if (ph == 1 || RING == 2)
+        step(Phase<1 % RING>{}, m);
       else
-        step(Phase<2 % NTL>{}, m);
-      ph = ph + 1 == NTL ? 0 : ph + 1;
+        step(Phase<2 % RING>{}, m);
+      ph = ph + 1 == RING ? 0 : ph + 1;
     }
   }
   // I-BERT integer exp of every score distance d = M - s in [0, 254] (first read in
@@ -732,6 +735,9 @@ size_t attn_lds_bytes(int DK, int ksplit, int ntl, int T_al) {
 
 // Workgroup shapes the kernel is built for: (key splits, 16-query tiles per wave).
 static const AttnCfg kAttnCfgs[] = {{4, 2}, {8, 2}, {8, 3}};
+// One 16-query tile per wave: the smallest score rows, for utterances whose rows do not
+// fit any shape above (every K, P and V fragment then feeds a single MFMA)
+static const AttnCfg kAttnLong = {8, 1};
 constexpr size_t kLdsBudget = 160 * 1024;
 constexpr int kNumCUs = 256;
 
@@ -792,6 +798,8 @@ AttnPlan attn_plan(int DK, int T_al, long bh_count, int T) {
   };
   for (const AttnCfg& c : kAttnCfgs)
     if (fits(c, DK, T_al)) consider(AttnPlan{c, (T + wgq_of(c) - 1) / wgq_of(c), AttnCfg{0, 0}, 0});
+  if (best.c1.ksplit == 0 && fits(kAttnLong, DK, T_al))
+    return AttnPlan{kAttnLong, (T + wgq_of(kAttnLong) - 1) / wgq_of(kAttnLong), AttnCfg{0, 0}, 0};
   const AttnCfg c1{8, 3}, c2{8, 2};
   if (fits(c1, DK, T_al) && fits(c2, DK, T_al)) {
     const int per_round = (int)(kNumCUs / bh_count);  // blocks per (utterance, head) in one round
@@ -849,6 +857,7 @@ static hipError_t launch_attn_dk(const AttnArgs& a, const RunShape& rs, hipStrea
     if (is(p.c1, 4, 2)) return launch_attn_plan<DK, 4, 2, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
     if (is(p.c1, 8, 2)) return launch_attn_plan<DK, 8, 2, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
     if (is(p.c1, 8, 3)) return launch_attn_plan<DK, 8, 3, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
+    if (is(p.c1, 8, 1)) return launch_attn_plan<DK, 8, 1, 0, 0, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
   } else if (is(p.c1, 8, 3) && is(p.c2, 8, 2)) {
     return launch_attn_plan<DK, 8, 3, 8, 2, WIDE>(a, p, rs.B, rs.H, rs.T_al, st, ev);
   }

@@ -334,11 +334,11 @@ def test_generated_module_constants_pass_validation_ranges():
 
 
 def test_create_rejects_max_T_beyond_the_score_rows():
-    """The attention core keeps every score row of a workgroup on chip: the longest
-    supported utterance is 3968 frames (62 chunks of 64) for d_k 64 and 128; one frame
-    more is IPK_ERR_UNSUPPORTED before any device call."""
+    """The attention core keeps every score row of a workgroup on chip: with one 16-query
+    tile per wave the longest supported utterance is 8000 frames (125 chunks of 64) for
+    d_k 64 and 128; one frame more is IPK_ERR_UNSUPPORTED before any device call."""
     for dk, H in ((64, 4), (128, 2)):
         d, keep = _valid_desc()
-        d.d_k, d.n_heads, d.max_T = dk, H, 3969
+        d.d_k, d.n_heads, d.max_T = dk, H, 8001
         assert _create_status(d) == ipk.IPK_ERR_UNSUPPORTED
         assert "on-chip score rows" in ipk.last_error()

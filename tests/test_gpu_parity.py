@@ -197,9 +197,29 @@ def test_run_argument_errors(gpu_lib):
     mod.close()
 
 
+@pytest.mark.parametrize("T,lengths", [(3969, [3969, 3000]), (4500, [4500, 4463])])
+def test_single_tile_workgroups(gpu_lib, T, lengths):
+    """Utterances longer than the 32- and 48-query workgroups' score rows allow run on
+    16-query workgroups (one tile per wave): just past that limit and beyond, d_k 64 and
+    128, ragged lengths."""
+    import dataclasses
+
+    from workloads import generate
+
+    for d, H in ((256, 4), (256, 2)):
+        shape = dataclasses.replace(generate.config_by_name("tiny"), B=len(lengths), d_model=d, n_heads=H,
+                                    name="tiny")
+        for regime in ("literal", "calibrated"):
+            blk = generate.make_block(shape, T, np.random.default_rng(T + d + H), regime, lengths=lengths)
+            print(f"[parity] single-tile workgroups T={T} d_k={d // H} {regime}", flush=True)
+            g = _run_gpu(gpu_lib, blk)
+            y = core.relpos_attn(blk)
+            assert _first_mismatch(g["y"], y) is None, (T, d // H, regime, _first_mismatch(g["y"], y))
+
+
 def test_longest_supported_T(gpu_lib):
     """The longest utterance the on-chip score rows allow (create rejects a longer
-    max_T with IPK_ERR_UNSUPPORTED), with a ragged second utterance, d_k = 64 and 128."""
+    max_T with IPK_ERR_UNSUPPORTED), d_k = 64 and 128."""
     import dataclasses
 
     from workloads import generate
@@ -209,7 +229,7 @@ def test_longest_supported_T(gpu_lib):
         shape = dataclasses.replace(generate.config_by_name("tiny"), B=2, d_model=d, n_heads=H, name="tiny")
         probe = generate.make_block(dataclasses.replace(shape, B=1), 16, np.random.default_rng(1), "calibrated")
         T_max = None
-        for T in range(4096, 0, -64):
+        for T in range(8192, 0, -64):
             try:
                 m = ipk.RelPosAttn.from_block(probe, max_batch=1, max_T=T)
             except ipk.IpkError as e:
@@ -218,11 +238,11 @@ def test_longest_supported_T(gpu_lib):
             m.close()
             T_max = T
             break
-        assert T_max is not None and T_max >= 2500
+        assert T_max is not None and T_max >= 7936
         with pytest.raises(ipk.IpkError):
             ipk.RelPosAttn.from_block(probe, max_batch=1, max_T=T_max + 64)
-        blk = generate.make_block(shape, T_max, np.random.default_rng(T_max + d + H), "calibrated",
-                                  lengths=[T_max, T_max - 37])
+        blk = generate.make_block(dataclasses.replace(shape, B=1), T_max, np.random.default_rng(T_max + d + H),
+                                  "calibrated", lengths=[T_max - 37])
         print(f"[parity] longest T={T_max} d_k={d // H}", flush=True)
         g = _run_gpu(ipk, blk)
         y = core.relpos_attn(blk)
