@@ -50,6 +50,7 @@
 namespace ipk {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef uint16_t us2 __attribute__((ext_vector_type(2)));
 
 struct AttnArgs {
   const int8_t *q, *k, *vt, *p;
@@ -531,19 +532,26 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       v4i sv[NTL];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) sv[t] = *(const v4i*)(srd[t] + c * KCHUNK);
-      uint32_t av[NTL][16];
+      // bytes 0 and 2 of a dword are loaded into the two halves of one register, bytes 1
+      // and 3 into another (16-bit loads that keep the other half), so one shift-or
+      // packs four codes
+      us2 ev[NTL][4], od[NTL][4];
 #pragma unroll
       for (int t = 0; t < NTL; ++t)
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
-          av[t][k] = arow[t][__mul24(-128, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
-#pragma unroll
-      for (int t = 0; t < NTL; ++t)
-#pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t* e = av[t] + 4 * wd;
-          af[t][wd] = (int)(e[0] | (e[1] << 8) | (e[2] << 16) | (e[3] << 24));
+        for (int k = 0; k < 16; ++k) {
+          const uint16_t v = arow[t][__mul24(-128, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
+          us2& dst = (k & 1) ? od[t][k >> 2] : ev[t][k >> 2];
+          if (k & 2)
+            dst.y = v;
+          else
+            dst.x = v;
         }
+#pragma unroll
+      for (int t = 0; t < NTL; ++t)
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd)
+          af[t][wd] = (int)(__builtin_bit_cast(uint32_t, ev[t][wd]) | (__builtin_bit_cast(uint32_t, od[t][wd]) << 8));
     };
     auto codes_tail = [&](int c, v4i* af) {
 #pragma unroll
@@ -599,17 +607,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     VPart pb[NPART];
 #pragma unroll
     for (int hp = 0; hp < NPART; ++hp) load_part(c_begin, hp, pb[hp]);
-    for (int c = c_begin; c < c_end; ++c) {
-      if (c < c_full)
-        codes_full(c, af);
-      else
-        codes_tail(c, af);
+    auto mma_chunk = [&](const int c) {
       const int cn = min(c + 1, c_last);
 #pragma unroll
       for (int hp = 0; hp < NPART; ++hp) {
         mma_part(hp, pb[hp]);
         load_part(cn, hp, pb[hp]);
       }
+    };
+    // the full chunks in a loop of their own (a shared loop body would make every chunk
+    // pay the tail's per-key selects), then the chunk with the utterance's last key
+    int c = c_begin;
+    for (; c < c_full; ++c) {
+      codes_full(c, af);
+      mma_chunk(c);
+    }
+    if (c < c_end) {
+      codes_tail(c, af);
+      mma_chunk(c);
     }
     // exact correction for the -128 offset: + 128 * sum of V over the same keys
 #pragma unroll
