@@ -23,10 +23,10 @@
 //              integers when the descriptor bounds |m_c c + m_p p| below 2^31,
 //              otherwise in float64 (every intermediate is an integer below 2^53).
 //              Scores are kept as biased codes s + 128 in [1, 255].
-//  * the four scores a lane holds (four queries, one key) are packed into a
-//    dword and transposed inside each lane quad with DPP, so every lane stores
-//    four keys of one query with one ds_write_b32: the int8 score rows of the
-//    workgroup stay in LDS, never in HBM.
+//  * each of the four scores a lane holds (four queries, one key) is stored as
+//    one byte of its query's score row (ds_write_b8 of the code's byte; packing
+//    and transposing them first cost more than it saved): the int8 score rows of
+//    the workgroup stay in LDS, never in HBM.
 // Phase 2: row max (shuffles + LDS across the KSPLIT waves), I-BERT integer exp
 // of every distance d = max - s from a table, row sums, F = floor(2^32 / sum).
 // Phase 3: per-row tables of the softmax code a = min(floor(e F / 2^24), 255),

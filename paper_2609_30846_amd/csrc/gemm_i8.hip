@@ -11,8 +11,8 @@
 // cache line.  The weights are stored in MFMA operand-fragment order (each 32-channel x
 // 32-byte fragment a contiguous 1 KB block in lane order), so every wave loads its own
 // weight fragments straight into registers with fully coalesced 16-byte loads, one K
-// step ahead.  The token tile is fetched into registers one step ahead and staged in
-// LDS, whose rows are 128 bytes with the eight 16-byte chunks XOR-swizzled by the row
+// step ahead.  The token tile is fetched into registers one step ahead (two for the
+// small output-projection tiles) and staged in LDS, whose rows are 128 bytes with the eight 16-byte chunks XOR-swizzled by the row
 // index, which keeps both the 16-byte stores of the fetch and the 16-byte MFMA operand
 // reads free of bank conflicts.
 //

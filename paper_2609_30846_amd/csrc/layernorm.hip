@@ -1,5 +1,6 @@
-// Integer LayerNorm of the MHSA module (Eq. 2: the module normalizes its input before
-// the attention block; the paper takes LayerNorm's integer form from I-BERT).
+// Integer LayerNorm of the Conformer block (Eq. 1 - 4: every module normalizes its input
+// first, and the block ends with one; the paper takes LayerNorm's integer form from
+// I-BERT).
 //
 // For a row z of d int8 values:
 //   mu    = floor((2 sum z + d) / (2 d))                 mean, ties up
