@@ -10,21 +10,25 @@
 // Every product fits 64 bits: the host proves |a sigma| m_glu and |swish(v)| m_sw below
 // 2^62 for every int8 pair and every int16 v before it accepts the constants.
 //
-// One thread per channel, a workgroup per (utterance, 256 channels, 16 frames): the
-// thread computes the GLU of its channel over the 24 frames the window needs, in
-// registers, then slides the 9 taps over them.  The GLU's sigmoid of every int8 input
+// One thread per channel, a workgroup per (utterance, 256 channels, 8 frames): the
+// thread computes the GLU of its channel over the 16 frames the window needs, in
+// registers, then slides the 9 taps over them.  The kernel is bound by the latency of
+// its byte-wide loads and stores, not by its arithmetic, so short tiles pay: 8 frames
+// (twice the GLU work of the window's halo) ran the module 8 % faster than 16, and
+// 4 or 32 frames slower.  The GLU's sigmoid of every int8 input
 // sits in LDS (256 values, computed by the workgroup), and the Swish of every int16
 // value and its requantization in a 64 KB table computed once per handle
 // (`swish16_table`), so an output costs its nine multiply-adds, one requantization
 // and one table load.  Loads and stores of a frame are 256 consecutive elements across
-// the workgroup.  Per frame and channel the kernel moves 2 bytes of PW1's output in and
-// 3 bytes out (the int8 Swish output and the int16 BatchNorm output).
+// the workgroup.  Per frame and channel the kernel reads 2 bytes of PW1's output (each
+// twice, with the halo) and writes 3 (the int8 Swish output and the int16 BatchNorm
+// output).
 #include "ipk_internal.h"
 
 namespace ipk {
 
 constexpr int CONV_TAPS = 9, CONV_HALF = 4;
-constexpr int CONV_FRAMES = 16;   // output frames per workgroup (the window: 24 frames in registers)
+constexpr int CONV_FRAMES = 8;    // output frames per workgroup (the window: 16 frames in registers)
 constexpr int CONV_CH = 256;      // channels per workgroup (one per thread)
 constexpr int CONV_WIN = CONV_FRAMES + 2 * CONV_HALF;
 
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(CONV_CH) void conv_glu_dw_swish(ConvArgs a) {
   if (c >= d) return;
   const int L = a.lens.len[b];
   const int8_t* ub = a.u + (size_t)b * T * 2 * d + c;
-  // GLU over the window t0 - 4 .. t0 + 19, in registers (static indices)
+  // GLU over the window t0 - 4 .. t0 + 11, in registers (static indices)
   int g[CONV_WIN];
 #pragma unroll
   for (int f = 0; f < CONV_WIN; ++f) {

@@ -49,8 +49,8 @@ def test_conv_configs(gpu_lib, name, regime):
     _check(gpu_lib, cv, blk.x, blk.lengths, f"{name}/{regime}")
 
 
-# (B, T, d, lengths): a single frame, frames fewer than the taps, time tiles of 64
-# frames crossed with the window reaching into the next tile, ragged lengths, d not a
+# (B, T, d, lengths): a single frame, frames fewer than the taps, many 8-frame time
+# tiles with the window reaching into the neighbouring ones, ragged lengths, d not a
 # multiple of the 256-channel workgroup
 RAGGED = [
     (1, 1, 256, None),
