@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define IPK_ABI_VERSION 2
+#define IPK_ABI_VERSION 3
 
 /* Status codes. */
 typedef enum ipk_status {
@@ -160,6 +160,21 @@ int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst,
  */
 enum { IPK_NUM_STAGES = 3 };
 int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
+
+/*
+ * How the attention core evaluates the fused score of Eq. 11.  Both paths are exact
+ * integer arithmetic and give the same bytes.  IPK_SCORE_AUTO (what create selects)
+ * takes 32-bit multiply-adds when create proves m_c |c| + m_p |p| plus the rounding and
+ * code bias below 2^31 for every possible score (|c|, |p| <= d_k 255 127), and 64-bit
+ * ones otherwise; IPK_SCORE_WIDE forces the 64-bit path, so that tests can exercise it on
+ * descriptors that would take the 32-bit one.  Takes effect from the next run.
+ * ipk_relpos_attn_score_path returns the path the next run takes (IPK_SCORE_NARROW or
+ * IPK_SCORE_WIDE), or a negative status.
+ * Errors: IPK_ERR_INVALID_ARG (null handle, unknown path).
+ */
+enum { IPK_SCORE_AUTO = 0, IPK_SCORE_WIDE = 1, IPK_SCORE_NARROW = 2 };
+int ipk_relpos_attn_set_score_path(ipk_relpos_attn_t* h, int32_t path);
+int ipk_relpos_attn_score_path(const ipk_relpos_attn_t* h);
 
 /*
  * Position projection kept on the handle (Sec. 3.1: q_P depends only on the

@@ -1,45 +1,46 @@
 // Relative-position attention core of the integer MHSA block (Sec. 3.1).
 //
 // Work split: a workgroup of ATTN_WAVES waves owns (utterance b, head h, WGQ
-// consecutive queries).  Each wave owns NTL 16-query MFMA tiles (32 or 48 queries:
-// every K, P and V fragment it loads feeds NTL MFMAs, and the loads bound the
-// kernel); KSPLIT waves share one set of queries and split its keys: phase 1 in
-// 16-key steps, phases 2 and 3 in 64-key chunks (scores are exchanged through LDS in
-// between).  The host picks (KSPLIT, NTL) per launch from the LDS the score rows need
-// and the rounds of workgroups over the CUs.
+// consecutive queries).  Its int8 score rows stay in LDS (never in HBM), laid out in
+// 16-key blocks: block j/16 holds the WGQ rows' 16 scores of those keys, 16 bytes per
+// row, so the row of query r and key j sits at byte (j/16) WGQ 16 + 16 r + j % 16.
+// The host picks the workgroup shape per launch from the LDS the rows need and the
+// rounds of workgroups over the CUs.
 //
-// Phase 1, per 16-key step, with v_mfma_i32_16x16x64_i8 (queries on MFMA rows):
+// Phase 1 (scores), per 16-key step, with v_mfma_i32_16x16x64_i8 (queries on MFMA
+// rows).  KSPLIT waves share a query set of NTL 16-query tiles (every K and P fragment
+// a wave loads feeds NTL MFMAs) and split its keys:
 //  * content   c = Q K^T, accumulator seeded with the rank-1 term u.K_j
-//  * position  G = Q P_win^T, seeded with v.P_r, for the 16 table rows that
-//              start at relative position j0-i0+T-1 ("hi" window).  The rows
-//              just before it ("lo") are the previous step's hi window, and tile t
-//              reuses the P fragment tile 0 loaded t steps earlier, so each step
-//              loads one new P fragment and runs one new position MFMA pair per
-//              tile.
-//  * Phi       p_ij = G_i(j-i+T-1) is a rotation by the row index inside each
-//              16-lane row group: every source lane picks the window its value
-//              belongs to and ds_bpermute moves it to the lane of its key.
-//  * Eq. 11    s = clamp8(RS(m_c c + m_p p, 1, n)), exact: in 32-bit
-//              integers when the descriptor bounds |m_c c + m_p p| below 2^31,
-//              otherwise in float64 (every intermediate is an integer below 2^53).
-//              Scores are kept as biased codes s + 128 in [1, 255].
-//  * each of the four scores a lane holds (four queries, one key) is stored as
-//    one byte of its query's score row (ds_write_b8 of the code's byte; packing
-//    and transposing them first cost more than it saved): the int8 score rows of
-//    the workgroup stay in LDS, never in HBM.
-// Phase 2: row max (shuffles + LDS across the KSPLIT waves), I-BERT integer exp
-// of every distance d = max - s from a table, row sums, F = floor(2^32 / sum).
-// Phase 3: per-row tables of the softmax code a = min(floor(e F / 2^24), 255),
-// stored as a - 128; A.V on MFMA with that signed operand plus the exact
-// correction 128 * sum_j V_j over the same keys (per-chunk sums of V, fetched
-// with the V fragments; V is streamed in parts of four 16-channel tiles); partial
-// contexts of the KSPLIT waves are added with LDS atomics (exact int32) and
-// requantized with (m_o, shift_o) by all waves together.
-// Both lookup tables are laid out [d][32 banks] in dwords: the exp table holds one
-// copy per bank (lane l reads copy l % 32); the code tables hold bytes, row r = 16 tt
-// + rr in byte tt of banks rr and rr + 16, and the two half-waves' lanes g = 0, 1 (2,
-// 3) read different copies, so a lookup is one multiply-add and one conflict-free
-// LDS read.
+//  * position  G = Q P_win^T, seeded with v.P_r, for the 16 table rows that start at
+//              relative position j0-i0+T-1 ("hi" window).  The rows just before it
+//              ("lo") are the previous step's hi window, and tile t reuses the P
+//              fragment tile 0 loaded t steps earlier, so each step loads one new P
+//              fragment and runs one new position MFMA pair per tile.
+//  * Phi       p_ij = G_i(j-i+T-1) is a rotation by the row index inside each 16-lane
+//              row group: every source lane picks the window its value belongs to and
+//              ds_bpermute moves it to the lane of its key.
+//  * Eq. 11    s = clamp8(RS(m_c c + m_p p, 1, n)), exact: in 32-bit integers when
+//              the descriptor bounds |m_c c + m_p p| below 2^31, otherwise in 64-bit
+//              integers.  Scores are kept as biased codes s + 128 in [1, 255].
+//  * each score byte is stored straight into its row's block (one address add per
+//    step: the tile and row offsets are instruction immediates).
+// Phase 2 (row sums): row max over the key splits (LDS); every lane then reads 16
+// scores of one row (16 bytes), forms the four distances d = M - s of each dword with
+// one subtraction (every s <= M, so no byte borrows), and looks up the I-BERT integer
+// exp of each d in a table with one copy per LDS bank; the address of one lookup is
+// a single v_dot4 (base + 128 d).
+// Conversion: F = floor(2^32 / sum) per row (integer long division), per-row tables of
+// the softmax code a - 128 = min(floor(e F / 2^24), 255) - 128, and every score byte of
+// the workgroup replaced in place by its code (keys past the utterance by -128, i.e.
+// a = 0).
+// Phase 3 (A.V): the waves split the d_k channels (two 16-channel MFMA tiles each) and
+// the keys; with the V^T fragment as the A operand and 16 queries' codes (16 bytes of
+// one row, read straight from its block) as B, each output lane holds four consecutive
+// channels of one query.  The exact correction 128 sum_j V_j for the -128 offset is
+// summed from the V fragments themselves (v_dot4 against ones).  The key parts' int32
+// partial contexts are added in LDS (exact, order-free) and requantized with
+// (m_o, shift_o) in 64-bit integers.
+// No floating-point instruction runs in the kernel.
 #include <mutex>
 #include <type_traits>
 #include <utility>
@@ -50,12 +51,15 @@
 namespace ipk {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef uint16_t us2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) uint8_t lds8;
+typedef __attribute__((address_space(3))) uint32_t lds32;
+typedef __attribute__((address_space(3))) int32_t ldsi32;
+typedef __attribute__((address_space(3))) v4i ldsv4;
 
 struct AttnArgs {
   const int8_t *q, *k, *vt, *p;
-  const int8_t *u, *v;  // [H][d_k]
-  const int32_t* vsum;
+  const int8_t *u, *v;   // [H][d_k]
+  const uint32_t* etab;  // [256]: integer exp of every distance d (0 at d = 255)
   int8_t* ctx;
   Lengths lens;
   int T, T_al, H, d, p_rows, p_base;
@@ -64,23 +68,26 @@ struct AttnArgs {
   // second segment of a two-shape grid: blocks from seg2_block on cover the queries
   // from seg2_q0 on, nqb2 blocks per (utterance, head), with the second shape
   int seg2_block, seg2_q0, nqb2;
-  // fused score: narrow path
-  int32_t mc24, mp24, bias32, post_shift;
-  // fused score: wide path (multipliers scaled by 2^-shift_s)
-  double mcd, mpd;
-  int32_t m_o, shift_o, q_ln2, q_b, q_c;
+  // fused score, 32-bit path: t = mc24 c + mp24 p + bias32, code in bits 16..23
+  int32_t mc24, mp24, bias32;
+  // fused score, 64-bit path: t = m_c c + m_p p + bias64, code = t >> shift_s
+  int32_t m_c, m_p, shift_s;
+  int64_t bias64;
+  int32_t m_o, shift_o;
 };
 
-constexpr int SCORE_PAD = 16;  // bytes added to each LDS score row
 constexpr int TAB_DW = 256 * 32;  // dwords of the [d][32 banks] lookup-table region
+constexpr int ATTN_WAVES = 8;     // waves per workgroup (two per SIMD)
+constexpr int AV_NT = 2;          // 16-channel tiles per wave in phase 3
 
-__device__ __forceinline__ uint32_t iexp_int(int d, int q_ln2, int q_b, int q_c) {
-  // I-BERT integer exp of -d: d = z q_ln2 - r with r in (-q_ln2, 0]
-  const int z = d / q_ln2;
-  const int r = z * q_ln2 - d;
-  const int poly = (r + q_b) * (r + q_b) + q_c;  // < 2^24 (checked at create)
-  return z >= 32 ? 0u : ((uint32_t)poly >> z);
-}
+// Share (out of 256) of a SIMD's work that its older wave takes in phase 1 and in the
+// later phases: the arbiter favours the older wave of a SIMD (the lower index), so with
+// equal shares the younger one finishes long after it.
+constexpr int P1_OLDER = 166;
+constexpr int P3_OLDER = 150;
+
+template <int S>
+using Phase = std::integral_constant<int, S>;
 
 // Low 32 bits of a * b + c for 24-bit signed a, b (v_mad_i32_i24); the addition
 // wraps modulo 2^32.
@@ -88,16 +95,46 @@ __device__ __forceinline__ int mad_i24(int a, int b, int c) {
   return (int)((uint32_t)__mul24(a, b) + (uint32_t)c);
 }
 
-constexpr int ATTN_WAVES = 8;  // waves per workgroup (two per SIMD)
-// Share (out of 256) of a SIMD's keys that its older wave takes in phase 1 and in
-// phases 2 and 3.  With equal shares the younger wave of a pair ends phase 1 about
-// 1.35x and phase 3 about 1.25x later than the older one on the long-form workload;
-// these shares (about 65 % and 59 %) measured fastest over the whole kernel.
-constexpr int P1_OLDER = 166;
-constexpr int P3_OLDER = 150;
+// floor(2^32 / D) for 2 <= D < 2^32 by binary long division (integer only):
+// floor((2^32 - 1) / D), plus one when D divides 2^32 (a power of two).
+__device__ __forceinline__ uint32_t floor_2p32_div(uint32_t D) {
+  uint64_t r = 0;
+  uint32_t q = 0;
+#pragma unroll 4
+  for (int i = 31; i >= 0; --i) {
+    r = (r << 1) | 1u;
+    if (r >= D) {
+      r -= D;
+      q |= 1u << i;
+    }
+  }
+  return q + ((D & (D - 1)) == 0 ? 1u : 0u);
+}
 
-template <int S>
-using Phase = std::integral_constant<int, S>;
+// LDS carve-up of one workgroup shape (the host computes the same sizes).
+struct AttnLds {
+  uint32_t tab, etab, smax, ssum, sF, total;
+};
+__host__ __device__ constexpr AttnLds attn_lds(int wgq, int rows, int T_al) {
+  const uint32_t s = (uint32_t)wgq * (uint32_t)T_al;  // score blocks (a multiple of 16)
+  const uint32_t tab = s;
+  const uint32_t etab = tab + TAB_DW * 4;
+  const uint32_t smax = etab + 256 * 4;
+  const uint32_t ssum = smax + (uint32_t)rows * ATTN_WAVES * 4;
+  const uint32_t sF = ssum + (uint32_t)rows * ATTN_WAVES * 4;
+  return AttnLds{tab, etab, smax, ssum, sF, sF + (uint32_t)wgq * 4};
+}
+
+// Work units [*b, *e) of part `part` of 2 hk parts out of n: the parts come in pairs that
+// share a SIMD (part p and p + hk, the first one older); each pair gets n / hk of the
+// units, of which the older wave takes older / 256 (rounded).
+__device__ __forceinline__ void split_pairs(int n, int older, int hk, int part, int* b, int* e) {
+  const int pair = part % hk, younger = part / hk;
+  const int ps = n * pair / hk, pe = n * (pair + 1) / hk;
+  const int mid = ps + ((pe - ps) * older + 128) / 256;
+  *b = younger ? mid : ps;
+  *e = younger ? pe : mid;
+}
 
 // One workgroup of the core: block `lin` of a segment of nqb query blocks per
 // (utterance, head) that starts at query q_base.
@@ -107,90 +144,81 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets per workgroup
   constexpr int ROWS = 16 * NTL;            // queries per set: NTL 16-query MFMA tiles
   constexpr int WGQ = ROWS * NQS;           // queries per workgroup
+  constexpr int NTILES = WGQ / 16;          // 16-query tiles per workgroup
   constexpr int NKS = DK / 64;              // MFMA K-steps over d_k
-  constexpr int NT = DK / 16;               // 16-channel output tiles of the context
-  static_assert(NQS * NTL <= 4, "the code tables hold four 16-row tiles");
+  constexpr int BLK = WGQ * 16;             // bytes per 16-key block of score rows
+  constexpr int NCG = DK / (16 * AV_NT);    // channel groups of phase 3
+  constexpr int KH = ATTN_WAVES / NCG;      // key parts of phase 3
+  static_assert(NTILES <= 4, "the code tables hold four 16-row tiles");
+  static_assert(KH >= 2 && KH % 2 == 0, "phase-3 wave grid");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in SGPRs
   const int col = lane & 15, g = lane >> 4;
-  // Waves w and w + 4 share SIMD w % 4, whose instruction arbiter favours the older
-  // one (the lower index): given equal work, the younger wave finishes long after it
-  // and runs its tail alone.  The two waves of a SIMD therefore take the same query set
-  // and split its keys unevenly, the older one taking the larger share.
+  // Waves w and w + 4 share SIMD w % 4.  In phase 1 the two waves of a SIMD take the
+  // same query set and split its keys unevenly (the older one the larger share).
   constexpr int HK = KSPLIT > 1 ? KSPLIT / 2 : 1;  // key parts per age class
   const int simd = w & 3, younger = w >> 2;
   const int qset = KSPLIT > 1 ? simd / HK : w;
   const int kpart = KSPLIT > 1 ? younger * HK + simd % HK : 0;
   const int slot = qset * KSPLIT + kpart;  // this wave's row-max and row-sum slot
-  // work units [*b, *e) of this wave out of n: every SIMD gets n / HK of them, of
-  // which its older wave takes older / 256 (rounded) and its younger wave the rest
   auto split = [&](const int n, const int older, int* b, int* e) {
     if (KSPLIT == 1) {
       *b = 0;
       *e = n;
-      return;
+    } else {
+      split_pairs(n, older, HK, kpart, b, e);
     }
-    const int pair = kpart % HK;
-    const int ps = n * pair / HK, pe = n * (pair + 1) / HK;
-    const int mid = ps + ((pe - ps) * older + 128) / 256;
-    *b = younger ? mid : ps;
-    *e = younger ? pe : mid;
   };
   // Workgroups go round-robin to the 8 XCDs (id % 8); when the (utterance, head)
   // pairs divide evenly, every workgroup of one pair is placed on the same XCD so that
   // its K, P and V stay in that XCD's L2.
   int qb, bhi;
   if (a.xcd_group) {
-    const int x = lin & 7, k = lin >> 3, slot = k / nqb;
-    qb = k - slot * nqb;
-    bhi = x + 8 * slot;
+    const int x = lin & 7, k = lin >> 3, s = k / nqb;
+    qb = k - s * nqb;
+    bhi = x + 8 * s;
   } else {
     qb = lin % nqb;
     bhi = lin / nqb;
   }
   const int b = bhi / a.H, h = bhi - (bhi / a.H) * a.H;
   const int wg_q0 = q_base + qb * WGQ;
-  const int q0 = wg_q0 + ROWS * qset;  // first query of this wave
+  const int q0 = wg_q0 + ROWS * qset;  // first query of this wave's set
   const int L = a.lens.len[b];
   const int T = a.T, T_al = a.T_al;
-  const int srow = T_al + SCORE_PAD;
   const int nkc = (L + KCHUNK - 1) / KCHUNK;
   int c_begin, c_end;
   split(nkc, P3_OLDER, &c_begin, &c_end);
   // chunks below c_full hold only valid keys; c_full < c_end only when this wave's
-  // range holds the chunk with the utterance's last key (an empty range past it too
-  // ends at c_full = c_end)
+  // range holds the chunk with the utterance's last key
   const int c_full = max(c_begin, min(c_end, L / KCHUNK));
   const bool active = q0 < L;
 
-  // LDS carve-up (the host computes the same sizes)
-  constexpr int RSTRIDE = DK + 4;  // dwords per row of the key-split partial sums
-  const int s_bytes = WGQ * srow;
-  const int red_bytes = KSPLIT > 1 ? NQS * ROWS * RSTRIDE * 4 : 0;
-  const int big = ((s_bytes > red_bytes ? s_bytes : red_bytes) + 15) & ~15;
-  uint8_t* sbuf = smem;
-  int32_t* red = (int32_t*)smem;  // reused once the scores are consumed
-  // lookup tables, [d][32 banks] in dwords: first the per-bank copies of the exp
-  // table (phase 2), then the code tables (phase 3)
-  uint32_t* tab = (uint32_t*)(smem + big);
-  uint32_t* etab = tab + TAB_DW;  // the 255 exp values, once
-  int32_t* smax = (int32_t*)(etab + 256);
-  uint32_t* ssum = (uint32_t*)(smax + ROWS * ATTN_WAVES);
-  uint32_t* sF = ssum + ROWS * ATTN_WAVES;
+  constexpr AttnLds lay0 = attn_lds(WGQ, ROWS, 0);
+  const uint32_t base = (uint32_t)(uintptr_t)(lds8*)smem;
+  const uint32_t s_bytes = (uint32_t)WGQ * (uint32_t)T_al;
+  const uint32_t TAB = base + s_bytes;                  // [d][32 banks] dwords
+  const uint32_t ETAB = TAB + (lay0.etab - lay0.tab);   // the 256 exp values, once
+  lds32* tab = (lds32*)(uintptr_t)TAB;
+  lds32* etab = (lds32*)(uintptr_t)ETAB;
+  ldsi32* smax = (ldsi32*)(uintptr_t)(TAB + (lay0.smax - lay0.tab));
+  lds32* ssum = (lds32*)(uintptr_t)(TAB + (lay0.ssum - lay0.tab));
+  lds32* sF = (lds32*)(uintptr_t)(TAB + (lay0.sF - lay0.tab));
 
   const size_t bh = (size_t)b * a.H + h;
   const int8_t* Qh = a.q + bh * T_al * DK;
   const int8_t* Kh = a.k + bh * T_al * DK;
   const int8_t* VTh = a.vt + bh * DK * T_al;
   const int8_t* Ph = a.p + (size_t)h * a.p_rows * DK;
-  const int32_t* vs = a.vsum + bh * (size_t)(T_al / KCHUNK) * DK;
-  uint8_t* my_rows = sbuf + (size_t)(ROWS * qset) * srow;
   // this lane's 16 bytes of a 1 KB operand fragment (stored in lane order)
   const int frag_off = lane * 16;
 
   constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
+
+  // the integer exp of this thread's distance, written to LDS after phase 1
+  const uint32_t e_mine = a.etab[tid & 255];
 
   // ---------------- phase 1: fused scores into LDS, running row max
   int mx[NTL][4];
@@ -225,9 +253,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       take_hi[i] = (col + arow) < 16;                    // as a source lane
       src_addr[i] = (g * 16 + ((col - arow) & 15)) * 4;  // as a destination lane
     }
-    // a lane's score of query row 4g + i of tile t and key j0 + col is one byte of
-    // the row: stored directly, so no packing or transposing is spent on it
-    uint8_t* sdst = my_rows + (size_t)(4 * g) * srow + col;
+    // a lane's score of query row 4g + i of tile t and key j0 + col is byte col of that
+    // row's 16 bytes in block j0 / 16: the row and tile offsets are immediates
+    const uint32_t sdst0 = base + (uint32_t)((ROWS * qset + 4 * g) * 16 + col);
 
     // K and the position table are streamed with raw buffer loads: the lane's offset in
     // a fragment is fixed and the step's offset is a scalar, so no vector address
@@ -265,13 +293,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     //  pr[u]:    tile 0's hi-window P fragment of the step with phase u; at phase S
     //            tile t uses slot (S - t) mod RING (its window is tile 0's window of t
     //            steps before)
+    //  bv[u]:    the seed v.P_r of that window (all four rows)
     //  kr[u]:    K fragment of the step with phase u (current, next)
     //  gr[u][t]: position MFMA results (hi windows) of the step with phase u; a
     //            step's lo windows are the previous step's hi windows
     constexpr int RING = NTL > 1 ? NTL : 2;
-    v4i pr[RING][NKS], kr[RING][NKS], gr[RING][NTL];
-    int bvp[RING];
-    auto splat = [](int bb) { return (v4i){bb, bb, bb, bb}; };
+    v4i pr[RING][NKS], kr[RING][NKS], gr[RING][NTL], bv[RING];
     {
       // tile t's hi window of the first step: tile 0's window 16 t rows lower
 #pragma unroll
@@ -286,12 +313,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
       for (int s = 0; s < NKS; ++s) plast[s] = ldp(poff - 16 * NTL * DK, s);
 #pragma unroll
-      for (int t = 0; t < NTL; ++t) bvp[(RING - t) % RING] = rank1(vf, pr[(RING - t) % RING])[0];
-      const int bvlast = rank1(vf, plast)[0];
+      for (int t = 0; t < NTL; ++t) bv[(RING - t) % RING] = rank1(vf, pr[(RING - t) % RING]);
+      const v4i bvlast = rank1(vf, plast);
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         const int u = (RING - t - 1) % RING;  // slot of tile (t + 1)'s hi window
-        v4i gacc = splat(t + 1 < NTL ? bvp[u] : bvlast);
+        v4i gacc = t + 1 < NTL ? bv[u] : bvlast;
 #pragma unroll
         for (int s = 0; s < NKS; ++s)
           gacc = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][s], t + 1 < NTL ? pr[u][s] : plast[s], gacc, 0, 0, 0);
@@ -311,17 +338,16 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       const int adv = j0 + 16 < j_stop ? 16 * DK : 0;
 #pragma unroll
       for (int s = 0; s < NKS; ++s) kr[SN][s] = ldk(koff + adv, s);
-      // seeds: u.K_j of this step's keys (shared by the tiles) and, per tile, v.P_r
-      // of the tile's window (recomputed rather than kept: the matrix pipe has room,
-      // the registers do not)
+      // seeds: u.K_j of this step's keys (shared by the tiles) and v.P_r of this step's
+      // new window (kept with it in the ring)
       const v4i uk = rank1(uf, kr[S]);
-      bvp[S] = rank1(vf, pr[S])[0];
+      bv[S] = rank1(vf, pr[S]);
       v4i cs[NTL];
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         cs[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], kr[S][0], uk, 0, 0, 0);
         gr[S][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(qf[t][0], pr[(S + RING - t) % RING][0],
-                                                         splat(bvp[(S + RING - t) % RING]), 0, 0, 0);
+                                                         bv[(S + RING - t) % RING], 0, 0, 0);
       }
 #pragma unroll
       for (int s = 1; s < NKS; ++s)
@@ -333,10 +359,8 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       // the last tile's window (slot SN) is consumed: it takes the next step's tile-0 window
 #pragma unroll
       for (int s = 0; s < NKS; ++s) pr[SN][s] = ldp(poff + adv, s);
-      // cs holds c0 + u.K_j: the addend is the rounding and code bias alone
-      const int k1 = a.bias32;
-      const double k1d = 128.5;
       const bool key_ok = j0 + col < L;
+      lds8* sp = (lds8*)(uintptr_t)(sdst0 + (uint32_t)(j0 >> 4) * BLK);
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
 #pragma unroll
@@ -345,18 +369,21 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
           const int pt = __builtin_amdgcn_ds_bpermute(src_addr[i], sel);
           int v;
           if (WIDE) {
-            // truncation equals the floor here: every negative value clamps to code 1
-            v = (int)__builtin_fma(a.mcd, (double)cs[t][i], __builtin_fma(a.mpd, (double)pt, k1d));
+            // exact in 64 bits: |m c| + |m p| < 2^47
+            const int64_t tt = (int64_t)a.m_c * cs[t][i] + (int64_t)a.m_p * pt + a.bias64;
+            const int64_t q = tt >> a.shift_s;
+            v = q < 1 ? 1 : (q > 255 ? 255 : (int)q);
           } else {
-            int x = mad_i24(a.mp24, pt, k1);
+            // cs holds c0 + u.K_j: the addend is the rounding and code bias alone
+            int x = mad_i24(a.mp24, pt, a.bias32);
             asm("" : "+v"(x));  // opaque to the optimizer (keeps the multiply-adds apart), not a scheduling barrier
             v = mad_i24(a.mc24, cs[t][i], x);
+            v = min(max(v, LOCODE), HICODE);
           }
-          v = min(max(v, LOCODE), HICODE);
           if (masked && !key_ok) v = LOCODE;
           mx[t][i] = max(mx[t][i], v);
-          // the code is bits 0..7 (wide path) or 16..23 (narrow path) of v
-          sdst[(size_t)(16 * t + i) * srow + j0] = (uint8_t)(WIDE ? v : (v >> 16));
+          // the code is bits 0..7 (64-bit path) or 16..23 (32-bit path) of v
+          sp[(16 * t + i) * 16] = (uint8_t)(WIDE ? v : (v >> 16));
         }
       }
       koff += 16 * DK;
@@ -382,17 +409,15 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       ph = ph + 1 == RING ? 0 : ph + 1;
     }
   }
-  // I-BERT integer exp of every score distance d = M - s in [0, 254] (first read in
-  // phase 2, so waves that finish phase 1 early fill it while the others score): once, and
-  // in 32 per-bank copies (copy (d + c) % 32 of the pass is written by lane d,
-  // which keeps the writes free of bank conflicts)
+  // the integer exp of every distance d in [0, 255): once, and in 32 per-bank copies
+  // (copy (d + c) % 32 of pass c is written by the thread of d, which keeps the writes
+  // free of bank conflicts)
   {
     const int dd = tid & 255;
-    const uint32_t e = dd < 255 ? iexp_int(dd, a.q_ln2, a.q_b, a.q_c) : 0u;
-    if (tid < 256) etab[dd] = e;
+    if (tid < 256) etab[dd] = e_mine;
     for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
 #pragma unroll
-      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e;
+      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e_mine;
     }
   }
 
@@ -414,40 +439,54 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   }
   __syncthreads();
 
-  // phases 2 and 3: lane (g, col) works on query row `col` of each tile and keys
-  // g*16 .. g*16+15 of a chunk
-  int Mrow[NTL];
-  const uint8_t* srd[NTL];
+  // phase 2 and the conversion: lane (g, col) works on row 16 t + col of its set and
+  // keys 16 g .. 16 g + 15 of a 64-key chunk, 16 bytes at
+  // base + (4 c + g) BLK + (ROWS qset + 16 t + col) 16
+  uint32_t Mrep[NTL];
 #pragma unroll
   for (int t = 0; t < NTL; ++t) {
     int m = 1;
 #pragma unroll
     for (int k2 = 0; k2 < KSPLIT; ++k2) m = max(m, smax[(qset * KSPLIT + k2) * ROWS + 16 * t + col]);
-    Mrow[t] = m;
-    srd[t] = my_rows + (size_t)(16 * t + col) * srow + g * 16;
+    Mrep[t] = (uint32_t)m * 0x01010101u;
   }
+  const uint32_t rd0 = base + (uint32_t)(g * BLK + (ROWS * qset + col) * 16);
+  auto chunk_ptr = [&](int c, int t) { return (ldsv4*)(uintptr_t)(rd0 + (uint32_t)c * (4 * BLK) + t * 256); };
 
   // ---------------- phase 2: row sums of the integer exp
-  // lane l reads copy l % 32 of the exp table: e(M - code) at erow[-32 code]
+  // lane l reads copy l % 32 of the exp table: e(d) at TAB + 4 (l % 32) + 128 d
   uint32_t sum[NTL];
 #pragma unroll
   for (int t = 0; t < NTL; ++t) sum[t] = 0u;
   if (active) {
-    const uint32_t* erow[NTL];
+    const uint32_t ebase = TAB + 4u * (uint32_t)(lane & 31);
+    auto e_at = [&](uint32_t dw, int k) {
+      return *(const lds32*)(uintptr_t)__builtin_amdgcn_udot4(dw, 128u << (8 * k), ebase, false);
+    };
+    // the next chunk's scores are read while the current chunk's lookups run
+    v4i svn[NTL];
+    if (c_begin < c_full) {
 #pragma unroll
-    for (int t = 0; t < NTL; ++t) erow[t] = tab + Mrow[t] * 32 + (lane & 31);
+      for (int t = 0; t < NTL; ++t) svn[t] = *chunk_ptr(c_begin, t);
+    }
     for (int c = c_begin; c < c_full; ++c) {
-      // all lookups of the chunk are issued before any is summed (LDS latency
-      // overlaps instead of being paid once per four codes)
       v4i sv[NTL];
+      const int cn = min(c + 1, c_full - 1);
 #pragma unroll
-      for (int t = 0; t < NTL; ++t) sv[t] = *(const v4i*)(srd[t] + c * KCHUNK);
+      for (int t = 0; t < NTL; ++t) {
+        sv[t] = svn[t];
+        svn[t] = *chunk_ptr(cn, t);
+      }
+      // all lookups of the chunk are issued before any is summed
       uint32_t ev[NTL][16];
 #pragma unroll
       for (int t = 0; t < NTL; ++t)
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
-          ev[t][k] = erow[t][__mul24(-32, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
+        for (int wd = 0; wd < 4; ++wd) {
+          const uint32_t dw = Mrep[t] - (uint32_t)sv[t][wd];  // four distances M - s, no borrows
+#pragma unroll
+          for (int k = 0; k < 4; ++k) ev[t][4 * wd + k] = e_at(dw, k);
+        }
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         uint32_t acc_e = 0;
@@ -458,15 +497,19 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
     if (c_full < c_end) {  // the chunk that holds the utterance's last key
       const int c = c_full;
+      const int kb = c * KCHUNK + g * 16;
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        const v4i sv = *(const v4i*)(srd[t] + c * KCHUNK);
+        const v4i sv = *chunk_ptr(c, t);
 #pragma unroll
-        for (int by = 0; by < 16; ++by) {
-          const bool ok = c * KCHUNK + g * 16 + by < L;
-          const int code = ok ? (int)(((uint32_t)sv[by >> 2] >> (8 * (by & 3))) & 0xff) : Mrow[t];
-          const uint32_t e = etab[Mrow[t] - code];
-          sum[t] += ok ? e : 0u;
+        for (int wd = 0; wd < 4; ++wd) {
+          // a byte past the last key may exceed M: its borrow only reaches later keys
+          const uint32_t dw = Mrep[t] - (uint32_t)sv[wd];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t e = e_at(dw, k);
+            sum[t] += kb + 4 * wd + k < L ? e : 0u;
+          }
         }
       }
     }
@@ -481,15 +524,14 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     for (int t = 0; t < NTL; ++t) ssum[slot * ROWS + 16 * t + col] = sum[t];
   }
   __syncthreads();
-  // F = floor(2^32 / sum), one row per thread.  The float64 quotient is correctly
-  // rounded, and 2^32 / sum lies at least 1 / sum below the next integer while its
-  // rounding error is at most 2^32 / sum * 2^-53, so truncating it gives the floor.
+  // F = floor(2^32 / sum), one row per thread; sum >= e(0) >= 2^8 on every row that has
+  // a valid key (rows without one, which are never stored, take F = 0)
   if (tid < WGQ) {
     const int qs = tid / ROWS, rr = tid - qs * ROWS;
     uint32_t tot = 0;
 #pragma unroll
     for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qs * KSPLIT + k2) * ROWS + rr];
-    sF[tid] = tot ? (uint32_t)(4294967296.0 / (double)tot) : 0u;
+    sF[tid] = tot >= 2 ? floor_2p32_div(tot) : 0u;
   }
   __syncthreads();
   // softmax code tables (over the exp copies, which phase 2 has finished with): the
@@ -502,7 +544,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     const uint32_t e8 = etab[dd] << 8;
     uint32_t packed = 0;
 #pragma unroll
-    for (int tt = 0; tt < NQS * NTL; ++tt) {
+    for (int tt = 0; tt < NTILES; ++tt) {
       const uint32_t v = __umulhi(e8, sF[16 * tt + rr]);
       packed |= ((v > 255u ? 255u : v) ^ 0x80u) << (8 * tt);
     }
@@ -511,186 +553,181 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   }
   __syncthreads();
 
-  // ---------------- phase 3: A.V on MFMA
-  v4i acc[NTL][NT];
+  // ---------------- conversion: every score byte of this wave's units replaced by its
+  // softmax code a - 128 (lanes g = 0, 1 (and 2, 3) read the two bank copies of their
+  // row, so one lookup touches 32 distinct banks)
+  if (active) {
+    uint32_t cbase[NTL];
 #pragma unroll
-  for (int t = 0; t < NTL; ++t)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[t][nt] = (v4i){0, 0, 0, 0};
-  if (active && c_begin < c_end) {
-    // code byte of (row, M - code) at arow[-128 code]: lanes g = 0, 1 (and 2, 3) read
-    // the two bank copies of their row, so one read touches 32 distinct banks
-    const uint8_t* arow[NTL];
-#pragma unroll
-    for (int t = 0; t < NTL; ++t)
-      arow[t] = (const uint8_t*)tab + (Mrow[t] * 32 + col + 16 * (g & 1)) * 4 + (qset * NTL + t);
-    const int vt_off = lane * 16;               // lane's bytes of a 16-channel x 64-key block
-    constexpr int CH = 64 * DK;                 // bytes of V^T per 64-key chunk
-    // softmax codes (as a - 128) of one chunk of keys for every query tile;
-    // all lookups of a chunk are issued before any is packed
-    auto codes_full = [&](int c, v4i* af) {
-      v4i sv[NTL];
-#pragma unroll
-      for (int t = 0; t < NTL; ++t) sv[t] = *(const v4i*)(srd[t] + c * KCHUNK);
-      // bytes 0 and 2 of a dword are loaded into the two halves of one register, bytes 1
-      // and 3 into another (16-bit loads that keep the other half), so one shift-or
-      // packs four codes
-      us2 ev[NTL][4], od[NTL][4];
-#pragma unroll
-      for (int t = 0; t < NTL; ++t)
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const uint16_t v = arow[t][__mul24(-128, (int)(((uint32_t)sv[t][k >> 2] >> (8 * (k & 3))) & 0xff))];
-          us2& dst = (k & 1) ? od[t][k >> 2] : ev[t][k >> 2];
-          if (k & 2)
-            dst.y = v;
-          else
-            dst.x = v;
-        }
-#pragma unroll
-      for (int t = 0; t < NTL; ++t)
-#pragma unroll
-        for (int wd = 0; wd < 4; ++wd)
-          af[t][wd] = (int)(__builtin_bit_cast(uint32_t, ev[t][wd]) | (__builtin_bit_cast(uint32_t, od[t][wd]) << 8));
+    for (int t = 0; t < NTL; ++t) cbase[t] = TAB + (uint32_t)((col + 16 * (g & 1)) * 4 + qset * NTL + t);
+    auto code_at = [&](uint32_t dw, int k, int t) {
+      return (uint32_t) * (const lds8*)(uintptr_t)__builtin_amdgcn_udot4(dw, 128u << (8 * k), cbase[t], false);
     };
-    auto codes_tail = [&](int c, v4i* af) {
+    // four codes of one dword: two 16-bit halves, then one merge
+    auto codes4 = [&](uint32_t dw, int t) {
+      const uint32_t lo = code_at(dw, 0, t) | (code_at(dw, 1, t) << 8);
+      const uint32_t hi = code_at(dw, 2, t) | (code_at(dw, 3, t) << 8);
+      return (int)(lo | (hi << 16));
+    };
+    // the next chunk is read before the current one is written back (chunks are disjoint)
+    v4i svn[NTL];
+    if (c_begin < c_full) {
+#pragma unroll
+      for (int t = 0; t < NTL; ++t) svn[t] = *chunk_ptr(c_begin, t);
+    }
+    for (int c = c_begin; c < c_full; ++c) {
+      v4i sv[NTL];
+      const int cn = min(c + 1, c_full - 1);
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
-        const v4i sv = *(const v4i*)(srd[t] + c * KCHUNK);
+        sv[t] = svn[t];
+        svn[t] = *chunk_ptr(cn, t);
+      }
+#pragma unroll
+      for (int t = 0; t < NTL; ++t) {
+        v4i out;
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) out[wd] = codes4(Mrep[t] - (uint32_t)sv[t][wd], t);
+        *chunk_ptr(c, t) = out;
+      }
+    }
+    if (c_full < c_end) {
+      const int c = c_full;
+      const int kb = c * KCHUNK + g * 16;
+#pragma unroll
+      for (int t = 0; t < NTL; ++t) {
+        const v4i sv = *chunk_ptr(c, t);
+        v4i out;
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
+          const uint32_t dw = Mrep[t] - (uint32_t)sv[wd];
           uint32_t packed = 0;
 #pragma unroll
-          for (int by = 0; by < 4; ++by) {
-            const bool ok = c * KCHUNK + g * 16 + wd * 4 + by < L;
-            const int code = ok ? (int)(((uint32_t)sv[wd] >> (8 * by)) & 0xff) : Mrow[t];
-            const uint32_t av = arow[t][-128 * code];
-            packed |= (ok ? av : 0x80u) << (8 * by);  // a = 0 for padded keys
-          }
-          af[t][wd] = (int)packed;
+          for (int k = 0; k < 4; ++k) packed |= (kb + 4 * wd + k < L ? code_at(dw, k, t) : 0x80u) << (8 * k);
+          out[wd] = (int)packed;
         }
+        *chunk_ptr(c, t) = out;
       }
-    };
-    // V^T operands in parts of NP = 2 channel tiles, each with this lane's V sums over
-    // the chunk for channels (hp NP + k) * 16 + col.  One buffer per part of a chunk:
-    // a part is refilled with the next chunk's as soon as its MFMAs are issued, so a
-    // whole chunk of V is in flight while the current one is multiplied (past the last
-    // chunk the loads re-read it: in bounds, unused, and the loads stay unconditional).
-    constexpr int NP = 2;
-    constexpr int NPART = NT / NP;
-    struct VPart {
-      v4i v[NP];
-      int s[NP];
-    };
-    auto load_part = [&](int c, int hp, VPart& dst) {
-      const int8_t* src = VTh + (size_t)c * CH + hp * NP * 1024 + vt_off;
-#pragma unroll
-      for (int k = 0; k < NP; ++k) dst.v[k] = *(const v4i*)(src + k * 1024);
-      const int2 sv2 = *(const int2*)(vs + ((size_t)c * 16 + col) * NT + hp * NP);
-      dst.s[0] = sv2.x;
-      dst.s[1] = sv2.y;
-    };
-    int vacc[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) vacc[nt] = 0;
-    v4i af[NTL];
-    auto mma_part = [&](const int hp, const VPart& vp) {
-#pragma unroll
-      for (int k = 0; k < NP; ++k) {
-#pragma unroll
-        for (int t = 0; t < NTL; ++t)
-          acc[t][hp * NP + k] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[t], vp.v[k], acc[t][hp * NP + k], 0, 0, 0);
-        vacc[hp * NP + k] += vp.s[k];
-      }
-    };
-    const int c_last = c_end - 1;
-    VPart pb[NPART];
-#pragma unroll
-    for (int hp = 0; hp < NPART; ++hp) load_part(c_begin, hp, pb[hp]);
-    auto mma_chunk = [&](const int c) {
-      const int cn = min(c + 1, c_last);
-#pragma unroll
-      for (int hp = 0; hp < NPART; ++hp) {
-        mma_part(hp, pb[hp]);
-        load_part(cn, hp, pb[hp]);
-      }
-    };
-    // the full chunks in a loop of their own (a shared loop body would make every chunk
-    // pay the tail's per-key selects), then the chunk with the utterance's last key
-    int c = c_begin;
-    for (; c < c_full; ++c) {
-      codes_full(c, af);
-      mma_chunk(c);
     }
-    if (c < c_end) {
-      codes_tail(c, af);
-      mma_chunk(c);
-    }
-    // exact correction for the -128 offset: + 128 * sum of V over the same keys
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int t = 0; t < NTL; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[t][nt][i] += 128 * vacc[nt];
   }
+  __syncthreads();
 
-  // ---------------- combine the key splits, requantize, store
-  const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
-  auto requant_o = [&](int32_t v) -> int {
-    const int64_t r = ((int64_t)v * a.m_o + half_o) >> a.shift_o;
-    return r < -127 ? -127 : (r > 127 ? 127 : (int)r);
-  };
-  if (KSPLIT == 1) {
+  // ---------------- phase 3: A.V on MFMA, the waves split channels and keys
+  const int cg = w % NCG, kh = w / NCG;
+  int a_begin, a_end;
+  split_pairs(nkc, P3_OLDER, KH / 2, kh, &a_begin, &a_end);
+  v4i acc[NTILES][AV_NT];
 #pragma unroll
-    for (int t = 0; t < NTL; ++t)
+  for (int tt = 0; tt < NTILES; ++tt)
+#pragma unroll
+    for (int j = 0; j < AV_NT; ++j) acc[tt][j] = (v4i){0, 0, 0, 0};
+  const bool wg_active = wg_q0 < L;
+  if (wg_active && a_begin < a_end) {
+    // V^T fragment of 16 channels x 64 keys (A operand: lane (ch, g) holds keys
+    // 16 g .. 16 g + 15 of channel ch); codes of 16 queries x the same keys (B operand:
+    // lane (q, g) holds keys 16 g .. of row q), straight from the score blocks
+    constexpr int CH = 64 * DK;  // bytes of V^T per 64-key chunk
+    const int8_t* vsrc = VTh + (size_t)(cg * AV_NT) * 1024 + frag_off;
+    const uint32_t av0 = base + (uint32_t)(g * BLK + col * 16);
+    // rings over the chunk phase (chunk - a_begin) % 3, all indices static: V fragments
+    // two chunks ahead, codes one chunk ahead (past the last chunk the reads re-read it)
+    int vpart[AV_NT];
+    v4i vr[3][AV_NT], br[3][NTILES];
+    auto ldv = [&](int c, v4i* dst) {
+#pragma unroll
+      for (int j = 0; j < AV_NT; ++j) dst[j] = *(const v4i*)(vsrc + (size_t)c * CH + j * 1024);
+    };
+    auto ldc = [&](int c, v4i* dst) {
+      const uint32_t cp = av0 + (uint32_t)c * (4 * BLK);
+#pragma unroll
+      for (int tt = 0; tt < NTILES; ++tt) dst[tt] = *(const ldsv4*)(uintptr_t)(cp + tt * 256);
+    };
+#pragma unroll
+    for (int j = 0; j < AV_NT; ++j) vpart[j] = 0;
+    const int c_last = a_end - 1;
+    ldv(a_begin, vr[0]);
+    ldv(min(a_begin + 1, c_last), vr[1]);
+    ldc(a_begin, br[0]);
+    int c = a_begin;
+    auto avstep = [&](auto Sc) {
+      constexpr int S = decltype(Sc)::value;
+      ldv(min(c + 2, c_last), vr[(S + 2) % 3]);
+      ldc(min(c + 1, c_last), br[(S + 1) % 3]);
+#pragma unroll
+      for (int j = 0; j < AV_NT; ++j) {
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) vpart[j] = __builtin_amdgcn_sdot4(vr[S][j][wd], 0x01010101, vpart[j], false);
+#pragma unroll
+        for (int tt = 0; tt < NTILES; ++tt)
+          acc[tt][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(vr[S][j], br[S][tt], acc[tt][j], 0, 0, 0);
+      }
+      ++c;
+    };
+    while (c + 3 <= a_end) {
+      avstep(Phase<0>{});
+      avstep(Phase<1>{});
+      avstep(Phase<2>{});
+    }
+    if (c < a_end) avstep(Phase<0>{});
+    if (c < a_end) avstep(Phase<1>{});
+    // exact correction for the -128 offset: + 128 * sum of V over the same keys.  Lane
+    // (ch, g) summed keys 16 g .. of channel ch; the output lane (q, g) needs channels
+    // 4 g .. 4 g + 3.
+#pragma unroll
+    for (int j = 0; j < AV_NT; ++j) {
+      int vs = vpart[j];
+      vs += __shfl_xor(vs, 16);
+      vs += __shfl_xor(vs, 32);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int qi = q0 + 16 * t + 4 * g + i;
-        if (qi >= T) continue;
-        int8_t* out = a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + col;
+        const int vi = __shfl(vs, 4 * g + i);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) out[nt * 16] = (int8_t)(qi < L ? requant_o(acc[t][nt][i]) : 0);
+        for (int tt = 0; tt < NTILES; ++tt) acc[tt][j][i] += 128 * vi;
       }
-  } else {
-    // partial sums of one query set: [ROWS][RSTRIDE] int32; the padding puts rows 4
-    // apart into different banks.  The first key split stores, the others add with
-    // LDS atomics (exact, order-free).
-    int32_t* rq = red + (size_t)qset * ROWS * RSTRIDE;
-    __syncthreads();  // every wave is done with the score rows
-    if (kpart == 0) {
-#pragma unroll
-      for (int t = 0; t < NTL; ++t)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) rq[(16 * t + 4 * g + i) * RSTRIDE + nt * 16 + col] = acc[t][nt][i];
     }
-    __syncthreads();
-    if (kpart != 0 && active) {
+  }
+
+  // ---------------- combine the key parts, requantize, store.  Partial sums in the
+  // table region as [cg][value][lane] int32: the first key part stores, the others
+  // add with LDS atomics (exact, order-free).
+  constexpr int R = NTILES * AV_NT * 4;
+  ldsi32* red = (ldsi32*)(uintptr_t)TAB;
+  if (kh == 0) {
 #pragma unroll
-      for (int t = 0; t < NTL; ++t)
+    for (int tt = 0; tt < NTILES; ++tt)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
+      for (int j = 0; j < AV_NT; ++j)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) atomicAdd(&rq[(16 * t + 4 * g + i) * RSTRIDE + nt * 16 + col], acc[t][nt][i]);
+        for (int i = 0; i < 4; ++i) red[(cg * R + (tt * AV_NT + j) * 4 + i) * 64 + lane] = acc[tt][j][i];
+  }
+  __syncthreads();
+  if (kh != 0 && wg_active && a_begin < a_end) {
+#pragma unroll
+    for (int tt = 0; tt < NTILES; ++tt)
+#pragma unroll
+      for (int j = 0; j < AV_NT; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          atomicAdd((int32_t*)&red[(cg * R + (tt * AV_NT + j) * 4 + i) * 64 + lane], acc[tt][j][i]);
+  }
+  __syncthreads();
+  // the KH waves of a channel group share its (tile, channel tile) units; lane (q, g) of
+  // unit (tt, j) holds query wg_q0 + 16 tt + q, channels 16 (cg AV_NT + j) + 4 g .. + 3
+  const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
+  auto requant_o = [&](int32_t v) -> uint32_t {
+    const int64_t r = ((int64_t)v * a.m_o + half_o) >> a.shift_o;
+    return (uint32_t)(r < -127 ? -127 : (r > 127 ? 127 : (int)r)) & 0xffu;
+  };
+  for (int u = kh; u < NTILES * AV_NT; u += KH) {
+    const int tt = u / AV_NT, j = u - tt * AV_NT;
+    const int qi = wg_q0 + 16 * tt + col;
+    if (qi >= T) continue;
+    uint32_t packed = 0;
+    if (qi < L) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) packed |= requant_o(red[(cg * R + u * 4 + i) * 64 + lane]) << (8 * i);
     }
-    __syncthreads();
-    // the KSPLIT waves of the set share its rows: items of 4 channels, row-major
-    constexpr int IPR = DK / 4;  // items per row
-    for (int it = kpart * 64 + lane; it < ROWS * IPR; it += 64 * KSPLIT) {
-      const int rr = it / IPR;
-      const int ch = (it % IPR) * 4;
-      const int qi = q0 + rr;
-      if (qi >= T) continue;
-      const v4i v = *(const v4i*)(rq + rr * RSTRIDE + ch);
-      uint32_t packed = 0;
-      if (qi < L) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) packed |= ((uint32_t)requant_o(v[e]) & 0xffu) << (8 * e);
-      }
-      *(uint32_t*)(a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + ch) = packed;
-    }
+    *(uint32_t*)(a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + (cg * AV_NT + j) * 16 + 4 * g) = packed;
   }
 }
 
@@ -708,6 +745,30 @@ __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) 
     else
       attn_block<DK, KS2, NTL2, WIDE>(a, smem, blockIdx.x - a.seg2_block, a.nqb2, a.seg2_q0);
   }
+}
+
+// The I-BERT integer exp of every score distance d = M - s in [0, 254] (Sec. 2.2:
+// d = z q_ln2 - r with r in (-q_ln2, 0], e = ((r + q_b)^2 + q_c) >> z), and 0 at d = 255,
+// which no score reaches; integer arithmetic only.  One thread per d.
+__global__ __launch_bounds__(256) void iexp_table(uint32_t* tab, int q_ln2, int q_b, int q_c) {
+  const int dd = threadIdx.x;
+  uint32_t e = 0;
+  if (dd < 255) {
+    int z = 0, rem = dd;
+    while (rem >= q_ln2) {  // z = floor(d / q_ln2), d <= 254
+      rem -= q_ln2;
+      ++z;
+    }
+    const int r = -rem;
+    const int poly = (r + q_b) * (r + q_b) + q_c;  // < 2^24 (checked at create)
+    e = z >= 32 ? 0u : ((uint32_t)poly >> z);
+  }
+  tab[dd] = e;
+}
+
+hipError_t launch_iexp_table(uint32_t* tab, int q_ln2, int q_b, int q_c, hipStream_t st) {
+  hipLaunchKernelGGL(iexp_table, dim3(1), dim3(256), 0, st, tab, q_ln2, q_b, q_c);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -740,18 +801,15 @@ __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
 
 // ---------------------------------------------------------------------------
 size_t attn_lds_bytes(int DK, int ksplit, int ntl, int T_al) {
-  const int rows = 16 * ntl, nqs = ATTN_WAVES / ksplit;
-  const int wgq = rows * nqs;
-  const size_t s_bytes = (size_t)wgq * (T_al + SCORE_PAD);
-  const size_t red = ksplit > 1 ? (size_t)nqs * rows * (DK + 4) * 4 : 0;
-  const size_t big = ((s_bytes > red ? s_bytes : red) + 15) & ~(size_t)15;
-  return big + (size_t)TAB_DW * 4 + 256 * 4 + 2 * (size_t)rows * ATTN_WAVES * 4 + (size_t)wgq * 4;
+  (void)DK;
+  const int rows = 16 * ntl, wgq = rows * (ATTN_WAVES / ksplit);
+  return attn_lds(wgq, rows, T_al).total;
 }
 
 // Workgroup shapes the kernel is built for: (key splits, 16-query tiles per wave).
 static const AttnCfg kAttnCfgs[] = {{4, 2}, {8, 2}, {8, 3}};
 // One 16-query tile per wave: the smallest score rows, for utterances whose rows do not
-// fit any shape above (every K, P and V fragment then feeds a single MFMA)
+// fit any shape above (every K and P fragment then feeds a single MFMA)
 static const AttnCfg kAttnLong = {8, 1};
 constexpr size_t kLdsBudget = 160 * 1024;
 constexpr int kNumCUs = 256;
@@ -888,7 +946,7 @@ hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars&
   a.p = ws.p;
   a.u = w.u;
   a.v = w.v;
-  a.vsum = ws.vsum;
+  a.etab = w.etab;
   a.ctx = ws.ctx;
   a.lens = lens;
   a.T = rs.T;
@@ -900,14 +958,12 @@ hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars&
   a.mc24 = sc.fs_mc24;
   a.mp24 = sc.fs_mp24;
   a.bias32 = sc.fs_bias32;
-  a.post_shift = sc.fs_post_shift;
-  a.mcd = sc.fs_mcd;
-  a.mpd = sc.fs_mpd;
+  a.m_c = sc.m_c;
+  a.m_p = sc.m_p;
+  a.shift_s = sc.shift_s;
+  a.bias64 = ((int64_t)1 << (sc.shift_s - 1)) + ((int64_t)128 << sc.shift_s);
   a.m_o = sc.m_o;
   a.shift_o = sc.shift_o;
-  a.q_ln2 = sc.q_ln2;
-  a.q_b = sc.q_b;
-  a.q_c = sc.q_c;
   if (rs.DK == 128) return sc.fs_wide ? launch_attn_dk<128, true>(a, rs, st, ev) : launch_attn_dk<128, false>(a, rs, st, ev);
   if (rs.DK == 64) return sc.fs_wide ? launch_attn_dk<64, true>(a, rs, st, ev) : launch_attn_dk<64, false>(a, rs, st, ev);
   return hipErrorInvalidValue;

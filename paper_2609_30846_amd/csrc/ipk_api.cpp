@@ -97,32 +97,30 @@ static int validate_desc(const ipk_relpos_attn_desc* d) {
   return IPK_OK;
 }
 
-// Chooses how the attention core evaluates Eq. 11.  |c|, |p| <= d_k * 254 * 127
-// (int8 keys/positions times the 9-bit q + u, q + v); the 32-bit path is used when
-// m_c |c| + m_p |p| plus the rounding and code bias stays below 2^31 for every
-// possible score, so its wrap-around arithmetic is exact.
-static void plan_fused_score(Scalars* sc, int d_k) {
-  const int64_t cmax = (int64_t)d_k * 254 * 127;
+// Chooses how the attention core evaluates Eq. 11.  |c|, |p| <= d_k * 255 * 127
+// (int8 keys/positions times q + u, q + v with q in [-127, 127] and u, v in
+// [-128, 127]); the 32-bit path is used when m_c |c| + m_p |p| plus the rounding and
+// code bias stays below 2^31 for every possible score, so its wrap-around arithmetic
+// is exact.  force_wide selects the 64-bit path whatever the bound (both are exact and
+// give the same bytes).
+static void plan_fused_score(Scalars* sc, int d_k, bool force_wide) {
+  const int64_t cmax = (int64_t)d_k * 255 * 127;
   const int n = sc->shift_s;
   // 32-bit path: scale the multipliers to a shift of 16 so that the biased code
   // s + 128 = floor((m_c c + m_p p + 2^15 + 128 * 2^16) / 2^16) is byte 2 of the
   // clamped sum; only possible for n <= 16
-  bool narrow = n <= 16;
-  int64_t mc = 0, mp = 0, bias = ((int64_t)1 << 15) + ((int64_t)128 << 16);
+  bool narrow = n <= 16 && !force_wide;
+  int64_t mc = 0, mp = 0;
+  const int64_t bias = ((int64_t)1 << 15) + ((int64_t)128 << 16);
   if (narrow) {
     mc = (int64_t)sc->m_c << (16 - n);
     mp = (int64_t)sc->m_p << (16 - n);
     narrow = mc < (1 << 23) && mp < (1 << 23) && (mc + mp) * cmax + bias < ((int64_t)1 << 31);
   }
-  const char* force = getenv("IPK_SCORE_PATH");  // testing aid: "wide" forces float64
-  if (force && strcmp(force, "wide") == 0) narrow = false;
   sc->fs_wide = !narrow;
   sc->fs_mc24 = narrow ? (int32_t)mc : 0;
   sc->fs_mp24 = narrow ? (int32_t)mp : 0;
   sc->fs_bias32 = (int32_t)bias;
-  sc->fs_post_shift = 0;
-  sc->fs_mcd = ldexp((double)sc->m_c, -n);
-  sc->fs_mpd = ldexp((double)sc->m_p, -n);
 }
 
 static void free_handle(ipk_relpos_attn* h) {
@@ -171,7 +169,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   h->sc.q_ln2 = desc->q_ln2;
   h->sc.q_b = desc->q_b;
   h->sc.q_c = desc->q_c;
-  plan_fused_score(&h->sc, desc->d_k);
+  plan_fused_score(&h->sc, desc->d_k, false);
   h->has_run = false;
   h->last_was_residual = false;
   h->last_p = nullptr;
@@ -193,6 +191,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->w.w_out, d * d));
   chk(dev_alloc(h, &h->w.u, H * DK));
   chk(dev_alloc(h, &h->w.v, H * DK));
+  chk(dev_alloc(h, &h->w.etab, 256));
   chk(dev_alloc(h, &h->w.scale_qkv, 3 * d));
   chk(dev_alloc(h, &h->w.scale_pos, d));
   chk(dev_alloc(h, &h->w.scale_out, d));
@@ -224,6 +223,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(pack_weight_fragments(stage, h->w.w_out, (int)d, (int)d, nullptr));
   chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
   chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
+  chk(launch_iexp_table(h->w.etab, desc->q_ln2, desc->q_b, desc->q_c, nullptr));
   // Eq. 7 scales m * 2^-n: m < 2^23 and n <= 40, so each is an exact double
   std::vector<double> sq(3 * d), sp(d), so(d);
   for (size_t c = 0; c < d; ++c) {
@@ -450,6 +450,18 @@ extern "C" int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* 
   for (int i = 0; i < IPK_NUM_STAGES + 1; ++i) h->stage_ev[i] = (hipEvent_t)events[i];
   h->stages_pending = true;
   return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_set_score_path(ipk_relpos_attn_t* h, int32_t path) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (path != IPK_SCORE_AUTO && path != IPK_SCORE_WIDE) return fail(IPK_ERR_INVALID_ARG, "unknown score path %d", path);
+  plan_fused_score(&h->sc, h->DK, path == IPK_SCORE_WIDE);
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_score_path(const ipk_relpos_attn_t* h) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  return h->sc.fs_wide ? IPK_SCORE_WIDE : IPK_SCORE_NARROW;
 }
 
 extern "C" int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h) {

@@ -80,6 +80,7 @@ struct Weights {
   int8_t* w_pos;       // [d][d], in fragment order
   int8_t* w_out;       // [d][d], in fragment order
   int8_t *u, *v;       // [H][DK]
+  uint32_t* etab;      // [256] I-BERT integer exp of every score distance (0 at 255)
   // per-output-channel requantization scales m * 2^-n (exact in float64)
   double* scale_qkv;  // [3d]
   double* scale_pos;  // [d]
@@ -90,13 +91,11 @@ struct Scalars {
   int32_t m_c, m_p, shift_s;
   int32_t m_o, shift_o;
   int32_t q_ln2, q_b, q_c;
-  // Eq. 11 as evaluated by the attention core: either in 32-bit integers
-  // (t = mc24 c + mp24 p + bias32, then >> post_shift; exact when the bound on
-  // |t| proven at create holds) or, when that bound fails, in float64 with the
-  // multipliers pre-scaled by 2^-shift_s.
+  // Eq. 11 as evaluated by the attention core: in 32-bit integers
+  // (t = mc24 c + mp24 p + bias32 with the biased code in bits 16..23; exact when the
+  // bound on |t| proven at create holds), otherwise in 64-bit integers.
   bool fs_wide;
-  int32_t fs_mc24, fs_mp24, fs_bias32, fs_post_shift;
-  double fs_mcd, fs_mpd;
+  int32_t fs_mc24, fs_mp24, fs_bias32;
 };
 
 // Per-utterance valid lengths, passed by value to the kernels that mask.
@@ -130,6 +129,8 @@ inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t shmem,
 // pos_table == nullptr: Q|K|V only (the projected table is already in ws.p)
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev = {});
+// The I-BERT integer exp of every score distance into tab[256] (create time).
+hipError_t launch_iexp_table(uint32_t* tab, int q_ln2, int q_b, int q_c, hipStream_t st);
 hipError_t launch_attention(const RunShape& rs, const Weights& w, const Scalars& sc, const Workspace& ws,
                             const Lengths& lens, hipStream_t st, const LaunchEv& ev = {});
 // res != nullptr: the epilogue adds the residual, y := clamp8(RS(m_z z1 + m_y y, 1, shift_r))

@@ -28,6 +28,7 @@ IPK_MAX_T = 8192
 IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN = range(6)
 IPK_FFN_X, IPK_FFN_O = range(2)
 IPK_CONV_X, IPK_CONV_U, IPK_CONV_V, IPK_CONV_O = range(4)
+IPK_SCORE_AUTO, IPK_SCORE_WIDE, IPK_SCORE_NARROW = range(3)
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p
@@ -38,6 +39,8 @@ SIGNATURES = [
     ("ipk_relpos_attn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_relpos_attn_record_stages", C.c_int, [_vp, _vp]),
     ("ipk_relpos_attn_cache_positions", C.c_int, [_vp, _vp, C.c_int32, _vp]),
+    ("ipk_relpos_attn_set_score_path", C.c_int, [_vp, C.c_int32]),
+    ("ipk_relpos_attn_score_path", C.c_int, [_vp]),
     ("ipk_mhsa_residual_set", C.c_int, [_vp, _vp]),
     ("ipk_mhsa_residual_run", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
     ("ipk_ffn_create", C.c_int, [_vp, C.POINTER(_vp)]),
@@ -192,6 +195,17 @@ def ipk_relpos_attn_run(h: int, x, pos_table, lengths: Optional[Sequence[int]], 
     lp = lens.ctypes.data if lens is not None else None
     _check(load().ipk_relpos_attn_run(h, _ptr(x), _ptr(pos_table), lp, int(B), int(T), _ptr(y),
                                       _stream_ptr(stream)))
+
+
+def ipk_relpos_attn_set_score_path(h: int, path: int) -> None:
+    _check(load().ipk_relpos_attn_set_score_path(h, int(path)))
+
+
+def ipk_relpos_attn_score_path(h: int) -> int:
+    r = int(load().ipk_relpos_attn_score_path(h))
+    if r < 0:
+        raise IpkError(r, last_error())
+    return r
 
 
 def ipk_relpos_attn_cache_positions(h: int, pos_table, T_table: int, stream=None) -> None:

@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert ipk.abi_version() == 2
+    assert ipk.abi_version() == 3
     assert ipk.status_name(0) == "IPK_OK"
     assert ipk.status_name(-1) == "IPK_ERR_INVALID_ARG"
     assert ipk.status_name(-2) == "IPK_ERR_UNSUPPORTED"

@@ -14,16 +14,26 @@ from workloads import make_workload
 pytestmark = pytest.mark.gpu
 
 
+_SCORE_PATH = {"path": "auto"}
+
+
 @pytest.fixture(params=["auto", "wide"])
-def score_path(request, monkeypatch):
+def score_path(request):
     """The attention core evaluates Eq. 11 in 32-bit integers when the descriptor
-    bounds the fused score below 2^31 ("auto" picks it for the calibrated regime)
-    and in float64 otherwise; "wide" forces the float64 path at create time."""
-    if request.param == "wide":
-        monkeypatch.setenv("IPK_SCORE_PATH", "wide")
-    else:
-        monkeypatch.delenv("IPK_SCORE_PATH", raising=False)
-    return request.param
+    bounds the fused score below 2^31 (what create picks for the calibrated regime)
+    and in 64-bit integers otherwise; "wide" forces the 64-bit path on every handle
+    the test creates (ipk_relpos_attn_set_score_path)."""
+    _SCORE_PATH["path"] = request.param
+    yield request.param
+    _SCORE_PATH["path"] = "auto"
+
+
+def _make_module(ipk, blk, max_batch=None, max_T=None):
+    mod = ipk.RelPosAttn.from_block(blk, max_batch=max_batch, max_T=max_T)
+    if _SCORE_PATH["path"] == "wide":
+        ipk.ipk_relpos_attn_set_score_path(mod.handle, ipk.IPK_SCORE_WIDE)
+        assert ipk.ipk_relpos_attn_score_path(mod.handle) == ipk.IPK_SCORE_WIDE
+    return mod
 
 
 def _run_gpu(ipk, blk, x=None, lengths=None, inter=False, module=None):
@@ -32,7 +42,7 @@ def _run_gpu(ipk, blk, x=None, lengths=None, inter=False, module=None):
     x = blk.x if x is None else x
     lengths = blk.lengths if lengths is None else lengths
     B, T, d = x.shape
-    mod = module or ipk.RelPosAttn.from_block(blk, max_batch=B, max_T=T)
+    mod = module or _make_module(ipk, blk, max_batch=B, max_T=T)
     xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
     pe = torch.from_numpy(np.ascontiguousarray(blk.pos_table)).cuda()
     y = mod(xd, pe, lengths=lengths)
