@@ -78,13 +78,13 @@ struct AttnArgs {
 
 constexpr int TAB_DW = 256 * 32;  // dwords of the [d][32 banks] lookup-table region
 constexpr int ATTN_WAVES = 8;     // waves per workgroup (two per SIMD)
-constexpr int AV_NT = 2;          // 16-channel tiles per wave in phase 3
 
 // Share (out of 256) of a SIMD's work that its older wave takes in phase 1 and in the
 // later phases: the arbiter favours the older wave of a SIMD (the lower index), so with
 // equal shares the younger one finishes long after it.
-constexpr int P1_OLDER = 166;
-constexpr int P3_OLDER = 150;
+constexpr int P1_OLDER = 160;  // phase 1 (16-key steps)
+constexpr int P2_OLDER = 162;  // phase 2 and the conversion (64-key chunks)
+constexpr int P3_OLDER = 156;  // phase 3 (64-key chunks)
 
 template <int S>
 using Phase = std::integral_constant<int, S>;
@@ -95,18 +95,20 @@ __device__ __forceinline__ int mad_i24(int a, int b, int c) {
   return (int)((uint32_t)__mul24(a, b) + (uint32_t)c);
 }
 
-// floor(2^32 / D) for 2 <= D < 2^32 by binary long division (integer only):
-// floor((2^32 - 1) / D), plus one when D divides 2^32 (a power of two).
+// floor(2^32 / D) for 2^8 <= D < 2^32 by binary long division in 32-bit integers:
+// floor((2^32 - 1) / D), plus one when D divides 2^32 (a power of two).  Quotient bits
+// 31..24 are zero for D >= 2^8, which leaves the remainder 2^8 - 1 after them; each
+// further step doubles the remainder and adds the next dividend bit (a one): it stays
+// below D after the conditional subtraction, so the wrap-around of 2 r + 1 past 2^32
+// cancels in the subtraction.
 __device__ __forceinline__ uint32_t floor_2p32_div(uint32_t D) {
-  uint64_t r = 0;
-  uint32_t q = 0;
-#pragma unroll 4
-  for (int i = 31; i >= 0; --i) {
-    r = (r << 1) | 1u;
-    if (r >= D) {
-      r -= D;
-      q |= 1u << i;
-    }
+  const uint32_t half = D >> 1;  // 2 r + 1 >= D  <=>  r >= floor(D / 2)
+  uint32_t r = 255u, q = 0;
+#pragma unroll
+  for (int i = 23; i >= 0; --i) {
+    const bool c = r >= half;
+    r = (r << 1) + 1u - (c ? D : 0u);
+    q = (q << 1) | (c ? 1u : 0u);
   }
   return q + ((D & (D - 1)) == 0 ? 1u : 0u);
 }
@@ -147,10 +149,11 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   constexpr int NTILES = WGQ / 16;          // 16-query tiles per workgroup
   constexpr int NKS = DK / 64;              // MFMA K-steps over d_k
   constexpr int BLK = WGQ * 16;             // bytes per 16-key block of score rows
-  constexpr int NCG = DK / (16 * AV_NT);    // channel groups of phase 3
-  constexpr int KH = ATTN_WAVES / NCG;      // key parts of phase 3
+  constexpr int AV_NT = DK / 64;            // 16-channel tiles per wave in phase 3
+  constexpr int NCG = DK / (16 * AV_NT);    // channel groups of phase 3 (four)
+  constexpr int KH = ATTN_WAVES / NCG;      // key parts of phase 3 (two)
   static_assert(NTILES <= 4, "the code tables hold four 16-row tiles");
-  static_assert(KH >= 2 && KH % 2 == 0, "phase-3 wave grid");
+  static_assert(KH == 2, "phase-3 wave grid");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index: uniform, kept in SGPRs
@@ -189,7 +192,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int T = a.T, T_al = a.T_al;
   const int nkc = (L + KCHUNK - 1) / KCHUNK;
   int c_begin, c_end;
-  split(nkc, P3_OLDER, &c_begin, &c_end);
+  split(nkc, P2_OLDER, &c_begin, &c_end);
   // chunks below c_full hold only valid keys; c_full < c_end only when this wave's
   // range holds the chunk with the utterance's last key
   const int c_full = max(c_begin, min(c_end, L / KCHUNK));
@@ -531,21 +534,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     uint32_t tot = 0;
 #pragma unroll
     for (int k2 = 0; k2 < KSPLIT; ++k2) tot += ssum[(qs * KSPLIT + k2) * ROWS + rr];
-    sF[tid] = tot >= 2 ? floor_2p32_div(tot) : 0u;
+    sF[tid] = tot >= 256 ? floor_2p32_div(tot) : 0u;
   }
   __syncthreads();
   // softmax code tables (over the exp copies, which phase 2 has finished with): the
   // dword of distance d and bank rr + 16 c (c = 0, 1: two copies) holds in byte tt
   // min(floor(e(d) F_r / 2^24), 255) ^ 0x80 of row r = 16 tt + rr, i.e. a - 128.
-  // floor(e F / 2^24) is the high word of (e 2^8) F (e < 2^24).  Each dword is
-  // computed once and written to both copies.
+  // e < 2^24 and F <= 2^24: floor(e F / 2^24) is bits 24..55 of the 48-bit product of
+  // the 24-bit multiplies (F = 2^24, when the sum is 2^8, gives e itself).  Each dword
+  // is computed once and written to both copies.
   for (int idx = tid; idx < TAB_DW / 2; idx += 64 * ATTN_WAVES) {
     const int dd = idx >> 4, rr = idx & 15;
-    const uint32_t e8 = etab[dd] << 8;
+    const uint32_t e = etab[dd];
     uint32_t packed = 0;
 #pragma unroll
     for (int tt = 0; tt < NTILES; ++tt) {
-      const uint32_t v = __umulhi(e8, sF[16 * tt + rr]);
+      const uint32_t F = sF[16 * tt + rr];
+      const uint64_t prod = (uint64_t)(e & 0xffffffu) * (uint64_t)(F & 0xffffffu);  // 24-bit operands
+      const uint32_t v = F == (1u << 24) ? e : (uint32_t)(prod >> 24);
       packed |= ((v > 255u ? 255u : v) ^ 0x80u) << (8 * tt);
     }
     tab[dd * 32 + rr] = packed;
@@ -615,7 +621,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   // ---------------- phase 3: A.V on MFMA, the waves split channels and keys
   const int cg = w % NCG, kh = w / NCG;
   int a_begin, a_end;
-  split_pairs(nkc, P3_OLDER, KH / 2, kh, &a_begin, &a_end);
+  split_pairs(nkc, P3_OLDER, 1, kh, &a_begin, &a_end);
   v4i acc[NTILES][AV_NT];
 #pragma unroll
   for (int tt = 0; tt < NTILES; ++tt)
@@ -687,45 +693,37 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
   }
 
-  // ---------------- combine the key parts, requantize, store.  Partial sums in the
-  // table region as [cg][value][lane] int32: the first key part stores, the others
-  // add with LDS atomics (exact, order-free).
+  // ---------------- combine the two key parts, requantize, store.  The (tile, channel
+  // tile) units of a channel group alternate between its two waves: each wave leaves
+  // the partial sums of the units it does not own in the table region, as
+  // [cg][value][lane] int32, and adds its partner's to the units it owns (exact).
   constexpr int R = NTILES * AV_NT * 4;
+  constexpr int NU = NTILES * AV_NT;
   ldsi32* red = (ldsi32*)(uintptr_t)TAB;
-  if (kh == 0) {
 #pragma unroll
-    for (int tt = 0; tt < NTILES; ++tt)
+  for (int u = 0; u < NU; ++u)
+    if (u % KH != kh) {
 #pragma unroll
-      for (int j = 0; j < AV_NT; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) red[(cg * R + (tt * AV_NT + j) * 4 + i) * 64 + lane] = acc[tt][j][i];
-  }
+      for (int i = 0; i < 4; ++i) red[(cg * R + u * 4 + i) * 64 + lane] = acc[u / AV_NT][u % AV_NT][i];
+    }
   __syncthreads();
-  if (kh != 0 && wg_active && a_begin < a_end) {
-#pragma unroll
-    for (int tt = 0; tt < NTILES; ++tt)
-#pragma unroll
-      for (int j = 0; j < AV_NT; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          atomicAdd((int32_t*)&red[(cg * R + (tt * AV_NT + j) * 4 + i) * 64 + lane], acc[tt][j][i]);
-  }
-  __syncthreads();
-  // the KH waves of a channel group share its (tile, channel tile) units; lane (q, g) of
-  // unit (tt, j) holds query wg_q0 + 16 tt + q, channels 16 (cg AV_NT + j) + 4 g .. + 3
+  // lane (q, g) of unit (tt, j) holds query wg_q0 + 16 tt + q, channels
+  // 16 (cg AV_NT + j) + 4 g .. + 3
   const int64_t half_o = (int64_t)1 << (a.shift_o - 1);
   auto requant_o = [&](int32_t v) -> uint32_t {
     const int64_t r = ((int64_t)v * a.m_o + half_o) >> a.shift_o;
     return (uint32_t)(r < -127 ? -127 : (r > 127 ? 127 : (int)r)) & 0xffu;
   };
-  for (int u = kh; u < NTILES * AV_NT; u += KH) {
-    const int tt = u / AV_NT, j = u - tt * AV_NT;
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    if (u % KH != kh) continue;
+    const int tt = u / AV_NT, j = u % AV_NT;
     const int qi = wg_q0 + 16 * tt + col;
     if (qi >= T) continue;
     uint32_t packed = 0;
     if (qi < L) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) packed |= requant_o(red[(cg * R + u * 4 + i) * 64 + lane]) << (8 * i);
+      for (int i = 0; i < 4; ++i) packed |= requant_o(acc[tt][j][i] + red[(cg * R + u * 4 + i) * 64 + lane]) << (8 * i);
     }
     *(uint32_t*)(a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + (cg * AV_NT + j) * 16 + 4 * g) = packed;
   }
