@@ -31,8 +31,8 @@
 // a single v_dot4 (base + 128 d).
 // Conversion: F = floor(2^32 / sum) per row (integer long division), per-row tables of
 // the softmax code a - 128 = min(floor(e F / 2^24), 255) - 128, and every score byte of
-// the workgroup replaced in place by its code (keys past the utterance by -128, i.e.
-// a = 0).
+// the workgroup replaced in place by its code.  Keys past the utterance take distance
+// 255 in both passes: its exp is 0 (left out of the sum) and its code -128 (a = 0).
 // Phase 3 (A.V): the waves split the d_k channels (two 16-channel MFMA tiles each) and
 // the keys; with the V^T fragment as the A operand and 16 queries' codes (16 bytes of
 // one row, read straight from its block) as B, each output lane holds four consecutive
@@ -82,7 +82,7 @@ constexpr int ATTN_WAVES = 8;     // waves per workgroup (two per SIMD)
 // Share (out of 256) of a SIMD's work that its older wave takes in phase 1 and in the
 // later phases: the arbiter favours the older wave of a SIMD (the lower index), so with
 // equal shares the younger one finishes long after it.
-constexpr int P1_OLDER = 160;  // phase 1 (16-key steps)
+constexpr int P1_OLDER = 166;  // phase 1 (16-key steps)
 constexpr int P2_OLDER = 162;  // phase 2 and the conversion (64-key chunks)
 constexpr int P3_OLDER = 156;  // phase 3 (64-key chunks)
 
@@ -454,6 +454,13 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     Mrep[t] = (uint32_t)m * 0x01010101u;
   }
   const uint32_t rd0 = base + (uint32_t)(g * BLK + (ROWS * qset + col) * 16);
+  // Distances of four keys of the chunk that holds the utterance's last key: keys at or
+  // past L get distance 255, whose integer exp is 0 and whose softmax code is -128
+  // (a = 0).  A byte past L may exceed M, but its borrow only reaches later keys.
+  auto tail_dist = [&](uint32_t dw, int c, int wd) {
+    const int nv = L - (c * KCHUNK + g * 16 + 4 * wd);  // valid keys from this dword's first
+    return nv >= 4 ? dw : (nv <= 0 ? 0xffffffffu : dw | (0xffffffffu << (8 * nv)));
+  };
   auto chunk_ptr = [&](int c, int t) { return (ldsv4*)(uintptr_t)(rd0 + (uint32_t)c * (4 * BLK) + t * 256); };
 
   // ---------------- phase 2: row sums of the integer exp
@@ -500,20 +507,17 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
     if (c_full < c_end) {  // the chunk that holds the utterance's last key
       const int c = c_full;
-      const int kb = c * KCHUNK + g * 16;
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         const v4i sv = *chunk_ptr(c, t);
+        uint32_t acc_e = 0;
 #pragma unroll
         for (int wd = 0; wd < 4; ++wd) {
-          // a byte past the last key may exceed M: its borrow only reaches later keys
-          const uint32_t dw = Mrep[t] - (uint32_t)sv[wd];
+          const uint32_t dw = tail_dist(Mrep[t] - (uint32_t)sv[wd], c, wd);
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const uint32_t e = e_at(dw, k);
-            sum[t] += kb + 4 * wd + k < L ? e : 0u;
-          }
+          for (int k = 0; k < 4; ++k) acc_e += e_at(dw, k);
         }
+        sum[t] += acc_e;
       }
     }
   }
@@ -599,19 +603,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
     if (c_full < c_end) {
       const int c = c_full;
-      const int kb = c * KCHUNK + g * 16;
 #pragma unroll
       for (int t = 0; t < NTL; ++t) {
         const v4i sv = *chunk_ptr(c, t);
         v4i out;
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t dw = Mrep[t] - (uint32_t)sv[wd];
-          uint32_t packed = 0;
-#pragma unroll
-          for (int k = 0; k < 4; ++k) packed |= (kb + 4 * wd + k < L ? code_at(dw, k, t) : 0x80u) << (8 * k);
-          out[wd] = (int)packed;
-        }
+        for (int wd = 0; wd < 4; ++wd) out[wd] = codes4(tail_dist(Mrep[t] - (uint32_t)sv[wd], c, wd), t);
         *chunk_ptr(c, t) = out;
       }
     }

@@ -136,9 +136,10 @@ def test_longform(gpu_lib, regime, score_path):
 
 @pytest.mark.parametrize("regime", ["literal", "calibrated"])
 def test_stack_of_24_blocks(gpu_lib, regime):
-    """The 24-block stack chained on the GPU; each layer is checked against the oracle
-    on the GPU's own input for that layer, one utterance per layer (utterances are
-    independent), and the first four layers on the whole batch."""
+    """The 24-block stack chained on the GPU (each block's int8 output is the next
+    block's input, Eq. 2 stacked): every layer's whole batch (B = 8 utterances, ragged
+    lengths) is compared byte for byte with the oracle run on the GPU's own input for
+    that layer, so the final 24-layer output is checked in full as well."""
     import torch
 
     wl = make_workload("stack", regime)
@@ -151,14 +152,9 @@ def test_stack_of_24_blocks(gpu_lib, regime):
         yd = mod(xd, pe, lengths=blk.lengths)
         torch.cuda.synchronize()
         xin, yg = xd.cpu().numpy(), yd.cpu().numpy()
-        if layer < 4:
-            y = core.relpos_attn(blk, x=xin)
-            assert _first_mismatch(yg, y) is None, (layer, _first_mismatch(yg, y))
-        else:
-            b = layer % B
-            y = core.relpos_attn(blk, x=xin[b:b + 1].copy(), lengths=blk.lengths[b:b + 1])
-            assert _first_mismatch(yg[b:b + 1], y) is None, (layer, b, _first_mismatch(yg[b:b + 1], y))
-        print(f"[parity] stack/{regime} layer {layer} ok", flush=True)
+        y = core.relpos_attn(blk, x=xin)
+        assert _first_mismatch(yg, y) is None, (layer, _first_mismatch(yg, y))
+        print(f"[parity] stack/{regime} layer {layer} ok (B={B})", flush=True)
         xd = yd
     for m in mods:
         m.close()
