@@ -64,6 +64,7 @@ struct AttnArgs {
   Lengths lens;
   int T, T_al, H, d, p_rows, p_base;
   int nqb;        // query blocks per (utterance, head) of the first segment
+  DivU dv_nqb, dv_nqb2, dv_H;  // the block decomposition's divisors
   int xcd_group;  // keep each (utterance, head) on one XCD
   // second segment of a two-shape grid: blocks from seg2_block on cover the queries
   // from seg2_q0 on, nqb2 blocks per (utterance, head), with the second shape
@@ -141,8 +142,9 @@ __device__ __forceinline__ void split_pairs(int n, int older, int hk, int part, 
 // One workgroup of the core: block `lin` of a segment of nqb query blocks per
 // (utterance, head) that starts at query q_base.
 template <int DK, int KSPLIT, int NTL, bool WIDE>
-__device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* smem, const int lin, const int nqb,
+__device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* smem, const int lin, const DivU& dnqb,
                                            const int q_base) {
+  const int nqb = (int)dnqb.d;
   constexpr int NQS = ATTN_WAVES / KSPLIT;  // query sets per workgroup
   constexpr int ROWS = 16 * NTL;            // queries per set: NTL 16-query MFMA tiles
   constexpr int WGQ = ROWS * NQS;           // queries per workgroup
@@ -178,14 +180,14 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   // its K, P and V stay in that XCD's L2.
   int qb, bhi;
   if (a.xcd_group) {
-    const int x = lin & 7, k = lin >> 3, s = k / nqb;
+    const int x = lin & 7, k = lin >> 3, s = (int)div_u(k, dnqb);
     qb = k - s * nqb;
     bhi = x + 8 * s;
   } else {
-    qb = lin % nqb;
-    bhi = lin / nqb;
+    bhi = (int)div_u(lin, dnqb);
+    qb = lin - bhi * nqb;
   }
-  const int b = bhi / a.H, h = bhi - (bhi / a.H) * a.H;
+  const int b = (int)div_u(bhi, a.dv_H), h = bhi - b * a.H;
   const int wg_q0 = q_base + qb * WGQ;
   const int q0 = wg_q0 + ROWS * qset;  // first query of this wave's set
   const int L = a.lens.len[b];
@@ -733,12 +735,12 @@ template <int DK, int KS1, int NTL1, int KS2, int NTL2, bool WIDE>
 __global__ __launch_bounds__(64 * ATTN_WAVES) void relpos_attn_core(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   if constexpr (NTL2 == 0) {
-    attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.nqb, 0);
+    attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.dv_nqb, 0);
   } else {
     if ((int)blockIdx.x < a.seg2_block)
-      attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.nqb, 0);
+      attn_block<DK, KS1, NTL1, WIDE>(a, smem, blockIdx.x, a.dv_nqb, 0);
     else
-      attn_block<DK, KS2, NTL2, WIDE>(a, smem, blockIdx.x - a.seg2_block, a.nqb2, a.seg2_q0);
+      attn_block<DK, KS2, NTL2, WIDE>(a, smem, blockIdx.x - a.seg2_block, a.dv_nqb2, a.seg2_q0);
   }
 }
 
@@ -771,25 +773,27 @@ hipError_t launch_iexp_table(uint32_t* tab, int q_ln2, int q_b, int q_c, hipStre
 struct GatherArgs {
   const int8_t* src;
   int8_t* dst;
-  int which, B, T, T_al, H, DK, d, p_rows, p_base;
+  int which, B, T, T_al, H, dks, d, p_rows, p_base;  // d_k = 2^dks
 };
 
+// grid: (d / 256 rounded up, rows per utterance, utterances); no division on the device
 __global__ __launch_bounds__(256) void gather_intermediate(GatherArgs a) {
-  const long rows = a.which == 3 ? (long)(2 * a.T - 1) : (long)a.B * a.T;
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= rows * a.d) return;
-  const long m = idx / a.d;
-  const int c = (int)(idx % a.d);
-  const int h = c / a.DK, kk = c % a.DK;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= a.d) return;
+  const int t = blockIdx.y, b = blockIdx.z;
+  const int h = c >> a.dks, kk = c & ((1 << a.dks) - 1), DK = 1 << a.dks;
+  const size_t idx = ((size_t)b * a.T + t) * a.d + c;
   int8_t v;
-  if (a.which == 3) {
-    v = a.src[(size_t)h * a.p_rows * a.DK + frag_index(a.p_base + (int)m, kk, a.DK)];
-  } else if (a.which >= 4) {  // the context or the LayerNorm output, [B][T][d]
+  if (a.which == 3) {  // the position table, [2T-1][d]
+    v = a.src[(size_t)h * a.p_rows * DK + frag_index(a.p_base + t, kk, DK)];
+    a.dst[(size_t)t * a.d + c] = v;
+    return;
+  }
+  if (a.which >= 4) {  // the context or the LayerNorm output, [B][T][d]
     v = a.src[idx];
   } else {
-    const long b = m / a.T, t = m % a.T;
-    const size_t base = ((size_t)b * a.H + h) * a.T_al * a.DK;
-    v = a.src[base + (a.which == 2 ? vt_index((int)t, kk, a.DK) : frag_index((int)t, kk, a.DK))];
+    const size_t base = ((size_t)b * a.H + h) * a.T_al * DK;
+    v = a.src[base + (a.which == 2 ? vt_index(t, kk, DK) : frag_index(t, kk, DK))];
   }
   a.dst[idx] = v;
 }
@@ -912,6 +916,9 @@ static hipError_t launch_attn_plan(const AttnArgs& args, const AttnPlan& p, int 
   a2.seg2_block = p.nqb1 * B * H;
   a2.seg2_q0 = p.nqb1 * wgq_of(p.c1);
   a2.nqb2 = p.nqb2;
+  a2.dv_nqb = make_div((uint32_t)p.nqb1);
+  a2.dv_nqb2 = make_div((uint32_t)(p.nqb2 > 0 ? p.nqb2 : 1));
+  a2.dv_H = make_div((uint32_t)H);
   dim3 grid((p.nqb1 + p.nqb2) * B * H);
   return launch_kernel(relpos_attn_core<DK, KS1, NTL1, KS2, NTL2, WIDE>, grid, dim3(64 * ATTN_WAVES),
                        (uint32_t)shmem, st, ev, a2);
@@ -974,13 +981,13 @@ hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, i
   a.T = rs.T;
   a.T_al = rs.T_al;
   a.H = rs.H;
-  a.DK = rs.DK;
+  a.dks = rs.DK == 128 ? 7 : 6;
   a.d = rs.d;
   a.p_rows = rs.p_rows;
   a.p_base = rs.p_base;
-  const long rows = which == 3 ? (long)(2 * rs.T - 1) : (long)rs.B * rs.T;
-  const long total = rows * rs.d;
-  hipLaunchKernelGGL(gather_intermediate, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a);
+  const dim3 grid((unsigned)((rs.d + 255) / 256), (unsigned)(which == 3 ? 2 * rs.T - 1 : rs.T),
+                  (unsigned)(which == 3 ? 1 : rs.B));
+  hipLaunchKernelGGL(gather_intermediate, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -27,14 +27,18 @@
 // to the eight XCDs in contiguous, roughly square groups of the tile grid, so the
 // operand rows one XCD touches fit its L2.
 //
-// Epilogue: the requantization y = clamp8(floor((acc m + 2^(n-1)) / 2^n)) is
-// evaluated exactly in float64 as floor(acc * (m 2^-n) + 128.5) clamped to [1, 255],
-// the biased code y + 128: |acc m| < 2^51, so acc * (m 2^-n) + 128.5 is a multiple of
-// 2^-n below 2^52 units and the fused multiply-add is exact.  Each lane then owns 4
-// consecutive outputs per accumulator group; one exchange with the lane 32 away gives
-// it 16 consecutive bytes, stored with one 16-byte write.  Channel-major V^T is
-// produced by swapping the MFMA operands in the waves whose channels are V, so that
-// its 16-byte pieces run along tokens.
+// Epilogue: the requantization y = clamp8(floor((acc m + 2^(n-1)) / 2^n)) in integers.
+// When every channel of the matrix allows it (n <= 16, m' = m 2^(16-n) < 2^23 and
+// one clamp bound A for all channels, at least ceil(2^23 / m') + 1 for each, with
+// A m' + 2^15 < 2^31), the accumulator is first clamped to [-A, A] (beyond a channel's
+// own bound the result saturates anyway), then one 24-bit multiply-add gives
+// t = a m' + 2^15, whose clamp to [-127 2^16, 127 2^16 + 2^16 - 1] holds the int8
+// result in byte 2: three full-rate instructions per value, one multiplier register per
+// value, and a byte permute gathers four results into a dword.  Otherwise the value
+// is evaluated in 64-bit integers, its constants read from LDS per value.  Each lane owns 4 consecutive outputs per accumulator group; one
+// exchange with the lane 32 away gives it 16 consecutive bytes, stored with one 16-byte
+// write.  Channel-major V^T is produced by swapping the MFMA operands in the waves whose
+// channels are V, so that its 16-byte pieces run along tokens.
 #include <type_traits>
 #include <utility>
 
@@ -54,13 +58,16 @@ enum Epilogue { EPI_PLAIN = 0, EPI_RESID = 1, EPI_SWISH = 2 };
 struct GemmProblem {
   const int8_t* x;      // [nb][rows][K] activations
   const int8_t* w;      // [N][K] weights
-  const double* scale;  // [N] m * 2^-n per output channel
+  const int32_t* req;   // [2][N] per output channel: multiplier, and shift in the wide form (Requant)
+  int wide;             // 64-bit evaluation
+  int clamp;            // the fast form's clamp bound
   int nb, rows, N, K;
   int mode;
   int tile_begin;   // first logical tile of this problem
   int tiles_n;      // tiles along N
   int tiles_m_per;  // token tiles per utterance
   int band;         // token tiles per band of the logical order
+  DivU dv_band_span, dv_band, dv_last_band, dv_tiles_m_per;  // divisors of the tile decomposition
 };
 
 struct GemmArgs {
@@ -95,40 +102,63 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// four biased codes -> four int8 bytes (code - 128 == code ^ 0x80 for code in [1, 255])
-__device__ __forceinline__ uint32_t pack4(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3) {
-  return (c0 | (c1 << 8) | (c2 << 16) | (c3 << 24)) ^ 0x80808080u;
+// byte 2 of four words -> one dword (v_perm_b32 selector bytes: 0-3 pick the second
+// operand's bytes, 4-7 the first's, 0x0c a zero byte)
+__device__ __forceinline__ uint32_t pack_b2(uint32_t v0, uint32_t v1, uint32_t v2, uint32_t v3) {
+  return __builtin_amdgcn_perm(v1, v0, 0x0c0c0602u) | __builtin_amdgcn_perm(v3, v2, 0x06020c0cu);
 }
 
-// int8 codes of the 16 accumulators of one MFMA output block (exact, see the header
-// comment), packed four per dword: D[g] holds elements 4g .. 4g + 3.  All sixteen
-// products are formed before any is converted, and the conversions go four to an asm
-// statement, so independent values overlap instead of running as one long chain.
-// v_cvt_i32_f64 truncates and saturates to the int32 range; truncation equals the
-// floor wherever the clamp to [1, 255] does not decide the result (t >= 1).
-// With SW, each code goes through the Swish table `stab` (LDS) instead.
+// v_med3_i32 with the low bound in a scalar register and the high one in a vector
+// register (the compiler forms med3 from min/max only with constant bounds)
+__device__ __forceinline__ int med3_sv(int x, int lo, int hi) {
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(lo), "v"(hi));
+  return r;
+}
+
+// a b + c for a, b in the signed 24-bit range (v_mad_i32_i24; the compiler cannot
+// see the range of a clamp to runtime bounds and would sign-extend both first)
+__device__ __forceinline__ int mad24_s(int a, int b, int c) {
+  int r;
+  asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(c));
+  return r;
+}
+
+// Eq. 7 on the 16 accumulators of one MFMA output block, fast form: m[e] is element
+// e's multiplier m', -A and A (negA, Av) the matrix's clamp bounds; v[e] receives the
+// int8 result in byte 2.
+__device__ __forceinline__ void requant16_fast(const v16i& a, const int (&m)[16], int negA, int Av, int (&v)[16]) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int c = med3_sv(a[e], negA, Av);
+    v[e] = min(max(mad24_s(c, m[e], 1 << 15), -127 * 65536), 127 * 65536 + 65535);
+  }
+}
+
+// The wide form: element e's multiplier and shift are sm[ch(e)], sn[ch(e)] (LDS).
+template <typename CH>
+__device__ __forceinline__ void requant16_wide(const v16i& a, const int* sm, const int* sn, CH ch, int (&v)[16]) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int m = sm[ch(e)], n = sn[ch(e)];
+    const long long q = ((long long)a[e] * m + (1ll << (n - 1))) >> n;
+    v[e] = (int)(q < -127 ? -127 : (q > 127 ? 127 : q)) << 16;
+  }
+}
+
+// The 16 results (byte 2 of v[e]) packed four per dword: D[g] holds elements 4g .. 4g + 3.
+// With SW, each int8 result h goes through the Swish table `stab` (LDS, indexed by h + 128).
 template <bool SW = false>
-__device__ __forceinline__ void requant16(const v16i& a, const double (&sc)[16], uint32_t (&D)[4],
-                                          const uint8_t* stab = nullptr) {
-  double t[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) t[e] = __builtin_fma((double)a[e], sc[e], 128.5);
-  int v[16];
-#pragma unroll
-  for (int g = 0; g < 4; ++g)
-    asm("v_cvt_i32_f64 %0, %4\n\tv_cvt_i32_f64 %1, %5\n\tv_cvt_i32_f64 %2, %6\n\tv_cvt_i32_f64 %3, %7"
-        : "=&v"(v[4 * g]), "=&v"(v[4 * g + 1]), "=&v"(v[4 * g + 2]), "=&v"(v[4 * g + 3])
-        : "v"(t[4 * g]), "v"(t[4 * g + 1]), "v"(t[4 * g + 2]), "v"(t[4 * g + 3]));
+__device__ __forceinline__ void pack16(const int (&v)[16], uint32_t (&D)[4], const uint8_t* stab = nullptr) {
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
     if constexpr (SW) {
       uint32_t o[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = stab[min(max(v[4 * g + e], 1), 255)];
+      for (int e = 0; e < 4; ++e) o[e] = stab[(((uint32_t)v[4 * g + e] >> 16) & 0xffu) ^ 0x80u];
       D[g] = o[0] | (o[1] << 8) | (o[2] << 16) | (o[3] << 24);
     } else {
-      D[g] = pack4((uint32_t)min(max(v[4 * g], 1), 255), (uint32_t)min(max(v[4 * g + 1], 1), 255),
-                   (uint32_t)min(max(v[4 * g + 2], 1), 255), (uint32_t)min(max(v[4 * g + 3], 1), 255));
+      D[g] = pack_b2((uint32_t)v[4 * g], (uint32_t)v[4 * g + 1], (uint32_t)v[4 * g + 2], (uint32_t)v[4 * g + 3]);
     }
   }
 }
@@ -158,8 +188,10 @@ __device__ __forceinline__ v4i residual16(const v4i& y, const v4i& z, int m_z, i
 // fragments from memory straight into registers, one K step ahead, and only the token
 // tile goes through LDS.  EPI: the epilogue of row-major outputs.  TPF: register sets of
 // the token tile in flight (2 fetches each step's tile two steps before it is stored, for
-// long K loops whose operands come from beyond the L2).
-template <int TN, int TM, int NWAVE, int WN, int EPI, int TPF>
+// long K loops whose operands come from beyond the L2).  WIDE: some problem of the
+// launch takes the wide form of Eq. 7 (its code costs registers even where unused, so
+// launches in the fast form alone leave it out).
+template <int TN, int TM, int NWAVE, int WN, int EPI, int TPF, bool WIDE>
 __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int NTH = 64 * NWAVE;
   constexpr int WM = NWAVE / WN;            // waves along M
@@ -174,7 +206,7 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int CPW = WTM >= KCHUNK ? WTM / KCHUNK : 1;  // 64-key chunks per wave (V sums)
   // two LDS buffers: the next K step is stored while the current one is multiplied
   __shared__ __align__(16) int8_t sx[2][TM * BK];
-  __shared__ double ssc[TN];
+  __shared__ __align__(16) int sreq[2][TN];  // Eq. 7 constants of the tile's channels
   __shared__ uint32_t stab32[EPI == EPI_SWISH ? 64 : 1];  // the Swish table (read after the K loop)
 
   // XCD-aware deal: workgroup i runs on XCD i % 8; XCD x owns logical tiles
@@ -184,28 +216,37 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   if (tile >= args.tiles_total) return;
   const int pi = (args.nprob > 1 && tile >= args.prob[1].tile_begin) ? 1 : 0;
   const GemmProblem& P = args.prob[pi];
+  // the problem's scalars, all loaded at once: left alone the compiler loads each one
+  // where it is first used, and every division below would wait for its own load
+  int tile_begin = P.tile_begin, nb = P.nb, tiles_m_per = P.tiles_m_per, band = P.band, tiles_n = P.tiles_n;
+  uint32_t m_span = P.dv_band_span.m, m_band = P.dv_band.m, m_last = P.dv_last_band.m, m_tmp = P.dv_tiles_m_per.m;
+  int K = P.K, rows = P.rows, N = P.N, mode = P.mode;
+  asm volatile(""
+               : "+s"(tile_begin), "+s"(nb), "+s"(tiles_m_per), "+s"(band), "+s"(tiles_n), "+s"(m_span), "+s"(m_band),
+                 "+s"(m_last), "+s"(m_tmp), "+s"(K), "+s"(rows), "+s"(N), "+s"(mode));
   // logical order inside a problem: bands of `band` token tiles, channels outer,
   // tokens inner within a band
-  const int local = tile - P.tile_begin;
-  const int tiles_m = P.nb * P.tiles_m_per;
-  const int band_idx = local / (P.band * P.tiles_n);
-  const int in_band = local - band_idx * P.band * P.tiles_n;
-  const int band_m = min(P.band, tiles_m - band_idx * P.band);
-  const int nt = in_band / band_m;
-  const int mt = band_idx * P.band + (in_band - nt * band_m);
-  // the divisions above run on the vector unit: readfirstlane keeps the tile
-  // coordinates (and the buffer descriptors built from them) in scalar registers
-  const int n0 = __builtin_amdgcn_readfirstlane(nt * TN);
-  const int ub = __builtin_amdgcn_readfirstlane(mt / P.tiles_m_per);                  // utterance
-  const int t0 = __builtin_amdgcn_readfirstlane((mt - (mt / P.tiles_m_per) * P.tiles_m_per) * TM);  // first token
-  const int K = __builtin_amdgcn_readfirstlane(P.K), rows = __builtin_amdgcn_readfirstlane(P.rows);
-  const int N = __builtin_amdgcn_readfirstlane(P.N), mode = __builtin_amdgcn_readfirstlane(P.mode);
+  const int local = tile - tile_begin;
+  const int tiles_m = nb * tiles_m_per;
+  const int band_idx = (int)div_u(local, DivU{0u, m_span});
+  const int in_band = local - band_idx * band * tiles_n;
+  const int band_m = min(band, tiles_m - band_idx * band);
+  const int nt = (int)div_u(in_band, DivU{0u, band_m == band ? m_band : m_last});
+  const int mt = band_idx * band + (in_band - nt * band_m);
+  const int n0 = nt * TN;
+  const int ub = (int)div_u(mt, DivU{0u, m_tmp});  // utterance
+  const int t0 = (mt - ub * tiles_m_per) * TM;      // first token
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave % WN, wm = wave / WN;
 
-  if (tid < TN) ssc[tid] = P.scale[min(n0 + tid, N - 1)];
+  if (tid < TN) {
+    const int c = min(n0 + tid, N - 1);
+    sreq[0][tid] = P.req[c];
+    sreq[1][tid] = P.req[N + c];
+  }
+  const int rq_wide = WIDE ? __builtin_amdgcn_readfirstlane(P.wide) : 0, rq_clamp = __builtin_amdgcn_readfirstlane(P.clamp);
   if (EPI == EPI_SWISH && tid < 64) stab32[tid] = ((const uint32_t*)args.swtab)[tid];
 
   // thread -> (row, chunk) of the fetch: 8 threads cover one 128-byte row segment.
@@ -368,18 +409,22 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
       dst = args.y + (size_t)ub * rows * N + nb;
       zsrc = args.z1 + (size_t)ub * rows * N + nb;
     }
-    // the scales of this sub-tile's channels, the same for all its token columns
-    double sc[16];
+    // the tile-local channel of element e: with rows as tokens (V^T) the column, else
+    // row g * 8 + half * 4 + e' of element e = 4g + e'
+    auto chan = [&](int e) { return vwave ? nl + col : nl + (e >> 2) * 8 + half * 4 + (e & 3); };
+    // the fast form's multipliers, the same for all the sub-tile's token columns
+    int mc[16];
     if (vwave) {
-      // rows are tokens, the column is the channel
-      const double s1 = ssc[nl + col];
+      const int m1 = sreq[0][nl + col];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sc[e] = s1;
+      for (int e = 0; e < 16; ++e) mc[e] = m1;
     } else {
-      // rows are channels (element 4g + e is channel g * 8 + half * 4 + e), the
-      // column is the token
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sc[e] = ssc[nl + (e >> 2) * 8 + half * 4 + (e & 3)];
+      for (int g = 0; g < 4; ++g) {
+        const v4i q = *(const v4i*)&sreq[0][nl + g * 8 + half * 4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mc[4 * g + e] = q[e];
+      }
     }
     // this lane's destination for token column j = 0 (relative to dst, under 2^31),
     // the first token it stores and the bound on tokens: one 32-token column further
@@ -404,8 +449,17 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
     for (int c = 0; c < CPW; ++c) vpart[c] = 0;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
+      int v[16];
+      if (rq_wide) {
+        // a compiler barrier keeps the wide form's LDS reads here instead of letting
+        // them be hoisted into live registers next to the fast form's
+        asm volatile("" ::: "memory");
+        requant16_wide(acc[i][j], sreq[0], sreq[1], chan, v);
+      } else {
+        requant16_fast(acc[i][j], mc, -rq_clamp, rq_clamp, v);
+      }
       uint32_t D[4];
-      requant16<EPI == EPI_SWISH>(acc[i][j], sc, D, (const uint8_t*)stab32);
+      pack16<EPI == EPI_SWISH>(v, D, (const uint8_t*)stab32);
       const auto x02 = __builtin_amdgcn_permlane32_swap(D[0], D[2], false, false);
       const auto x13 = __builtin_amdgcn_permlane32_swap(D[1], D[3], false, false);
       v4i out = (v4i){(int)x02[0], (int)x02[1], (int)x13[0], (int)x13[1]};
@@ -438,12 +492,14 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   }
 }
 
-static int add_problem(GemmArgs& a, int idx, const int8_t* x, const int8_t* w, const double* scale, int nb,
+static int add_problem(GemmArgs& a, int idx, const int8_t* x, const int8_t* w, const Requant& rq, int nb,
                        int rows, int N, int K, int mode, int tile_begin, int TN, int TM) {
   GemmProblem& p = a.prob[idx];
   p.x = x;
   p.w = w;
-  p.scale = scale;
+  p.req = rq.req;
+  p.wide = rq.wide;
+  p.clamp = rq.clamp;
   p.nb = nb;
   p.rows = rows;
   p.N = N;
@@ -460,6 +516,11 @@ static int add_problem(GemmArgs& a, int idx, const int8_t* x, const int8_t* w, c
   const double share = (tiles + 7) / 8;
   const int band = (int)(sqrt(share * TN / TM) + 0.5);
   p.band = band < 1 ? 1 : (band > tiles_m ? tiles_m : band);
+  const int last = tiles_m - (tiles_m - 1) / p.band * p.band;  // token tiles of the last band
+  p.dv_band_span = make_div((uint32_t)(p.band * p.tiles_n));
+  p.dv_band = make_div((uint32_t)p.band);
+  p.dv_last_band = make_div((uint32_t)last);
+  p.dv_tiles_m_per = make_div((uint32_t)p.tiles_m_per);
   return tiles;
 }
 
@@ -483,8 +544,11 @@ template <int TN, int TM, int NWAVE, int WN, int EPI = EPI_PLAIN, int TPF = 1>
 static hipError_t launch_gemm(GemmArgs& a, int tiles, hipStream_t st, const LaunchEv& ev) {
   a.tiles_total = tiles;
   a.per_xcd = (tiles + 7) / 8;
-  return launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI, TPF>, dim3(8 * a.per_xcd), dim3(64 * NWAVE), 0, st, ev,
-                       a);
+  const bool wide = a.prob[0].wide || (a.nprob > 1 && a.prob[1].wide);
+  return wide ? launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI, TPF, true>, dim3(8 * a.per_xcd), dim3(64 * NWAVE),
+                              0, st, ev, a)
+              : launch_kernel(gemm_i8_requant<TN, TM, NWAVE, WN, EPI, TPF, false>, dim3(8 * a.per_xcd),
+                              dim3(64 * NWAVE), 0, st, ev, a);
 }
 
 // Token-tile height for a launch of `tiles_of(TM)` tiles: every tile of a launch runs at
@@ -518,10 +582,10 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
     static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
     GemmArgs a{};
     fill_dest(a, rs, ws, nullptr);
-    int tiles = add_problem(a, 0, x, w.w_qkv, w.scale_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
+    int tiles = add_problem(a, 0, x, w.w_qkv, w.rq_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
     a.nprob = 1;
     if (pos_table) {
-      tiles += add_problem(a, 1, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
+      tiles += add_problem(a, 1, pos_table, w.w_pos, w.rq_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
       a.nprob = 2;
     }
     return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
@@ -536,7 +600,7 @@ hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p
   ws.p = p;
   fill_dest(a, rs, ws, nullptr);
   constexpr int TN = 256, TM = 256, NWAVE = 8, WN = 4;
-  const int tiles = add_problem(a, 0, pos_table, w.w_pos, w.scale_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, 0, TN, TM);
+  const int tiles = add_problem(a, 0, pos_table, w.w_pos, w.rq_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, 0, TN, TM);
   a.nprob = 1;
   return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, LaunchEv{});
 }
@@ -554,7 +618,7 @@ hipError_t launch_out_projection(const RunShape& rs, const Weights& w, const Wor
   // small tiles (640 at T = 2500): with K = d_model and few 64-token blocks the launch
   // is bound by load latency, and larger tiles measured no faster
   constexpr int TN = 64, TM = 64, NWAVE = 4, WN = 2;
-  int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.scale_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
+  int tiles = add_problem(a, 0, ws.ctx, w.w_out, w.rq_out, rs.B, rs.T, rs.d, rs.d, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
   // the token tile two steps ahead: 0.6 - 0.7 us less per call at T = 2500 (interleaved A/B)
   if (res) return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID, 2>(a, tiles, st, ev);
@@ -585,7 +649,7 @@ hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long l
   return hipGetLastError();
 }
 
-hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
+hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const Requant& rq1,
                          const uint8_t* swtab, int8_t* o, hipStream_t st) {
   // 256-channel tiles of eight waves; 192-token tiles when they need no more rounds
   // over the CUs than 256-token ones (2500 rows: 224 tiles instead of 160 of 4/3 the work)
@@ -596,7 +660,7 @@ hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_
     GemmArgs a{};
     a.y = o;
     a.swtab = swtab;
-    const int tiles = add_problem(a, 0, x, w1, scale1, 1, rows, d_ff, d, OUT_ROWMAJOR, 0, TN, TM);
+    const int tiles = add_problem(a, 0, x, w1, rq1, 1, rows, d_ff, d, OUT_ROWMAJOR, 0, TN, TM);
     a.nprob = 1;
     return launch_gemm<TN, TM, NWAVE, WN, EPI_SWISH>(a, tiles, st, LaunchEv{});
   };
@@ -604,7 +668,7 @@ hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_
                                                    : go(std::integral_constant<int, 256>{});
 }
 
-hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const double* scale,
+hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const Requant& rq,
                                const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st) {
   GemmArgs a{};
   a.y = z_out;
@@ -616,12 +680,12 @@ hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const in
   // module's W2 (K = d_ff) measured against 64 x 64, 128 x 64, 128 x 96, 64 x 192,
   // 256 x 128 and 128 x 256 tiles at 2500 and 4000 rows
   constexpr int TN = 128, TM = 128, NWAVE = 8, WN = 4;
-  const int tiles = add_problem(a, 0, x, w, scale, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
+  const int tiles = add_problem(a, 0, x, w, rq, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
   a.nprob = 1;
   return launch_gemm<TN, TM, NWAVE, WN, EPI_RESID>(a, tiles, st, LaunchEv{});
 }
 
-hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const double* scale, int8_t* y,
+hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const Requant& rq, int8_t* y,
                          hipStream_t st) {
   constexpr int TN = 256, NWAVE = 8, WN = 4;
   auto tiles_of = [&](int tm) { return (long)((rows + tm - 1) / tm) * ((N + TN - 1) / TN); };
@@ -631,7 +695,7 @@ hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* 
     constexpr int TM = decltype(tm_tag)::value;
     GemmArgs a{};
     a.y = y;
-    const int tiles = add_problem(a, 0, x, w, scale, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
+    const int tiles = add_problem(a, 0, x, w, rq, 1, rows, N, K, OUT_ROWMAJOR, 0, TN, TM);
     a.nprob = 1;
     return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, LaunchEv{});
   };
@@ -642,13 +706,12 @@ hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* 
 
 // one thread per 16-byte piece of the destination
 __global__ __launch_bounds__(256) void pack_wfrag(const int8_t* __restrict__ w, int8_t* __restrict__ dst, int N,
-                                                  int K) {
+                                                  int K, DivU dv_ksl) {
   const long p = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= (long)N * K / 16) return;
   const int l = (int)(p & 63);
-  const long frag = p >> 6;
-  const int ksl = K >> 5;
-  const int cb = (int)(frag / ksl), ks = (int)(frag - (long)cb * ksl);
+  const int frag = (int)(p >> 6);
+  const int cb = (int)div_u((uint32_t)frag, dv_ksl), ks = frag - cb * (int)dv_ksl.d;
   const int8_t* src = w + (size_t)(cb * 32 + (l & 31)) * K + ks * 32 + (l >> 5) * 16;
   *(uint4*)(dst + p * 16) = *(const uint4*)src;
 }
@@ -656,7 +719,8 @@ __global__ __launch_bounds__(256) void pack_wfrag(const int8_t* __restrict__ w, 
 hipError_t pack_weight_fragments(const int8_t* w, int8_t* dst, int N, int K, hipStream_t st) {
   if (N % 32 || K % 32) return hipErrorInvalidValue;
   const long pieces = (long)N * K / 16;
-  hipLaunchKernelGGL(pack_wfrag, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, st, w, dst, N, K);
+  hipLaunchKernelGGL(pack_wfrag, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, st, w, dst, N, K,
+                     make_div((uint32_t)(K >> 5)));
   return hipGetLastError();
 }
 

@@ -140,6 +140,60 @@ static hipError_t dev_alloc(H* h, T** p, size_t count) {
   return hipSuccess;
 }
 
+// Eq. 7 constants of `parts` stacked matrices of N channels each (Requant): the fast
+// form when every part's shift is at most 16 and one clamp bound serves every channel,
+// the wide form otherwise.  Returns the wide flag; `out` receives the 2 parts N values
+// and `clamp` the fast form's bound.
+static int build_requant(const int32_t* const* mults, const int32_t* shifts, int parts, int N,
+                         std::vector<int32_t>& out, int32_t* clamp) {
+  const size_t NT = (size_t)parts * N;
+  out.assign(2 * NT, 0);
+  *clamp = 0;
+  bool fast = true;
+  int64_t A = 0, mmax = 0;  // the largest channel bound and multiplier
+  for (int p = 0; p < parts && fast; ++p) {
+    const int n = shifts[p];
+    if (n > 16) {
+      fast = false;
+      break;
+    }
+    for (int c = 0; c < N && fast; ++c) {
+      const int64_t m1 = (int64_t)mults[p][c] << (16 - n);
+      fast = m1 < ((int64_t)1 << 23);
+      out[(size_t)p * N + c] = (int32_t)m1;
+      if (m1 > 0) {
+        const int64_t Ac = (((int64_t)1 << 23) + m1 - 1) / m1 + 1;
+        A = Ac > A ? Ac : A;
+        mmax = m1 > mmax ? m1 : mmax;
+      }
+    }
+  }
+  fast = fast && A < ((int64_t)1 << 23) && A * mmax + (1 << 15) < ((int64_t)1 << 31);
+  if (fast) {
+    *clamp = (int32_t)A;
+    return 0;
+  }
+  for (int p = 0; p < parts; ++p)
+    for (int c = 0; c < N; ++c) {
+      out[(size_t)p * N + c] = mults[p][c];
+      out[NT + (size_t)p * N + c] = shifts[p];
+    }
+  return 1;
+}
+
+// Builds and uploads a matrix's Eq. 7 constants into a device buffer of the handle.
+template <typename H>
+static hipError_t upload_requant(H* h, Requant* rq, const int32_t* const* mults, const int32_t* shifts, int parts,
+                                 int N) {
+  std::vector<int32_t> host;
+  rq->wide = build_requant(mults, shifts, parts, N, host, &rq->clamp);
+  int32_t* dev = nullptr;
+  hipError_t e = dev_alloc(h, &dev, host.size());
+  if (e == hipSuccess) e = hipMemcpy(dev, host.data(), host.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+  rq->req = dev;
+  return e;
+}
+
 extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t** out) {
   g_last_error[0] = 0;
   if (!out) return fail(IPK_ERR_INVALID_ARG, "out is NULL");
@@ -192,9 +246,6 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->w.u, H * DK));
   chk(dev_alloc(h, &h->w.v, H * DK));
   chk(dev_alloc(h, &h->w.etab, 256));
-  chk(dev_alloc(h, &h->w.scale_qkv, 3 * d));
-  chk(dev_alloc(h, &h->w.scale_pos, d));
-  chk(dev_alloc(h, &h->w.scale_out, d));
   chk(dev_alloc(h, &h->ws.q, Bm * H * T_al * DK));
   chk(dev_alloc(h, &h->ws.k, Bm * H * T_al * DK));
   chk(dev_alloc(h, &h->ws.vt, Bm * H * DK * T_al));
@@ -224,18 +275,14 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(hipMemcpy(h->w.u, desc->pos_bias_u, H * DK, hipMemcpyDefault));
   chk(hipMemcpy(h->w.v, desc->pos_bias_v, H * DK, hipMemcpyDefault));
   chk(launch_iexp_table(h->w.etab, desc->q_ln2, desc->q_b, desc->q_c, nullptr));
-  // Eq. 7 scales m * 2^-n: m < 2^23 and n <= 40, so each is an exact double
-  std::vector<double> sq(3 * d), sp(d), so(d);
-  for (size_t c = 0; c < d; ++c) {
-    sq[c] = ldexp((double)desc->mult_q[c], -desc->shift_q);
-    sq[d + c] = ldexp((double)desc->mult_k[c], -desc->shift_k);
-    sq[2 * d + c] = ldexp((double)desc->mult_v[c], -desc->shift_v);
-    sp[c] = ldexp((double)desc->mult_pos[c], -desc->shift_pos);
-    so[c] = ldexp((double)desc->mult_out[c], -desc->shift_out);
+  // Eq. 7 constants per output channel (integers only)
+  {
+    const int32_t* mq[3] = {desc->mult_q, desc->mult_k, desc->mult_v};
+    const int32_t sq[3] = {desc->shift_q, desc->shift_k, desc->shift_v};
+    chk(upload_requant(h, &h->w.rq_qkv, mq, sq, 3, (int)d));
+    chk(upload_requant(h, &h->w.rq_pos, &desc->mult_pos, &desc->shift_pos, 1, (int)d));
+    chk(upload_requant(h, &h->w.rq_out, &desc->mult_out, &desc->shift_out, 1, (int)d));
   }
-  chk(hipMemcpy(h->w.scale_qkv, sq.data(), 3 * d * sizeof(double), hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.scale_pos, sp.data(), d * sizeof(double), hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->w.scale_out, so.data(), d * sizeof(double), hipMemcpyHostToDevice));
   // deterministic contents for the padding rows of the workspace
   chk(hipMemset(h->ws.p, 0, H * PR * DK));
   chk(hipMemset(h->ws.vt, 0, Bm * H * DK * T_al));
@@ -483,7 +530,7 @@ struct ipk_ffn {
   int device;
   int d, f, max_rows;
   int8_t *w1, *w2;            // fragment order (wfrag_index)
-  double *scale1, *scale2;    // m 2^-n per output channel
+  Requant rq1, rq2;           // Eq. 7 constants of W1 and W2
   uint8_t* swtab;             // 256 bytes: Swish output of each biased code h + 128
   int8_t *x, *o;              // LayerNorm output [max_rows][d], Swish output [max_rows][f]
   Residual res;
@@ -564,8 +611,6 @@ extern "C" int ipk_ffn_create(const ipk_ffn_desc* desc, ipk_ffn_t** out) {
   int8_t* stage = nullptr;
   chk(dev_alloc(h, &h->w1, f * d));
   chk(dev_alloc(h, &h->w2, d * f));
-  chk(dev_alloc(h, &h->scale1, f));
-  chk(dev_alloc(h, &h->scale2, d));
   chk(dev_alloc(h, &h->swtab, 256));
   chk(dev_alloc(h, &h->x, R * d));
   chk(dev_alloc(h, &h->o, R * f));
@@ -582,11 +627,8 @@ extern "C" int ipk_ffn_create(const ipk_ffn_desc* desc, ipk_ffn_t** out) {
   chk(pack_weight_fragments(stage, h->w1, (int)f, (int)d, nullptr));
   chk(hipMemcpy(stage, desc->w2, d * f, hipMemcpyDefault));
   chk(pack_weight_fragments(stage, h->w2, (int)d, (int)f, nullptr));
-  std::vector<double> s1(f), s2(d);
-  for (size_t k = 0; k < f; ++k) s1[k] = ldexp((double)desc->mult1[k], -desc->shift1);
-  for (size_t k = 0; k < d; ++k) s2[k] = ldexp((double)desc->mult2[k], -desc->shift2);
-  chk(hipMemcpy(h->scale1, s1.data(), f * sizeof(double), hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->scale2, s2.data(), d * sizeof(double), hipMemcpyHostToDevice));
+  chk(upload_requant(h, &h->rq1, &desc->mult1, &desc->shift1, 1, (int)f));
+  chk(upload_requant(h, &h->rq2, &desc->mult2, &desc->shift2, 1, (int)d));
   std::vector<int64_t> cb(d);
   for (size_t k = 0; k < d; ++k) cb[k] = desc->ln_bias[k] + ((int64_t)1 << (desc->ln_shift - 1));
   chk(hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
@@ -625,9 +667,9 @@ extern "C" int ipk_ffn_run(ipk_ffn_t* h, const int8_t* z, int32_t rows, int8_t* 
     return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
-  if (e == hipSuccess) e = launch_ffn_up(h->x, rows, h->d, h->f, h->w1, h->scale1, h->swtab, h->o, st);
+  if (e == hipSuccess) e = launch_ffn_up(h->x, rows, h->d, h->f, h->w1, h->rq1, h->swtab, h->o, st);
   if (e == hipSuccess)
-    e = launch_linear_resid(h->o, rows, h->d, h->f, h->w2, h->scale2, z, h->res.m_z, h->res.m_y, h->res.shift_r, z_out,
+    e = launch_linear_resid(h->o, rows, h->d, h->f, h->w2, h->rq2, z, h->res.m_z, h->res.m_y, h->res.shift_r, z_out,
                             st);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last_rows = rows;
@@ -665,7 +707,7 @@ struct ipk_conv {
   int device;
   int d, max_B, max_T;
   int8_t *w_pw1, *w_pw2;        // fragment order (wfrag_index)
-  double *scale_pw1, *scale_pw2;
+  Requant rq_pw1, rq_pw2;       // Eq. 7 constants of PW1 and PW2
   ConvMiddle mid;               // depthwise weights and constants (device copies)
   int8_t *x, *u, *o;            // LayerNorm output, PW1 output [.][2 d], Swish output
   int16_t* v;                   // int16 BatchNorm output
@@ -769,8 +811,6 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   int64_t* c = nullptr;
   chk(dev_alloc(h, &h->w_pw1, 2 * d * d));
   chk(dev_alloc(h, &h->w_pw2, d * d));
-  chk(dev_alloc(h, &h->scale_pw1, 2 * d));
-  chk(dev_alloc(h, &h->scale_pw2, d));
   chk(dev_alloc(h, &wdw, d * 9));
   chk(dev_alloc(h, &bias, d));
   chk(dev_alloc(h, &mdw, d));
@@ -794,11 +834,8 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   chk(hipMemcpy(stage, desc->w_pw2, d * d, hipMemcpyDefault));
   chk(pack_weight_fragments(stage, h->w_pw2, (int)d, (int)d, nullptr));
   chk(hipMemcpy(wdw, desc->w_dw, d * 9, hipMemcpyDefault));
-  std::vector<double> s1(2 * d), s2(d);
-  for (size_t k = 0; k < 2 * d; ++k) s1[k] = ldexp((double)desc->mult_pw1[k], -desc->shift_pw1);
-  for (size_t k = 0; k < d; ++k) s2[k] = ldexp((double)desc->mult_pw2[k], -desc->shift_pw2);
-  chk(hipMemcpy(h->scale_pw1, s1.data(), 2 * d * sizeof(double), hipMemcpyHostToDevice));
-  chk(hipMemcpy(h->scale_pw2, s2.data(), d * sizeof(double), hipMemcpyHostToDevice));
+  chk(upload_requant(h, &h->rq_pw1, &desc->mult_pw1, &desc->shift_pw1, 1, 2 * (int)d));
+  chk(upload_requant(h, &h->rq_pw2, &desc->mult_pw2, &desc->shift_pw2, 1, (int)d));
   chk(hipMemcpy(bias, desc->bias_dw, d * sizeof(int32_t), hipMemcpyHostToDevice));
   chk(hipMemcpy(mdw, desc->mult_dw, d * sizeof(int32_t), hipMemcpyHostToDevice));
   std::vector<int64_t> cb(d);
@@ -858,10 +895,10 @@ extern "C" int ipk_conv_run(ipk_conv_t* h, const int8_t* z, const int32_t* lengt
   hipStream_t st = (hipStream_t)stream;
   const int rows = B * T;
   hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
-  if (e == hipSuccess) e = launch_linear(h->x, rows, h->d, 2 * h->d, h->w_pw1, h->scale_pw1, h->u, st);
+  if (e == hipSuccess) e = launch_linear(h->x, rows, h->d, 2 * h->d, h->w_pw1, h->rq_pw1, h->u, st);
   if (e == hipSuccess) e = launch_conv_middle(h->mid, h->u, lens, B, T, h->d, h->o, h->v, st);
   if (e == hipSuccess)
-    e = launch_linear_resid(h->o, rows, h->d, h->d, h->w_pw2, h->scale_pw2, z, h->res.m_z, h->res.m_y,
+    e = launch_linear_resid(h->o, rows, h->d, h->d, h->w_pw2, h->rq_pw2, z, h->res.m_z, h->res.m_y,
                             h->res.shift_r, z_out, st);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last_B = B;

@@ -39,6 +39,19 @@ constexpr int P_PADHI = 128;  // rows kept after the last table row
 constexpr int BUF_WORD3 = 0x00020000;  // buffer resource word 3 for gfx9-family raw loads
 
 inline int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+// Division by a divisor known only at launch, in integers: the compiler's lowering of a
+// 32-bit division uses a floating-point reciprocal.  With m = floor(2^32 / d) + 1,
+// floor(x / d) = mulhi(x, m) exactly whenever x d < 2^32 (the error term x (m - 2^32/d)
+// / 2^32 stays below 1/d, the smallest gap to the next multiple); d = 1 has m = 0 and
+// passes x, through a select rather than a branch (no load waits on another).
+struct DivU {
+  uint32_t d, m;
+};
+inline DivU make_div(uint32_t d) { return DivU{d, d <= 1 ? 0u : (uint32_t)((1ull << 32) / d + 1)}; }
+__device__ __forceinline__ uint32_t div_u(uint32_t x, const DivU& v) {
+  return __umulhi(x, v.m) + (v.m == 0u ? x : 0u);
+}
 inline int t_aligned(int T) { return round_up(T, KCHUNK); }
 inline int p_rows(int T_al) { return P_PADLO + 2 * T_al + P_PADHI; }
 // Row of table row 0: the smallest value >= P_PADLO with (p_base + T - 1) % 16 == 0.
@@ -75,16 +88,33 @@ __host__ __device__ inline size_t wfrag_index(int n, int k, int K) {
          (k & 15);
 }
 
+// Eq. 7 requantization constants of one weight matrix's N output channels (a stack of
+// matrices, e.g. Q, K and V, shares one form), on the device as int32 [2][N]:
+//  * fast (wide == 0): every part has n <= 16; row 0 holds m' = m 2^(16-n) < 2^23, and
+//    `clamp` is one bound A for the whole matrix with A >= ceil(2^23 / m') + 1 for every
+//    channel, A < 2^23 and A max(m') + 2^15 < 2^31.  Then clamp8(RS(a, m, n)) =
+//    clamp8(floor((clamp(a, -A, A) m' + 2^15) / 2^16)): inside [-A, A] the value is the
+//    exact one, past it the result saturates either way (each channel's own bound is at
+//    most A), and the 24-bit product cannot overflow.  Such an A exists when the largest
+//    m' is below about 2^8 times the smallest nonzero one;
+//  * wide (wide == 1): row 0 holds m, row 1 the channel's shift n, and the epilogue
+//    evaluates Eq. 7 in 64-bit integers.
+struct Requant {
+  const int32_t* req;
+  int wide;
+  int clamp;  // A of the fast form
+};
+
 struct Weights {
   int8_t* w_qkv;       // [3d][d]: w_q, w_k, w_v stacked, in fragment order (wfrag_index)
   int8_t* w_pos;       // [d][d], in fragment order
   int8_t* w_out;       // [d][d], in fragment order
   int8_t *u, *v;       // [H][DK]
   uint32_t* etab;      // [256] I-BERT integer exp of every score distance (0 at 255)
-  // per-output-channel requantization scales m * 2^-n (exact in float64)
-  double* scale_qkv;  // [3d]
-  double* scale_pos;  // [d]
-  double* scale_out;  // [d]
+  // Eq. 7 constants per output channel (Requant)
+  Requant rq_qkv;  // 3d channels: Q, K, V stacked (one form for the three)
+  Requant rq_pos;  // d channels
+  Requant rq_out;  // d channels
 };
 
 struct Scalars {
@@ -147,13 +177,13 @@ hipError_t launch_layernorm(const RunShape& rs, const Residual& r, const int8_t*
 // Swish in its epilogue (x [rows][d] -> o [rows][d_ff]), W2 with the residual add in
 // its epilogue (o -> z_out [rows][d]).
 hipError_t launch_swish_table(uint8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st);
-hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const double* scale1,
+hipError_t launch_ffn_up(const int8_t* x, int rows, int d, int d_ff, const int8_t* w1, const Requant& rq1,
                          const uint8_t* swtab, int8_t* o, hipStream_t st);
 // A row-major linear layer y = clamp8(RS(x W^T)) of `rows` rows (K -> N), and one with the
 // residual add z_out = clamp8(RS(m_z z + m_y y, 1, shift_r)) in its epilogue.
-hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const double* scale, int8_t* y,
+hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* w, const Requant& rq, int8_t* y,
                          hipStream_t st);
-hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const double* scale,
+hipError_t launch_linear_resid(const int8_t* x, int rows, int N, int K, const int8_t* w, const Requant& rq,
                                const int8_t* z, int m_z, int m_y, int shift_r, int8_t* z_out, hipStream_t st);
 
 // The middle of the convolution module (Eq. 5): GLU, depthwise convolution with folded

@@ -16,9 +16,9 @@
 // so the row is read once.  Both sums come from one pass: sum z and sum z^2 by
 // v_dot4 against ones and against z itself, and
 //   sum (z - mu)^2 = sum z^2 - 2 mu sum z + d mu^2
-// exactly in integers, and the wave sums are DPP adds.  floor(sqrt(v)) is the correctly
-// rounded double square root truncated and then checked against v (v < 2^31, so the
-// double is within one of the root and one correction step suffices either way).
+// exactly in integers, and the wave sums are DPP adds.  The mean (a binary search over
+// its 9-bit range), floor(sqrt(v)) (bit by bit) and floor(2^31 / sigma) (restoring
+// division) are wave-uniform integer sequences: no floating-point instruction runs.
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -48,10 +48,43 @@ __device__ __forceinline__ int wave_sum(int v) {
          __builtin_amdgcn_readlane(v, 48);
 }
 
-// floor(a / b) for b > 0
-__device__ __forceinline__ long long floor_div(long long a, long long b) {
-  const long long q = a / b;
-  return (q * b > a) ? q - 1 : q;
+// floor(x / D) for |x| <= 257 D / 2, D <= 2^15: the largest mu in [-256, 255] with
+// mu D <= x, by binary search (every product stays below 2^23 in magnitude)
+__device__ __forceinline__ int floor_div_small(int x, int D) {
+  int mu = -256;
+#pragma unroll
+  for (int step = 256; step >= 1; step >>= 1)
+    if ((mu + step) * D <= x) mu += step;
+  return mu;
+}
+
+// floor(sqrt(v)) for 0 <= v < 2^32, bit by bit
+__device__ __forceinline__ uint32_t isqrt_u32(uint32_t v) {
+  uint32_t res = 0, one = 1u << 30;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (v >= res + one) {
+      v -= res + one;
+      res = (res >> 1) + one;
+    } else {
+      res >>= 1;
+    }
+    one >>= 2;
+  }
+  return res;
+}
+
+// floor(2^31 / s) for 1 <= s < 2^16 by restoring division (the remainder stays below s)
+__device__ __forceinline__ uint32_t div_2p31(uint32_t s) {
+  uint32_t r = 1, q = 0;  // the dividend's only one bit, bit 31, enters first
+#pragma unroll
+  for (int i = 31; i >= 0; --i) {
+    const bool c = r >= s;
+    if (c) r -= s;
+    q |= (c ? 1u : 0u) << i;
+    r <<= 1;
+  }
+  return q;
 }
 
 // NP: 16-byte pieces per lane (d <= 1024 NP)
@@ -77,21 +110,17 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
   // |sum z| <= 128 d < 2^21 and sum z^2 <= 2^14 d < 2^29 for d <= 16384
   s = wave_sum(s);
   q = wave_sum(q);
-  const long long mu = floor_div(2ll * s + d, 2ll * d);
-  const long long var = (long long)q - 2 * mu * s + (long long)d * mu * mu;  // sum (z - mu)^2
-  long long sg = (long long)sqrt((double)var);
-  if (sg * sg > var) --sg;
-  if ((sg + 1) * (sg + 1) <= var) ++sg;
+  // mean, ties up: floor((2 sum z + d) / (2 d)), with |2 sum z + d| <= 257 d
+  const int mu = floor_div_small(2 * s + d, 2 * d);
+  const long long var = (long long)q - 2ll * mu * s + (long long)d * mu * mu;  // sum (z - mu)^2 < 2^31
+  uint32_t sg = isqrt_u32((uint32_t)var);
   if (sg < 1) sg = 1;
-  // floor(2^31 / sigma) from the correctly rounded double quotient: unless sigma divides
-  // 2^31 the quotient lies at least 1 / sigma >= 2^-16 below the next integer, far more
-  // than its rounding error (2^31 2^-53), so truncating it gives the floor
-  const long long F = (long long)(2147483648.0 / (double)sg);
+  const long long F = div_2p31(sg);  // floor(2^31 / sigma), sigma < 2^16
   // u = floor(y F / 2) for y = z - mu, in 32 bits: with F = 2 Fh + Fo,
   // u = y Fh + Fo floor(y / 2), and |y Fh| <= |y| F / 2 <= 2^30 since |y| <= sigma
   const int Fh = (int)(F >> 1), Fo = (F & 1) ? -1 : 0;
   const int shift = a.shift;
-  const int m = (int)mu;
+  const int m = mu;
 #pragma unroll
   for (int k = 0; k < NP; ++k) {
     const int p = lane + 64 * k;
