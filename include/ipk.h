@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define IPK_ABI_VERSION 3
+#define IPK_ABI_VERSION 4
 
 /* Status codes. */
 typedef enum ipk_status {
@@ -127,14 +127,41 @@ int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t**
 int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
                         int32_t B, int32_t T, int8_t* y, void* stream);
 
+/*
+ * ipk_relpos_attn_run without any device allocation, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and errors as ipk_relpos_attn_run; the run's workspace (Q,
+ * K, V^T, the projected position table unless pos_table is NULL, the V sums and the
+ * context) lives in one static device array of IPK_NOALLOC_SCRATCH_BYTES per GPU
+ * instead of the handle's: the library's code object holds it, each GPU the library
+ * runs on keeps its copy until the process ends, and its address is looked up on the
+ * device's first call.  The call allocates nothing and calls no allocating routine.
+ * Workspace bytes, each part rounded up to 256:
+ *   3 B H T_al d_k + H (2 T_al + 256) d_k (only with a pos_table) + B T d_model
+ *   + 4 B H (T_al / 64) d_k,  T_al = T rounded up to 64
+ * (8 x 2500 frames at d_model 512, 8 heads: 45.1 MB).
+ * All no-allocation calls on one GPU share that array, whatever their handle or
+ * stream, and it keeps the last call's contents (nothing in it has to start at zero:
+ * every byte a run reads was written by the same run, or is masked): calls that
+ * overlap on one GPU race, so order them (one stream, or events).  After such a call,
+ * ipk_relpos_attn_intermediate reads the array, valid until the next one on the GPU.
+ * Errors: those of ipk_relpos_attn_run, and IPK_ERR_UNSUPPORTED when (B, T) needs more
+ * than IPK_NOALLOC_SCRATCH_BYTES (nothing is enqueued); IPK_ERR_HIP when the array's
+ * address cannot be looked up.
+ */
+#define IPK_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int ipk_relpos_attn_run_noalloc(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
+                                const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream);
+
 /* Frees the handle and its workspace after synchronizing the device; NULL is a no-op.
  * Returns IPK_OK (or IPK_ERR_HIP if the device reported an error). */
 int ipk_relpos_attn_destroy(ipk_relpos_attn_t* h);
 
 /*
- * Copies one intermediate of the last run from the handle's workspace into a
- * caller buffer (DEVICE pointer `dst` of `bytes` bytes), on `stream`, for tests and
- * debugging.  Layouts for the last run's (B, T):
+ * Copies one intermediate of the last run from its workspace (the handle's, or the
+ * GPU's shared array after ipk_relpos_attn_run_noalloc) into a caller buffer (DEVICE
+ * pointer `dst` of `bytes` bytes), on `stream`, for tests and debugging.  Layouts for
+ * the last run's (B, T):
  *   IPK_INTER_Q, IPK_INTER_K:  int8 [B][T][d_model]
  *   IPK_INTER_V:               int8 [B][T][d_model]
  *   IPK_INTER_P:               int8 [2T-1][d_model]

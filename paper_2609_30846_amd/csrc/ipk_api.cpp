@@ -33,7 +33,7 @@ struct ipk_relpos_attn {
   RunShape last;
   bool has_run;
   bool last_was_residual;
-  int8_t* last_p;  // buffer of the last run's projected table (ws.p or pcache)
+  Workspace last_ws;  // the last run's buffers (ws, the kept table, or the no-allocation array)
   hipEvent_t stage_ev[IPK_NUM_STAGES + 1];
   bool stages_pending;
   // projected position table kept by ipk_relpos_attn_cache_positions
@@ -226,7 +226,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   plan_fused_score(&h->sc, desc->d_k, false);
   h->has_run = false;
   h->last_was_residual = false;
-  h->last_p = nullptr;
+  h->last_ws = Workspace{};
   h->stages_pending = false;
   h->pcache = nullptr;
   h->pcache_T = 0;
@@ -301,11 +301,9 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   return IPK_OK;
 }
 
-// Validates a run's arguments and enqueues it: LayerNorm (z1 != NULL, the MHSA
-// module), projections, attention core, output projection (with the residual add
-// when z1 != NULL).
-static int enqueue_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths, int32_t B,
-                       int32_t T, int8_t* y, void* stream, const int8_t* z1) {
+// Validates a run's arguments and fills its shape and lengths.
+static int validate_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
+                        int32_t B, int32_t T, int8_t* y, RunShape* rs, Lengths* lens) {
   if (((uintptr_t)x | (uintptr_t)pos_table | (uintptr_t)y) & 15)
     return fail(IPK_ERR_INVALID_ARG, "the input, pos_table and output must be 16-byte aligned");
   if (B < 1 || B > h->max_B) return fail(IPK_ERR_INVALID_ARG, "B=%d outside [1, max_batch=%d]", B, h->max_B);
@@ -315,24 +313,30 @@ static int enqueue_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_ta
                 h->pcache_T ? "pos_table is NULL and the kept projection covers T <= %d only" :
                               "pos_table is NULL and no position projection is kept (T_table %d)",
                 h->pcache_T);
-  Lengths lens;
   for (int b = 0; b < B; ++b) {
     const int L = lengths ? lengths[b] : T;
     if (L < 1 || L > T) return fail(IPK_ERR_INVALID_ARG, "lengths[%d]=%d outside [1, T=%d]", b, L, T);
-    lens.len[b] = L;
+    lens->len[b] = L;
   }
-  for (int b = B; b < IPK_MAX_BATCH; ++b) lens.len[b] = 0;
+  for (int b = B; b < IPK_MAX_BATCH; ++b) lens->len[b] = 0;
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
     return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
-  RunShape rs{B, T, t_aligned(T), h->H, h->DK, h->d, p_base_row(T), p_rows(t_aligned(T))};
-  Workspace ws = h->ws;
+  *rs = RunShape{B, T, t_aligned(T), h->H, h->DK, h->d, p_base_row(T), p_rows(t_aligned(T))};
+  return IPK_OK;
+}
+
+// Enqueues a validated run on the buffers of `ws`: LayerNorm (z1 != NULL, the MHSA
+// module), projections, attention core, output projection (with the residual add when
+// z1 != NULL).  With pos_table NULL the kept projection replaces ws.p.
+static int enqueue_run(ipk_relpos_attn* h, RunShape rs, const Lengths& lens, Workspace ws, const int8_t* x,
+                       const int8_t* pos_table, int8_t* y, void* stream, const int8_t* z1) {
   if (!pos_table) {
     // table row r of this T is row r + T_table - T of the kept one, whose relative
     // position 0 sits at a 16-row boundary for every T
     ws.p = h->pcache;
     rs.p_rows = h->pcache_rows;
-    rs.p_base = p_base_row(h->pcache_T) + h->pcache_T - T;
+    rs.p_base = p_base_row(h->pcache_T) + h->pcache_T - rs.T;
   }
   hipStream_t st = (hipStream_t)stream;
   const bool rec = h->stages_pending;
@@ -356,17 +360,68 @@ static int enqueue_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_ta
   if (e == hipSuccess) e = launch_out_projection(rs, h->w, ws, y, st, ev[2], z1 ? &h->res : nullptr, z1);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;
-  h->last_p = ws.p;
+  h->last_ws = ws;
   h->has_run = true;
   h->last_was_residual = z1 != nullptr;
   return IPK_OK;
+}
+
+static int run_on_handle(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_table, const int32_t* lengths,
+                         int32_t B, int32_t T, int8_t* y, void* stream, const int8_t* z1) {
+  RunShape rs;
+  Lengths lens;
+  const int st = validate_run(h, x, pos_table, lengths, B, T, y, &rs, &lens);
+  if (st != IPK_OK) return st;
+  return enqueue_run(h, rs, lens, h->ws, x, pos_table, y, stream, z1);
 }
 
 extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
                                    const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream) {
   if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
   if (!x || !y) return fail(IPK_ERR_INVALID_ARG, "x and y must be non-NULL");
-  return enqueue_run(h, x, pos_table, lengths, B, T, y, stream, nullptr);
+  return run_on_handle(h, x, pos_table, lengths, B, T, y, stream, nullptr);
+}
+
+// Bytes of a run's workspace for (B, T) carved from one block at `base` (each buffer
+// at a 256-byte boundary), the projected table only when the run projects one; with
+// base = NULL only the size is computed.
+static size_t carve_workspace(const RunShape& rs, bool own_p, uint8_t* base, Workspace* ws) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    uint8_t* p = base ? base + off : nullptr;
+    off += (bytes + 255) & ~(size_t)255;
+    return p;
+  };
+  const size_t B = rs.B, H = rs.H, DK = rs.DK, T_al = rs.T_al;
+  ws->q = (int8_t*)take(B * H * T_al * DK);
+  ws->k = (int8_t*)take(B * H * T_al * DK);
+  ws->vt = (int8_t*)take(B * H * DK * T_al);
+  ws->p = own_p ? (int8_t*)take(H * (size_t)rs.p_rows * DK) : nullptr;
+  ws->ctx = (int8_t*)take(B * (size_t)rs.T * rs.d);
+  ws->vsum = (int32_t*)take(B * H * (T_al / KCHUNK) * DK * sizeof(int32_t));
+  ws->xln = nullptr;
+  return off;
+}
+
+extern "C" int ipk_relpos_attn_run_noalloc(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
+                                           const int32_t* lengths, int32_t B, int32_t T, int8_t* y, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!x || !y) return fail(IPK_ERR_INVALID_ARG, "x and y must be non-NULL");
+  RunShape rs;
+  Lengths lens;
+  const int st = validate_run(h, x, pos_table, lengths, B, T, y, &rs, &lens);
+  if (st != IPK_OK) return st;
+  Workspace ws{};
+  const size_t need = carve_workspace(rs, pos_table != nullptr, nullptr, &ws);
+  if (need > IPK_NOALLOC_SCRATCH_BYTES)
+    return fail(IPK_ERR_UNSUPPORTED, "B=%d, T=%d needs %zu bytes of workspace; the no-allocation run holds %zu", B, T,
+                need, (size_t)IPK_NOALLOC_SCRATCH_BYTES);
+  uint8_t* base = nullptr;
+  size_t cap = 0;
+  const hipError_t e = noalloc_scratch(&base, &cap);
+  if (e != hipSuccess) return fail(IPK_ERR_HIP, "looking up the scratch array failed: %s", hipGetErrorString(e));
+  carve_workspace(rs, pos_table != nullptr, base, &ws);
+  return enqueue_run(h, rs, lens, ws, x, pos_table, y, stream, nullptr);
 }
 
 extern "C" int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* pos_table,
@@ -379,7 +434,7 @@ extern "C" int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, con
     const uintptr_t a = (uintptr_t)z1, b = (uintptr_t)z2;
     if (a < b + n && b < a + n) return fail(IPK_ERR_INVALID_ARG, "z1 and z2 overlap without being equal");
   }
-  return enqueue_run(h, z1, pos_table, lengths, B, T, z2, stream, z1);
+  return run_on_handle(h, z1, pos_table, lengths, B, T, z2, stream, z1);
 }
 
 extern "C" int ipk_mhsa_residual_set(ipk_relpos_attn_t* h, const ipk_mhsa_residual_desc* r) {
@@ -479,9 +534,7 @@ extern "C" int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which,
   const RunShape& rs = h->last;
   const int64_t need = (which == IPK_INTER_P ? (int64_t)(2 * rs.T - 1) : (int64_t)rs.B * rs.T) * rs.d;
   if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
-  Workspace ws = h->ws;
-  ws.p = h->last_p;
-  hipError_t e = launch_gather_intermediate(rs, ws, which, (int8_t*)dst, (hipStream_t)stream);
+  hipError_t e = launch_gather_intermediate(rs, h->last_ws, which, (int8_t*)dst, (hipStream_t)stream);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "gather failed: %s", hipGetErrorString(e));
   return IPK_OK;
 }

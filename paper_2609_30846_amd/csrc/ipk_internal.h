@@ -219,6 +219,10 @@ AttnPlan attn_plan(int DK, int T_al, long bh_count, int T);
 // Rearranges a row-major int8 matrix [N][K] into fragment order (wfrag_index).
 hipError_t pack_weight_fragments(const int8_t* w, int8_t* dst, int N, int K, hipStream_t st);
 
+// The no-allocation run's workspace on the current device: a static device array of
+// `bytes` bytes (its address looked up once per device).
+hipError_t noalloc_scratch(uint8_t** base, size_t* bytes);
+
 hipError_t launch_gather_intermediate(const RunShape& rs, const Workspace& ws, int which, int8_t* dst,
                                       hipStream_t st);
 

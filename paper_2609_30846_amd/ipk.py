@@ -29,12 +29,14 @@ IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN
 IPK_FFN_X, IPK_FFN_O = range(2)
 IPK_CONV_X, IPK_CONV_U, IPK_CONV_V, IPK_CONV_O = range(4)
 IPK_SCORE_AUTO, IPK_SCORE_WIDE, IPK_SCORE_NARROW = range(3)
+IPK_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p
 SIGNATURES = [
     ("ipk_relpos_attn_create", C.c_int, [_vp, C.POINTER(_vp)]),
     ("ipk_relpos_attn_run", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
+    ("ipk_relpos_attn_run_noalloc", C.c_int, [_vp, _vp, _vp, _vp, C.c_int32, C.c_int32, _vp, _vp]),
     ("ipk_relpos_attn_destroy", C.c_int, [_vp]),
     ("ipk_relpos_attn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_relpos_attn_record_stages", C.c_int, [_vp, _vp]),
@@ -197,6 +199,16 @@ def ipk_relpos_attn_run(h: int, x, pos_table, lengths: Optional[Sequence[int]], 
                                       _stream_ptr(stream)))
 
 
+def ipk_relpos_attn_run_noalloc(h: int, x, pos_table, lengths: Optional[Sequence[int]], B: int, T: int, y,
+                                stream=None) -> None:
+    lens = None
+    if lengths is not None:
+        lens = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    lp = lens.ctypes.data if lens is not None else None
+    _check(load().ipk_relpos_attn_run_noalloc(h, _ptr(x), _ptr(pos_table), lp, int(B), int(T), _ptr(y),
+                                              _stream_ptr(stream)))
+
+
 def ipk_relpos_attn_set_score_path(h: int, path: int) -> None:
     _check(load().ipk_relpos_attn_set_score_path(h, int(path)))
 
@@ -299,6 +311,13 @@ class RelPosAttn:
         if y is None:
             y = torch.empty_like(x)
         ipk_relpos_attn_run(self.handle, x, pos_table, lengths, B, T, y, stream)
+        return y
+
+    def run_noalloc(self, x, pos_table, lengths=None, y=None, stream=None):
+        """As a call, with the run's workspace in the GPU's static no-allocation array
+        (ipk_relpos_attn_run_noalloc); ``y`` is the caller's output buffer."""
+        B, T, d = x.shape
+        ipk_relpos_attn_run_noalloc(self.handle, x, pos_table, lengths, B, T, y, stream)
         return y
 
     def cache_positions(self, pos_table, stream=None):

@@ -35,8 +35,14 @@ def test_library_exports_every_declared_symbol():
     assert sorted(n for n, _, _ in ipk.SIGNATURES) == declared
 
 
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define IPK_NOALLOC_SCRATCH_BYTES \((\d+)u \* 1024u \* 1024u\)", text)
+    assert m and int(m.group(1)) * 1024 * 1024 == ipk.IPK_NOALLOC_SCRATCH_BYTES
+
+
 def test_status_strings_and_version():
-    assert ipk.abi_version() == 3
+    assert ipk.abi_version() == 4
     assert ipk.status_name(0) == "IPK_OK"
     assert ipk.status_name(-1) == "IPK_ERR_INVALID_ARG"
     assert ipk.status_name(-2) == "IPK_ERR_UNSUPPORTED"
@@ -152,6 +158,7 @@ def test_null_arguments_rejected():
     assert lib.ipk_relpos_attn_create(None, C.byref(h)) == ipk.IPK_ERR_INVALID_ARG
     assert h.value is None
     assert lib.ipk_relpos_attn_run(None, None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_relpos_attn_run_noalloc(None, None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_relpos_attn_intermediate(None, 0, None, 0, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_relpos_attn_destroy(None) == ipk.IPK_OK
 
