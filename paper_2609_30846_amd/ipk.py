@@ -29,7 +29,7 @@ IPK_INTER_Q, IPK_INTER_K, IPK_INTER_V, IPK_INTER_P, IPK_INTER_CTX, IPK_INTER_XLN
 IPK_FFN_X, IPK_FFN_O = range(2)
 IPK_CONV_X, IPK_CONV_U, IPK_CONV_V, IPK_CONV_O = range(4)
 IPK_SCORE_AUTO, IPK_SCORE_WIDE, IPK_SCORE_NARROW = range(3)
-IPK_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
+IPK_NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
 
 # Every function the header declares, as (name, restype, argtypes).
 _vp = C.c_void_p

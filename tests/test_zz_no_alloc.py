@@ -2,9 +2,10 @@
 ordinary one (ipk_relpos_attn_run), through the C ABI, byte for byte.
 
 Two calls in a row on one handle, the second smaller (fewer utterances, fewer frames,
-ragged lengths), so the second runs on the array the first left behind; a call with a
-kept position projection (pos_table NULL); the intermediates of a no-allocation run;
-and a shape beyond the array, refused before anything is enqueued.
+ragged lengths), so the second runs on the array the first left behind; every
+workload's shape (all fit the array); a call with a kept position projection
+(pos_table NULL); the intermediates of a no-allocation run; and a shape beyond the
+array, refused before anything is enqueued.
 """
 
 import numpy as np
@@ -50,6 +51,15 @@ def test_noalloc_matches_run_two_calls_second_smaller(gpu_lib):
     lengths2 = [T2, max(1, T2 // 3)]
     pe2 = _dev(blk.pos_table[T - T2:T + T2 - 1])
     _case(gpu_lib, mod, blk, blk.x[:2, :T2], lengths2, pe2, "second call, smaller")
+    mod.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "parakeet", "batched", "longform", "stack"])
+def test_noalloc_matches_run_on_every_workload(gpu_lib, name):
+    blk = make_workload(name, "literal", layers=1).blocks[0]
+    B, T, d = blk.x.shape
+    mod = gpu_lib.RelPosAttn.from_block(blk, max_batch=B, max_T=T)
+    _case(gpu_lib, mod, blk, blk.x, blk.lengths, _dev(blk.pos_table), name)
     mod.close()
 
 
