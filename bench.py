@@ -230,6 +230,29 @@ def main():
             s_ops += 2 * (p_ + q_ + r_)
         for m_ in smods:
             m_.close()
+        # the other single-block workloads, timed like the variants: frames per second of
+        # whole calls (parity of each is covered by the GPU tests)
+        other = {}
+        for wname in ("tiny", "parakeet", "batched"):
+            owl = make_workload(wname, args.regime)
+            ob = owl.blocks[0]
+            om = ipk.RelPosAttn.from_block(ob, device=dev)
+            ox = torch.from_numpy(ob.x).to(dev)
+            ope = torch.from_numpy(ob.pos_table).to(dev)
+            oy = torch.empty_like(ox)
+            oms = timed(lambda: om(ox, ope, lengths=ob.lengths, y=oy, stream=stream), n_stage)
+            osh = ob.shape
+            p_, q_, r_ = algorithmic_macs(ob.x.shape[0], ob.T, osh.d_model, osh.n_heads, osh.d_k, ob.lengths)
+            otops = 2 * (p_ + q_ + r_) / (oms * 1e-3) / 1e12
+            other[wname] = {
+                "workload": f"{wname}: B={ob.x.shape[0]} T={ob.T} d_model={osh.d_model} H={osh.n_heads} "
+                            f"d_k={osh.d_k}, {args.regime} scales, seed {owl.seed}",
+                "ms_per_call": round(oms, 5),
+                "frames_per_s": round(float(np.sum(ob.lengths)) / (oms * 1e-3), 1),
+                "tops": round(otops, 3),
+                "pct_int8_peak": round(100.0 * otops / INT8_PEAK_TOPS, 3),
+            }
+            om.close()
 
     proj, pos, attn = algorithmic_macs(B, T, d, H, dk, lengths)
     ops = 2 * (proj + pos + attn)
@@ -293,6 +316,7 @@ def main():
                 "tops": round(s_ops / (ms_stack * 1e-3) / 1e12, 3),
                 "passes_timed": n_stack,
             },
+            "other_workloads": other,
             "timing": f"{n_stage} steps each between two HIP events, after 5 warm-up steps",
         },
         "roofline": {
@@ -323,6 +347,34 @@ def main():
             "sample": f"one whole call of the same workload ({args.workload}, B={B}, T={T}); "
                       f"{cpu_s:.2f} s; output bit-exact vs GPU: {exact}",
         }
+        # the oracle on one thread, one call of the Parakeet-scale block
+        c1 = make_workload("parakeet", args.regime).blocks[0]
+        nthreads = core.num_threads()
+        core.set_num_threads(1)
+        t1 = time.perf_counter()
+        core.relpos_attn(c1)
+        c1_s = time.perf_counter() - t1
+        core.set_num_threads(nthreads)
+        c1p, c1q, c1r = algorithmic_macs(1, c1.T, c1.shape.d_model, c1.shape.n_heads, c1.shape.d_k, c1.lengths)
+        rec["cpu_baseline"]["single_thread"] = {
+            "workload": f"parakeet: B=1 T={c1.T} d_model={c1.shape.d_model} H={c1.shape.n_heads}",
+            "seconds_per_call": round(c1_s, 4),
+            "frames_per_s": round(float(np.sum(c1.lengths)) / c1_s, 1),
+            "tops": round(2 * (c1p + c1q + c1r) / c1_s / 1e12, 6),
+            "cores": 1,
+        }
+        # spec self-check 3 as the oracle measures it (committed analysis): the
+        # integer block against the float64 block of Eq. 8-9, relative L2 per workload
+        gap_path = os.path.join(ROOT, "oracle", "fp_gap_results.json")
+        if os.path.exists(gap_path):
+            with open(gap_path) as fh:
+                gap = json.load(fh)
+            rec["oracle_vs_fp_block"] = {
+                "rel_l2": {k: round(v["rel_l2"], 4) for k, v in gap["configs"].items()},
+                "regime": gap["regime"],
+                "target": 0.02,
+                "source": "oracle/fp_gap.py (written by python -m oracle.fp_gap)",
+            }
     print(json.dumps(rec), flush=True)
 
 

@@ -76,6 +76,8 @@ def lib():
             L = C.CDLL(path)
             L.ipk_oracle_num_threads.restype = C.c_int
             L.ipk_oracle_num_threads.argtypes = []
+            L.ipk_oracle_set_num_threads.restype = None
+            L.ipk_oracle_set_num_threads.argtypes = [C.c_int]
             L.ipk_oracle_rs.restype = C.c_int64
             L.ipk_oracle_rs.argtypes = [C.c_int64, C.c_int64, C.c_int32]
             L.ipk_oracle_clamp8.restype = C.c_int64
@@ -122,6 +124,11 @@ def _p(a: np.ndarray, t):
 
 def num_threads() -> int:
     return int(lib().ipk_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (for timing)."""
+    lib().ipk_oracle_set_num_threads(int(n))
 
 
 def rs(a: int, m: int, n: int) -> int:

@@ -50,8 +50,9 @@ typedef struct {
   int8_t *ctx;       /* [B][T][d] */
 } oracle_trace;
 
-/* Threads the parallel loops will use. */
+/* Threads the parallel loops will use, and a way to change it (timing only). */
 int ipk_oracle_num_threads(void) { return omp_get_max_threads(); }
+void ipk_oracle_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
 
 /* floor(v / 2^n) for n >= 0, written without relying on signed shifts. */
 static int64_t floor_div_pow2(int64_t v, int32_t n) {

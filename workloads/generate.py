@@ -190,13 +190,15 @@ def _scales_literal(rng, shape: ConfigShape, S_x: Optional[float]):
     return sc
 
 
-def _scales_calibrated(rng, shape: ConfigShape, S_x: Optional[float], logit_gain: float):
+def _scales_calibrated(rng, shape: ConfigShape, S_x: Optional[float], logit_gain: float,
+                       w_scale: Optional[float] = None):
     d, dk = shape.d_model, shape.d_k
     kcov = 4.0  # grids cover +-4 standard deviations
     sc = {}
     sc["S_x"] = (1.0 / _sigma_x(shape)) if S_x is None else float(S_x)
     sx_real = sc["S_x"] * _sigma_x(shape)
-    w_base = 1.0 / (SIGMA_W * math.sqrt(d))  # Xavier-scaled weights
+    # Xavier-scaled weights, or a given per-channel weight scale (the scale sweep)
+    w_base = 1.0 / (SIGMA_W * math.sqrt(d)) if w_scale is None else float(w_scale)
     for w in ("q", "k", "v", "pos", "out"):
         sc["S_W" + w] = w_base * rng.uniform(0.75, 1.0, size=d)
     sc["S_Wq"] = sc["S_Wq"] * logit_gain
@@ -240,7 +242,7 @@ def _consts_from_scales(sc, shape: ConfigShape):
 
 def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str = "literal",
                with_x: bool = True, S_x: Optional[float] = None, lengths=None,
-               logit_gain: float = 1.0) -> Block:
+               logit_gain: float = 1.0, w_scale: Optional[float] = None) -> Block:
     d, H, dk = shape.d_model, shape.n_heads, shape.d_k
     x = _draw_x(rng, shape, T) if with_x else None
     ws = [_uniform_i8(rng, (d, d)) for _ in range(5)]
@@ -249,7 +251,7 @@ def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str
     if regime == "literal":
         sc = _scales_literal(rng, shape, S_x)
     elif regime == "calibrated":
-        sc = _scales_calibrated(rng, shape, S_x, logit_gain)
+        sc = _scales_calibrated(rng, shape, S_x, logit_gain, w_scale)
     else:
         raise ValueError(regime)
     sc["S_pe"], sc["S_A"] = S_PE, S_A
@@ -266,7 +268,7 @@ def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str
 
 def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = None,
                   layers: Optional[int] = None, T: Optional[int] = None, B: Optional[int] = None,
-                  logit_gain: float = 1.0) -> Workload:
+                  logit_gain: float = 1.0, w_scale: Optional[float] = None) -> Workload:
     """All blocks of one named workload; the stack seeds layer l with seed + l.
 
     ``T``, ``B`` and ``layers`` override the configured sizes (smaller cases of
@@ -287,7 +289,7 @@ def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = No
     for layer in range(nl):
         rng = np.random.default_rng(seed + layer)
         blk = make_block(shape, T, rng, regime, with_x=(layer == 0), S_x=S_x, lengths=lengths,
-                         logit_gain=logit_gain)
+                         logit_gain=logit_gain, w_scale=w_scale)
         blocks.append(blk)
         S_x = blk.scales["S_y"]
         lengths = blk.lengths
