@@ -696,6 +696,11 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   // tile) units of a channel group alternate between its two waves: each wave leaves
   // the partial sums of the units it does not own in the table region, as
   // [cg][value][lane] int32, and adds its partner's to the units it owns (exact).
+  // The lane's column is read afresh from the lane counter: kept from the start, it
+  // was the one value the register allocator spilled to scratch memory.
+  int lane_now;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_now));
+  const int col_now = lane_now & 15;
   constexpr int R = NTILES * AV_NT * 4;
   constexpr int NU = NTILES * AV_NT;
   ldsi32* red = (ldsi32*)(uintptr_t)TAB;
@@ -717,7 +722,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   for (int u = 0; u < NU; ++u) {
     if (u % KH != kh) continue;
     const int tt = u / AV_NT, j = u % AV_NT;
-    const int qi = wg_q0 + 16 * tt + col;
+    const int qi = wg_q0 + 16 * tt + col_now;
     if (qi >= T) continue;
     uint32_t packed = 0;
     if (qi < L) {
