@@ -111,8 +111,9 @@ int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relpos_attn_t**
  * pos_table DEVICE int8 [2T-1][d_model]  sinusoidal relative-position table; row r
  *                                        holds relative position T-1-r; NULL uses the
  *                                        projection kept by ipk_relpos_attn_cache_positions
- * lengths  HOST int32 [B] valid frames L_b in [1, T], or NULL for all T; the values
- *          are captured when the call returns (the array may be reused at once)
+ * lengths  HOST int32 [B] valid frames L_b in [1, T], or NULL for all T; exactly B
+ *          entries are read (the array must hold them), and the values are captured
+ *          when the call returns (the array may be reused at once)
  * y        DEVICE int8 [B][T][d_model]   block output; rows t >= L_b are zero
  * x, pos_table and y must be 16-byte aligned.
  * The call is asynchronous: it enqueues kernels and returns.  Pointers are borrowed
@@ -391,7 +392,8 @@ int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out);
 
 /* Runs the module on `stream`: z DEVICE int8 [B][T][d_model] -> z_out (same layout),
  * both 16-byte aligned; z_out may be z itself but may not overlap it otherwise.
- * lengths: HOST int32 [B] valid frames in [1, T] (NULL: all T), captured at the call.
+ * lengths: HOST int32 [B] valid frames in [1, T] (NULL: all T; exactly B entries are
+ * read), captured at the call.
  * Asynchronous; calls on one handle must be ordered on one stream.
  * Errors: IPK_ERR_INVALID_ARG (null handle or pointer, misalignment, partial overlap,
  * B or T outside the handle's limits, a length outside [1, T]), IPK_ERR_HIP. */
@@ -401,8 +403,10 @@ int ipk_conv_run(ipk_conv_t* h, const int8_t* z, const int32_t* lengths, int32_t
 /* Copies an intermediate of the last run into `dst` (DEVICE, `bytes` bytes) on
  * `stream`: IPK_CONV_X the LayerNorm output int8 [B][T][d], IPK_CONV_U PW1's output int8
  * [B][T][2 d], IPK_CONV_V the BatchNorm output int16 [B][T][d], IPK_CONV_O the Swish
- * output int8 [B][T][d].  Errors: IPK_ERR_INVALID_ARG (no run yet, unknown `which`,
- * bytes too small, null), IPK_ERR_HIP. */
+ * output int8 [B][T][d].  A run does not store the BatchNorm output (it is consumed in
+ * registers); IPK_CONV_V enqueues the middle kernel again on the kept PW1 output, with
+ * the int16 store, before the copy.  Errors: IPK_ERR_INVALID_ARG (no run yet, unknown
+ * `which`, bytes too small, null), IPK_ERR_HIP. */
 enum { IPK_CONV_X = 0, IPK_CONV_U = 1, IPK_CONV_V = 2, IPK_CONV_O = 3 };
 int ipk_conv_intermediate(ipk_conv_t* h, int32_t which, void* dst, int64_t bytes, void* stream);
 

@@ -12,17 +12,20 @@
 //
 // One thread per channel, a workgroup per (utterance, 256 channels, 8 frames): the
 // thread computes the GLU of its channel over the 16 frames the window needs, in
-// registers, then slides the 9 taps over them.  The kernel is bound by the latency of
-// its byte-wide loads and stores, not by its arithmetic, so short tiles pay: 8 frames
-// (twice the GLU work of the window's halo) ran the module 8 % faster than 16, and
-// 4 or 32 frames slower.  The GLU's sigmoid of every int8 input
-// sits in LDS (256 values, computed by the workgroup), and the Swish of every int16
-// value and its requantization in a 64 KB table computed once per handle
-// (`swish16_table`), so an output costs its nine multiply-adds, one requantization
-// and one table load.  Loads and stores of a frame are 256 consecutive elements across
-// the workgroup.  Per frame and channel the kernel reads 2 bytes of PW1's output (each
-// twice, with the halo) and writes 3 (the int8 Swish output and the int16 BatchNorm
-// output).
+// registers, then slides the 9 taps over them.  The GLU of every int8 pair (a, b) and
+// the Swish of every int16 value with its requantization sit in tables computed once
+// per handle with the formulas above (`glu_table`, 64 KB; `swish16_table`, 64 KB), so
+// a GLU costs one byte load and an output its nine multiply-adds, one requantization
+// and one byte load: evaluated in place, the GLU's two 64-bit products were most of
+// the kernel's instructions.  8 frames per workgroup (twice the GLU work of the
+// window's halo) ran the module 8 % faster than 16, and 4 or 32 frames slower; four
+// channels per lane (dword loads and stores) ran it 13 % slower (a quarter of the
+// waves, each holding four times the registers).  Loads and stores of a frame are 256
+// consecutive elements across the workgroup.  Per frame and channel the kernel reads 2
+// bytes of PW1's output (each twice, with the halo) and writes the int8 Swish output;
+// the int16 BatchNorm output is written only when the launch asks for it (v != NULL:
+// an inspection of the intermediate, which reruns the kernel on the kept PW1 output),
+// not on a module run.
 #include "ipk_internal.h"
 
 namespace ipk {
@@ -35,11 +38,12 @@ constexpr int CONV_WIN = CONV_FRAMES + 2 * CONV_HALF;
 struct ConvArgs {
   const int8_t* u;  // [B][T][2 d] PW1 output: a = channels [0, d), b = [d, 2 d)
   int8_t* o;        // [B][T][d]
-  int16_t* v;       // [B][T][d]
+  int16_t* v;       // [B][T][d], or NULL: not stored
   const int8_t* w;  // [d][9]
   const int32_t* bias;
   const int32_t* mult;
   const int8_t* swtab16;  // [65535]: Swish output of each int16 v, at v + 32767
+  const int8_t* glutab;   // [256][256]: GLU output of (a, b), at (a + 128) 256 + b + 128
   Lengths lens;           // valid frames per utterance
   int T, d, shift_dw;
   long long glu_qc, glu_q1, m_glu;
@@ -68,17 +72,20 @@ __global__ __launch_bounds__(256) void swish16_table(int8_t* tab, long long q_c,
   tab[i] = (int8_t)(o < -127 ? -127 : (o > 127 ? 127 : o));
 }
 
+// The GLU of every int8 pair: g = clamp8(RS(a sigma(b), m_glu, n_glu)), one thread per
+// (a, b), at (a + 128) 256 + b + 128 (computed once per handle; the middle kernel looks
+// it up).
+__global__ __launch_bounds__(256) void glu_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift) {
+  const long long av = (long long)blockIdx.x - 128, bv = (long long)threadIdx.x - 128;
+  const long long ab = bv < 0 ? -bv : bv;
+  const long long sg = bv > 0 ? 1 : (bv < 0 ? -1 : 0);
+  const long long sig = -(q_1 + sg * poly_l(ab, q_c, q_1));
+  const long long r = rs64(av * sig, m, shift);
+  tab[blockIdx.x * 256 + threadIdx.x] = (int8_t)(r < -127 ? -127 : (r > 127 ? 127 : r));
+}
+
 __global__ __launch_bounds__(CONV_CH) void conv_glu_dw_swish(ConvArgs a) {
-  // the GLU sigmoid of every int8 b, at b + 128
-  __shared__ long long sig[256];
   const int tid = threadIdx.x;
-  {
-    const long long bv = (long long)tid - 128;
-    const long long ab = bv < 0 ? -bv : bv;
-    const long long sg = bv > 0 ? 1 : (bv < 0 ? -1 : 0);
-    sig[tid] = -(a.glu_q1 + sg * poly_l(ab, a.glu_qc, a.glu_q1));
-  }
-  __syncthreads();
   const int c = blockIdx.y * CONV_CH + tid;
   const int b = blockIdx.z;
   const int t0 = blockIdx.x * CONV_FRAMES;
@@ -93,9 +100,8 @@ __global__ __launch_bounds__(CONV_CH) void conv_glu_dw_swish(ConvArgs a) {
     const int t = t0 - CONV_HALF + f;
     int gv = 0;
     if (t >= 0 && t < L) {
-      const long long av = ub[(size_t)t * 2 * d], bi = ub[(size_t)t * 2 * d + d];
-      long long r = rs64(av * sig[bi + 128], a.m_glu, a.shift_glu);
-      gv = (int)(r < -127 ? -127 : (r > 127 ? 127 : r));
+      const int av = ub[(size_t)t * 2 * d], bi = ub[(size_t)t * 2 * d + d];
+      gv = a.glutab[(av + 128) * 256 + bi + 128];
     }
     g[f] = gv;
   }
@@ -114,13 +120,18 @@ __global__ __launch_bounds__(CONV_CH) void conv_glu_dw_swish(ConvArgs a) {
     long long vv = rs64(acc, mdw, a.shift_dw);
     vv = vv < -32767 ? -32767 : (vv > 32767 ? 32767 : vv);
     const size_t idx = ((size_t)b * T + t) * d + c;
-    a.v[idx] = (int16_t)vv;
+    if (a.v) a.v[idx] = (int16_t)vv;
     a.o[idx] = t < L ? a.swtab16[vv + 32767] : (int8_t)0;
   }
 }
 
 hipError_t launch_swish16_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st) {
   hipLaunchKernelGGL(swish16_table, dim3((65535 + 255) / 256), dim3(256), 0, st, tab, q_c, q_1, m, shift);
+  return hipGetLastError();
+}
+
+hipError_t launch_glu_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st) {
+  hipLaunchKernelGGL(glu_table, dim3(256), dim3(256), 0, st, tab, q_c, q_1, m, shift);
   return hipGetLastError();
 }
 
@@ -142,6 +153,7 @@ hipError_t launch_conv_middle(const ConvMiddle& m, const int8_t* u, const Length
   a.m_glu = m.m_glu;
   a.shift_glu = m.shift_glu;
   a.swtab16 = m.swtab16;
+  a.glutab = m.glutab;
   const dim3 grid((unsigned)((T + CONV_FRAMES - 1) / CONV_FRAMES), (unsigned)((d + CONV_CH - 1) / CONV_CH),
                   (unsigned)B);
   hipLaunchKernelGGL(conv_glu_dw_swish, grid, dim3(CONV_CH), 0, st, a);

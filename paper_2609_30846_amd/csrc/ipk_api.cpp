@@ -763,9 +763,10 @@ struct ipk_conv {
   Requant rq_pw1, rq_pw2;       // Eq. 7 constants of PW1 and PW2
   ConvMiddle mid;               // depthwise weights and constants (device copies)
   int8_t *x, *u, *o;            // LayerNorm output, PW1 output [.][2 d], Swish output
-  int16_t* v;                   // int16 BatchNorm output
+  int16_t* v;                   // int16 BatchNorm output (written on request only)
   Residual res;
   int last_B, last_T;
+  Lengths last_lens;            // the last run's lengths (to recompute v on request)
   std::vector<void*> allocs;
 };
 
@@ -876,6 +877,8 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   chk(dev_alloc(h, &stage, 2 * d * d));
   int8_t* sw16 = nullptr;
   chk(dev_alloc(h, &sw16, 65535));
+  int8_t* glu = nullptr;
+  chk(dev_alloc(h, &glu, 65536));
   if (e != hipSuccess) {
     free_conv(h);
     (void)hipGetLastError();
@@ -896,6 +899,7 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   chk(hipMemcpy(g, desc->ln_mult, d * sizeof(int32_t), hipMemcpyHostToDevice));
   chk(hipMemcpy(c, cb.data(), d * sizeof(int64_t), hipMemcpyHostToDevice));
   chk(launch_swish16_table(sw16, desc->sw_qc, desc->sw_q1, desc->m_sw, desc->shift_sw, nullptr));
+  chk(launch_glu_table(glu, desc->glu_qc, desc->glu_q1, desc->m_glu, desc->shift_glu, nullptr));
   chk(hipDeviceSynchronize());
   if (e != hipSuccess) {
     free_conv(h);
@@ -913,6 +917,7 @@ extern "C" int ipk_conv_create(const ipk_conv_desc* desc, ipk_conv_t** out) {
   h->mid.m_glu = desc->m_glu;
   h->mid.shift_glu = desc->shift_glu;
   h->mid.swtab16 = sw16;
+  h->mid.glutab = glu;
   h->res.ln_mult = g;
   h->res.ln_bias = c;
   h->res.ln_shift = desc->ln_shift;
@@ -949,13 +954,15 @@ extern "C" int ipk_conv_run(ipk_conv_t* h, const int8_t* z, const int32_t* lengt
   const int rows = B * T;
   hipError_t e = launch_layernorm_rows(rows, h->d, h->res, z, h->x, st);
   if (e == hipSuccess) e = launch_linear(h->x, rows, h->d, 2 * h->d, h->w_pw1, h->rq_pw1, h->u, st);
-  if (e == hipSuccess) e = launch_conv_middle(h->mid, h->u, lens, B, T, h->d, h->o, h->v, st);
+  // the int16 BatchNorm output is not stored on a run (ipk_conv_intermediate recomputes it)
+  if (e == hipSuccess) e = launch_conv_middle(h->mid, h->u, lens, B, T, h->d, h->o, nullptr, st);
   if (e == hipSuccess)
     e = launch_linear_resid(h->o, rows, h->d, h->d, h->w_pw2, h->rq_pw2, z, h->res.m_z, h->res.m_y,
                             h->res.shift_r, z_out, st);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last_B = B;
   h->last_T = T;
+  h->last_lens = lens;
   return IPK_OK;
 }
 
@@ -973,7 +980,10 @@ extern "C" int ipk_conv_intermediate(ipk_conv_t* h, int32_t which, void* dst, in
     default: return fail(IPK_ERR_INVALID_ARG, "unknown intermediate %d", which);
   }
   if (bytes < need) return fail(IPK_ERR_INVALID_ARG, "dst holds %lld bytes, %lld needed", (long long)bytes, (long long)need);
-  hipError_t e = hipMemcpyAsync(dst, src, (size_t)need, hipMemcpyDeviceToDevice, (hipStream_t)stream);
+  hipError_t e = hipSuccess;
+  if (which == IPK_CONV_V)  // rerun the middle kernel on the kept PW1 output, storing v (o is rewritten unchanged)
+    e = launch_conv_middle(h->mid, h->u, h->last_lens, h->last_B, h->last_T, h->d, h->o, h->v, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(dst, src, (size_t)need, hipMemcpyDeviceToDevice, (hipStream_t)stream);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "copy failed: %s", hipGetErrorString(e));
   return IPK_OK;
 }

@@ -196,8 +196,10 @@ struct ConvMiddle {
   long long glu_qc, glu_q1, m_glu;
   int shift_glu;
   const int8_t* swtab16;  // [65535] Swish output of each int16 value v, at v + 32767
+  const int8_t* glutab;   // [256][256] GLU output of each int8 pair (a, b), at (a + 128) 256 + b + 128
 };
 hipError_t launch_swish16_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st);
+hipError_t launch_glu_table(int8_t* tab, long long q_c, long long q_1, long long m, int shift, hipStream_t st);
 hipError_t launch_conv_middle(const ConvMiddle& m, const int8_t* u, const Lengths& lens, int B, int T, int d,
                               int8_t* o, int16_t* v, hipStream_t st);
 hipError_t launch_layernorm_rows(long rows, int d, const Residual& r, const int8_t* z, int8_t* out, hipStream_t st);

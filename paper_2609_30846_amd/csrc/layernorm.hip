@@ -12,8 +12,11 @@
 // fixed-point step per channel (the rounding term comes pre-added to c).
 //
 // The work is a few bytes per element, so the kernel is bound by moving the rows
-// (HBM or L2): one wave per row, each lane holding 16-byte pieces of it in registers,
-// so the row is read once.  Both sums come from one pass: sum z and sum z^2 by
+// (HBM or L2) and by the latency of doing so: one wave per row, each lane holding
+// 16-byte pieces of it in registers, so the row is read once; the per-channel
+// constants of the lane's pieces (4 + 8 bytes a channel, the same for every row) are
+// requested together with the row, so their latency hides behind the row's and the
+// sums'.  Both sums come from one pass: sum z and sum z^2 by
 // v_dot4 against ones and against z itself, and
 //   sum (z - mu)^2 = sum z^2 - 2 mu sum z + d mu^2
 // exactly in integers, and the wave sums are DPP adds.  The mean (a binary search over
@@ -24,6 +27,7 @@
 namespace ipk {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef long long v2l __attribute__((ext_vector_type(2)));
 
 struct LnArgs {
   const int8_t* z;
@@ -87,20 +91,42 @@ __device__ __forceinline__ uint32_t div_2p31(uint32_t s) {
   return q;
 }
 
-// NP: 16-byte pieces per lane (d <= 1024 NP)
+// NP: 16-byte pieces per lane (d <= 1024 NP).  With NP <= 2 the lane's constants
+// are loaded up front (at most 104 registers); wider rows load them per piece.
 template <int NP>
 __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
+  constexpr bool PRE = NP <= 2;
   const int lane = threadIdx.x & 63;
   const long row = (long)blockIdx.x * LN_WAVES + (threadIdx.x >> 6);
   if (row >= a.rows) return;
   const int d = a.d, npieces = d >> 4;
   const int8_t* src = a.z + row * d;
   v4i zv[NP];
-  int s = 0, q = 0;
 #pragma unroll
   for (int k = 0; k < NP; ++k) {
     const int p = lane + 64 * k;
     zv[k] = p < npieces ? *(const v4i*)(src + 16 * p) : (v4i){0, 0, 0, 0};
+  }
+  // the constants of the lane's 16 channels per piece: multipliers (4 x 16 bytes) and
+  // biases (8 x 16 bytes)
+  v4i gv[PRE ? NP : 1][4];
+  v2l cv[PRE ? NP : 1][8];
+  auto load_consts = [&](int c0, v4i (&g)[4], v2l (&c)[8]) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) g[w] = *(const v4i*)(a.g + c0 + 4 * w);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[j] = *(const v2l*)(a.c + c0 + 2 * j);
+  };
+  if constexpr (PRE) {
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      const int p = lane + 64 * k;
+      if (p < npieces) load_consts(16 * p, gv[k], cv[k]);
+    }
+  }
+  int s = 0, q = 0;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       s = __builtin_amdgcn_sdot4(zv[k][w], 0x01010101, s, false);
@@ -126,17 +152,27 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_i8(LnArgs a) {
     const int p = lane + 64 * k;
     if (p >= npieces) continue;
     const int c0 = 16 * p;
+    v4i g[4];
+    v2l c[8];
+    if constexpr (PRE) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) g[w] = gv[k][w];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) c[j] = cv[k][j];
+    } else {
+      load_consts(c0, g, c);
+    }
     v4i out;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const v4i gv = *(const v4i*)(a.g + c0 + 4 * w);
       uint32_t o = 0;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int zb = (zv[k][w] << (24 - 8 * b)) >> 24;
         const int y = zb - m;
         const int u = y * Fh + ((y >> 1) & Fo);
-        const long long t = ((long long)u * gv[b] + a.c[c0 + 4 * w + b]) >> shift;
+        const int e = 4 * w + b;
+        const long long t = ((long long)u * g[w][b] + c[e >> 1][e & 1]) >> shift;
         o |= ((uint32_t)(int)min(max(t, -127ll), 127ll) & 0xFFu) << (8 * b);
       }
       out[w] = (int)o;

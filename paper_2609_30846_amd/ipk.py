@@ -175,6 +175,41 @@ def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
 
 
+def _tensor(t, name: str, shape, device, dtype=None):
+    """Raises ValueError unless ``t`` is a contiguous int8 (or ``dtype``) tensor of
+    ``shape`` on ``device``: the library takes raw pointers and trusts their extents."""
+    import torch
+
+    dtype = torch.int8 if dtype is None else dtype
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    dev = torch.device(device)
+    if dev.type == "cuda" and dev.index is None:
+        dev = torch.device("cuda", torch.cuda.current_device())
+    if t.device != dev:
+        raise ValueError(f"{name} is on {t.device}, the handle's device is {dev}")
+    return t
+
+
+def _lengths(lengths, B: int, T: int):
+    """Raises ValueError unless ``lengths`` is None or holds B values in [1, T] (the
+    library reads exactly B entries from the host array)."""
+    if lengths is None:
+        return None
+    lens = np.asarray(lengths).reshape(-1)
+    if lens.shape[0] != B:
+        raise ValueError(f"lengths holds {lens.shape[0]} values for B={B}")
+    if lens.size and (lens.min() < 1 or lens.max() > T):
+        raise ValueError(f"lengths must lie in [1, T={T}]")
+    return lens
+
+
 def _stream_ptr(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -304,10 +339,21 @@ class RelPosAttn:
         return cls(blk.shape.d_model, blk.shape.n_heads, weights, blk.consts,
                    max_batch or blk.shape.B, max_T or blk.T, device)
 
+    def _check_run(self, x, pos_table, lengths, y):
+        if x.dim() != 3:
+            raise ValueError(f"x must be [B][T][d_model], got shape {tuple(x.shape)}")
+        B, T, _ = x.shape
+        _tensor(x, "x", (B, T, self.d_model), self.device)
+        if pos_table is not None:
+            _tensor(pos_table, "pos_table", (2 * T - 1, self.d_model), self.device)
+        if y is not None:
+            _tensor(y, "y", (B, T, self.d_model), self.device)
+        return B, T, _lengths(lengths, B, T)
+
     def __call__(self, x, pos_table, lengths=None, y=None, stream=None):
         import torch
 
-        B, T, d = x.shape
+        B, T, lengths = self._check_run(x, pos_table, lengths, y)
         if y is None:
             y = torch.empty_like(x)
         ipk_relpos_attn_run(self.handle, x, pos_table, lengths, B, T, y, stream)
@@ -316,14 +362,19 @@ class RelPosAttn:
     def run_noalloc(self, x, pos_table, lengths=None, y=None, stream=None):
         """As a call, with the run's workspace in the GPU's static no-allocation array
         (ipk_relpos_attn_run_noalloc); ``y`` is the caller's output buffer."""
-        B, T, d = x.shape
+        if y is None:
+            raise ValueError("run_noalloc writes into the caller's y")
+        B, T, lengths = self._check_run(x, pos_table, lengths, y)
         ipk_relpos_attn_run_noalloc(self.handle, x, pos_table, lengths, B, T, y, stream)
         return y
 
     def cache_positions(self, pos_table, stream=None):
         """Projects ``pos_table`` ([2 T_table - 1][d] int8 on the device) once; later
         calls with ``pos_table=None`` use it for any T <= T_table."""
+        if pos_table.dim() != 2 or pos_table.shape[0] % 2 == 0:
+            raise ValueError(f"pos_table must be [2 T - 1][d_model], got shape {tuple(pos_table.shape)}")
         T_table = (pos_table.shape[0] + 1) // 2
+        _tensor(pos_table, "pos_table", (2 * T_table - 1, self.d_model), self.device)
         ipk_relpos_attn_cache_positions(self.handle, pos_table, T_table, stream)
 
     def set_residual(self, ln_mult, ln_bias, ln_shift: int, m_z: int, m_y: int, shift_r: int):
@@ -341,7 +392,7 @@ class RelPosAttn:
         """z2 = z1 + MHSA(LN(z1)); ``z2`` may be ``z1`` (in place)."""
         import torch
 
-        B, T, d = z1.shape
+        B, T, lengths = self._check_run(z1, pos_table, lengths, z2)
         if z2 is None:
             z2 = torch.empty_like(z1)
         ipk_mhsa_residual_run(self.handle, z1, pos_table, lengths, B, T, z2, stream)
@@ -415,7 +466,12 @@ class FeedForward:
     def __call__(self, z, z_out=None, stream=None):
         import torch
 
+        if z.numel() % self.d_model or z.shape[-1] != self.d_model:
+            raise ValueError(f"z must end in d_model={self.d_model}, got shape {tuple(z.shape)}")
         rows = z.numel() // self.d_model
+        _tensor(z, "z", tuple(z.shape), self.device)
+        if z_out is not None:
+            _tensor(z_out, "z_out", tuple(z.shape), self.device)
         if z_out is None:
             z_out = torch.empty_like(z)
         ipk_ffn_run(self.handle, z, rows, z_out, stream)
@@ -496,7 +552,13 @@ class ConvModule:
     def __call__(self, z, lengths=None, z_out=None, stream=None):
         import torch
 
-        B, T, d = z.shape
+        if z.dim() != 3:
+            raise ValueError(f"z must be [B][T][d_model], got shape {tuple(z.shape)}")
+        B, T, _ = z.shape
+        _tensor(z, "z", (B, T, self.d_model), self.device)
+        if z_out is not None:
+            _tensor(z_out, "z_out", (B, T, self.d_model), self.device)
+        lengths = _lengths(lengths, B, T)
         if z_out is None:
             z_out = torch.empty_like(z)
         ipk_conv_run(self.handle, z, lengths, B, T, z_out, stream)
@@ -555,6 +617,11 @@ class LayerNorm:
     def __call__(self, z, x=None, stream=None):
         import torch
 
+        if z.numel() % self.d_model or z.shape[-1] != self.d_model:
+            raise ValueError(f"z must end in d_model={self.d_model}, got shape {tuple(z.shape)}")
+        _tensor(z, "z", tuple(z.shape), self.device)
+        if x is not None:
+            _tensor(x, "x", tuple(z.shape), self.device)
         if x is None:
             x = torch.empty_like(z)
         ipk_layernorm_run(self.handle, z, z.numel() // self.d_model, x, stream)

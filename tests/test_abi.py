@@ -349,3 +349,30 @@ def test_create_rejects_max_T_beyond_the_score_rows():
         d.d_k, d.n_heads, d.max_T = dk, H, 8001
         assert _create_status(d) == ipk.IPK_ERR_UNSUPPORTED
         assert "on-chip score rows" in ipk.last_error()
+
+
+def test_binding_rejects_bad_tensors_before_the_library():
+    """The wrappers check dtype, shape, contiguity, device and len(lengths) == B and raise
+    ValueError before any pointer reaches the library (no GPU needed: CPU tensors)."""
+    import torch
+
+    from paper_2609_30846_amd.ipk import _lengths, _tensor
+
+    t = torch.zeros((2, 8, 64), dtype=torch.int8)
+    assert _tensor(t, "x", (2, 8, 64), "cpu") is t
+    with pytest.raises(ValueError, match="int8"):
+        _tensor(t.to(torch.int16), "x", (2, 8, 64), "cpu")
+    with pytest.raises(ValueError, match="shape"):
+        _tensor(t, "x", (2, 8, 128), "cpu")
+    with pytest.raises(ValueError, match="contiguous"):
+        _tensor(t.transpose(1, 2).contiguous().transpose(1, 2), "x", (2, 8, 64), "cpu")
+    with pytest.raises(ValueError, match="device"):
+        _tensor(t, "x", (2, 8, 64), "meta")
+    assert _lengths(None, 2, 8) is None
+    assert list(_lengths([8, 3], 2, 8)) == [8, 3]
+    with pytest.raises(ValueError, match="B=2"):
+        _lengths([8], 2, 8)
+    with pytest.raises(ValueError, match="T=8"):
+        _lengths([9, 1], 2, 8)
+    with pytest.raises(ValueError, match="T=8"):
+        _lengths([0, 1], 2, 8)
