@@ -19,7 +19,7 @@ ARCH = "gfx950"
 FLAGS = [
     "--offload-arch=" + ARCH,
     "-O3",
-    "-std=c++17",
+    "-std=c++20",  # two's complement shifts and conversions are defined behaviour
     "-fPIC",
     "-Wall",
     # keep the compiler from forming packed fp32 instructions
