@@ -92,3 +92,32 @@ def test_noalloc_refuses_shapes_beyond_the_array(gpu_lib):
     torch.cuda.synchronize()
     assert int(y.min()) == 5 and int(y.max()) == 5  # nothing was enqueued
     mod.close()
+
+
+def test_noalloc_run_in_a_captured_graph(gpu_lib):
+    """The callers the entry point is for: a no-allocation run captured in a HIP graph
+    and replayed, with other no-allocation runs (a different input) writing the shared
+    array between the replays; every replay equals the eager result."""
+    import torch
+
+    blk = make_workload("parakeet", "calibrated").blocks[0]
+    mod = gpu_lib.RelPosAttn.from_block(blk)
+    x = _dev(blk.x)
+    pe = _dev(blk.pos_table)
+    y_eager = torch.empty_like(x)
+    mod(x, pe, lengths=blk.lengths, y=y_eager)
+    torch.cuda.synchronize()
+    y = torch.empty_like(x)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        mod.run_noalloc(x, pe, lengths=blk.lengths, y=y)
+    other = _dev(blk.x[:, ::-1])
+    y_other = torch.empty_like(x)
+    for k in range(4):
+        y.fill_(k + 1)
+        mod.run_noalloc(other, pe, lengths=blk.lengths, y=y_other)  # overwrites the array
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), k
+    del graph
+    mod.close()
