@@ -348,23 +348,23 @@ def main():
                       f"{cpu_s:.2f} s; output bit-exact vs GPU: {exact}",
         }
         # the oracle on one thread, one call of the Parakeet-scale block
-        c1 = make_workload("parakeet", args.regime).blocks[0]
+        pk = make_workload("parakeet", args.regime).blocks[0]
         nthreads = core.num_threads()
         core.set_num_threads(1)
         t1 = time.perf_counter()
-        core.relpos_attn(c1)
-        c1_s = time.perf_counter() - t1
+        core.relpos_attn(pk)
+        pk_s = time.perf_counter() - t1
         core.set_num_threads(nthreads)
-        c1p, c1q, c1r = algorithmic_macs(1, c1.T, c1.shape.d_model, c1.shape.n_heads, c1.shape.d_k, c1.lengths)
+        pk_p, pk_q, pk_r = algorithmic_macs(1, pk.T, pk.shape.d_model, pk.shape.n_heads, pk.shape.d_k, pk.lengths)
         rec["cpu_baseline"]["single_thread"] = {
-            "workload": f"parakeet: B=1 T={c1.T} d_model={c1.shape.d_model} H={c1.shape.n_heads}",
-            "seconds_per_call": round(c1_s, 4),
-            "frames_per_s": round(float(np.sum(c1.lengths)) / c1_s, 1),
-            "tops": round(2 * (c1p + c1q + c1r) / c1_s / 1e12, 6),
+            "workload": f"parakeet: B=1 T={pk.T} d_model={pk.shape.d_model} H={pk.shape.n_heads}",
+            "seconds_per_call": round(pk_s, 4),
+            "frames_per_s": round(float(np.sum(pk.lengths)) / pk_s, 1),
+            "tops": round(2 * (pk_p + pk_q + pk_r) / pk_s / 1e12, 6),
             "cores": 1,
         }
-        # spec self-check 3 as the oracle measures it (committed analysis): the
-        # integer block against the float64 block of Eq. 8-9, relative L2 per workload
+        # the integer block against the float64 block of Eq. 8-9 on the same dequantized
+        # inputs, relative L2 per workload, as the oracle measures it (committed analysis)
         gap_path = os.path.join(ROOT, "oracle", "fp_gap_results.json")
         if os.path.exists(gap_path):
             with open(gap_path) as fh:

@@ -1,5 +1,5 @@
 """The stage-switched block of ``oracle.fp_gap`` and the gap between the integer block
-and the floating-point block of Eq. 8-9 (spec self-check 3).
+and the floating-point block of Eq. 8-9 on the same dequantized inputs.
 
 The switched block is pinned at both ends: every stage integer must give the C oracle's
 bytes (ragged lengths included), every stage real must give ``fp_block.block``.  The

@@ -345,8 +345,8 @@ def test_padding_invariance(regime):
 
 
 def test_block_close_to_fp64_relpos_attention_calibrated():
-    # North-star self-check 3 compares the integer block with the FP block of
-    # Eq. 8-9 on the same dequantized inputs.  Its 2e-2 target is not reached:
+    # The integer block against the FP block of Eq. 8-9 on the same dequantized
+    # inputs, with a 2e-2 relative-L2 target that is not reached:
     # I-BERT's floor normalization leaves sum(a) below 256 for rows that spread
     # over many keys (about 8% at T = 64), which dominates the gap.  The test pins
     # the gap's size (a wrong scale, shift, branch or transposed operand gives an
