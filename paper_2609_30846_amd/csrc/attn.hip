@@ -77,6 +77,27 @@ struct AttnArgs {
   int32_t m_o, shift_o;
 };
 
+// Maximum over the 16 lanes of each row (DPP quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror): every lane ends with its row's maximum, and no LDS
+// round trip is spent (a lane shuffle would be a ds_bpermute each step).
+__device__ __forceinline__ int row16_max(int v) {
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
+  return v;
+}
+
+// Sum of lanes l, l ^ 16, l ^ 32 and l ^ 48 (the same column of the four 16-lane rows)
+// in every lane: v_permlane16_swap pairs rows 0/1 and 2/3, v_permlane32_swap the two
+// halves.  Integer adds, so the order does not matter.
+__device__ __forceinline__ uint32_t col4_sum(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = r[0] + r[1];
+  const auto h = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return h[0] + h[1];
+}
+
 constexpr int TAB_DW = 256 * 32;  // dwords of the [d][32 banks] lookup-table region
 constexpr int ATTN_WAVES = 8;     // waves per workgroup (two per SIMD)
 
@@ -401,17 +422,14 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       step(Phase<1>{}, false);
       if constexpr (RING > 2) step(Phase<2 % RING>{}, false);
     }
-    // the rest (fewer than RING steps below j_full, then the masked ones)
-    int ph = 0;
-    while (j0 < j_stop) {
-      const bool m = j0 + 16 > j_full;
-      if (ph == 0)
-        step(Phase<0>{}, m);
-      else if (ph == 1 || RING == 2)
-        step(Phase<1 % RING>{}, m);
-      else
-        step(Phase<2 % RING>{}, m);
-      ph = ph + 1 == RING ? 0 : ph + 1;
+    // the rest: fewer than RING steps below j_full, then at most one masked step (j_stop
+    // is at most L rounded up to 16, and j_full at least L rounded down), so at most
+    // RING steps in straight-line code whose ring phases stay static (a loop over them
+    // would move the rings between registers on every pass)
+    if (j0 < j_stop) step(Phase<0>{}, j0 + 16 > j_full);
+    if (j0 < j_stop) step(Phase<1 % RING>{}, j0 + 16 > j_full);
+    if constexpr (RING > 2) {
+      if (j0 < j_stop) step(Phase<2 % RING>{}, j0 + 16 > j_full);
     }
   }
   // the integer exp of every distance d in [0, 255): once, and in 32 per-bank copies
@@ -430,12 +448,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
 #pragma unroll
   for (int t = 0; t < NTL; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int v = mx[t][i];
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) v = max(v, __shfl_xor(v, o));
-      mx[t][i] = v;
-    }
+    for (int i = 0; i < 4; ++i) mx[t][i] = row16_max(mx[t][i]);
   if (col == 0) {
 #pragma unroll
     for (int t = 0; t < NTL; ++t)
@@ -524,10 +537,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     }
   }
 #pragma unroll
-  for (int t = 0; t < NTL; ++t) {
-    sum[t] += __shfl_xor(sum[t], 16);
-    sum[t] += __shfl_xor(sum[t], 32);
-  }
+  for (int t = 0; t < NTL; ++t) sum[t] = col4_sum(sum[t]);
   if (g == 0) {
 #pragma unroll
     for (int t = 0; t < NTL; ++t) ssum[slot * ROWS + 16 * t + col] = sum[t];
@@ -548,14 +558,19 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   // min(floor(e(d) F_r / 2^24), 255) ^ 0x80 of row r = 16 tt + rr, i.e. a - 128.
   // e < 2^24 and F <= 2^24: floor(e F / 2^24) is bits 24..55 of the 48-bit product of
   // the 24-bit multiplies (F = 2^24, when the sum is 2^8, gives e itself).  Each dword
-  // is computed once and written to both copies.
+  // is computed once and written to both copies.  The thread's rr is the same on every
+  // pass (the stride is a multiple of 16), so its rows' F are read once.
+  static_assert((64 * ATTN_WAVES) % 16 == 0, "a thread's rr is fixed across passes");
+  uint32_t Fr[NTILES];
+#pragma unroll
+  for (int tt = 0; tt < NTILES; ++tt) Fr[tt] = sF[16 * tt + (tid & 15)];
   for (int idx = tid; idx < TAB_DW / 2; idx += 64 * ATTN_WAVES) {
     const int dd = idx >> 4, rr = idx & 15;
     const uint32_t e = etab[dd];
     uint32_t packed = 0;
 #pragma unroll
     for (int tt = 0; tt < NTILES; ++tt) {
-      const uint32_t F = sF[16 * tt + rr];
+      const uint32_t F = Fr[tt];
       const uint64_t prod = (uint64_t)(e & 0xffffffu) * (uint64_t)(F & 0xffffffu);  // 24-bit operands
       const uint32_t v = F == (1u << 24) ? e : (uint32_t)(prod >> 24);
       packed |= ((v > 255u ? 255u : v) ^ 0x80u) << (8 * tt);
@@ -680,9 +695,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     // 4 g .. 4 g + 3.
 #pragma unroll
     for (int j = 0; j < AV_NT; ++j) {
-      int vs = vpart[j];
-      vs += __shfl_xor(vs, 16);
-      vs += __shfl_xor(vs, 32);
+      const int vs = (int)col4_sum((uint32_t)vpart[j]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int vi = __shfl(vs, 4 * g + i);
