@@ -243,8 +243,20 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   constexpr int LOCODE = WIDE ? 1 : (1 << 16);  // code of s = -127 (biased s + 128)
   constexpr int HICODE = WIDE ? 255 : ((255 << 16) | 0xFFFF);
 
-  // the integer exp of this thread's distance, written to LDS after phase 1
+  // the integer exp of this thread's distance
   const uint32_t e_mine = a.etab[tid & 255];
+  // the integer exp of every distance d in [0, 255): once, and in 32 per-bank copies
+  // (copy (d + c) % 32 of pass c is written by the thread of d, which keeps the writes
+  // free of bank conflicts).  Phase 1 does not touch the table region, so these stores
+  // go out while its first operands load.
+  {
+    const int dd = tid & 255;
+    if (tid < 256) etab[dd] = e_mine;
+    for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e_mine;
+    }
+  }
 
   // ---------------- phase 1: fused scores into LDS, running row max
   int mx[NTL][4];
@@ -432,18 +444,6 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
       if (j0 < j_stop) step(Phase<2 % RING>{}, j0 + 16 > j_full);
     }
   }
-  // the integer exp of every distance d in [0, 255): once, and in 32 per-bank copies
-  // (copy (d + c) % 32 of pass c is written by the thread of d, which keeps the writes
-  // free of bank conflicts)
-  {
-    const int dd = tid & 255;
-    if (tid < 256) etab[dd] = e_mine;
-    for (int c = (tid >> 8) * 16; c < 32; c += 16 * (64 * ATTN_WAVES / 256)) {
-#pragma unroll
-      for (int k = 0; k < 16; ++k) tab[dd * 32 + ((c + k + dd) & 31)] = e_mine;
-    }
-  }
-
   // row max over the 16 key lanes of each row group
 #pragma unroll
   for (int t = 0; t < NTL; ++t)
@@ -590,11 +590,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
     auto code_at = [&](uint32_t dw, int k, int t) {
       return (uint32_t) * (const lds8*)(uintptr_t)__builtin_amdgcn_udot4(dw, 128u << (8 * k), cbase[t], false);
     };
-    // four codes of one dword: two 16-bit halves, then one merge
+    // four codes of one dword: two 16-bit halves (a shift-or each), then one byte
+    // permute that takes bytes 0, 1 of each (three instructions per four codes)
     auto codes4 = [&](uint32_t dw, int t) {
       const uint32_t lo = code_at(dw, 0, t) | (code_at(dw, 1, t) << 8);
       const uint32_t hi = code_at(dw, 2, t) | (code_at(dw, 3, t) << 8);
-      return (int)(lo | (hi << 16));
+      return (int)__builtin_amdgcn_perm(hi, lo, 0x05040100u);
     };
     // the next chunk is read before the current one is written back (chunks are disjoint)
     v4i svn[NTL];
