@@ -132,16 +132,16 @@ int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos
  * ipk_relpos_attn_run without any device allocation, for callers that cannot allocate
  * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
  * Same arguments, results and errors as ipk_relpos_attn_run; the run's workspace (Q,
- * K, V^T, the projected position table unless pos_table is NULL, the V sums and the
- * context) lives in one static device array of IPK_NOALLOC_SCRATCH_BYTES per GPU
- * instead of the handle's: the library's code object holds it, each GPU the library
+ * K, V^T, the projected position table unless pos_table is NULL, and the context)
+ * lives in one static device array of IPK_NOALLOC_SCRATCH_BYTES per GPU instead of
+ * the handle's: the library's code object holds it, each GPU the library
  * runs on keeps its copy until the process ends, and its address is looked up on the
  * device's first call.  The call allocates nothing and calls no allocating routine.
  * Workspace bytes, each part rounded up to 256:
- *   3 B H T_al d_k + H (2 T_al + 256) d_k (only with a pos_table) + B T d_model
- *   + 4 B H (T_al / 64) d_k,  T_al = T rounded up to 64
- * (one 2500-frame utterance at d_model 1024, 8 heads: 16.1 MB; 16 x 375 frames:
- * 26.5 MB).
+ *   3 B H T_al d_k + H (2 T_al + 256) d_k (only with a pos_table) + B T d_model,
+ *   T_al = T rounded up to 64
+ * (one 2500-frame utterance at d_model 1024, 8 heads: 15.9 MB; 16 x 375 frames:
+ * 26.1 MB).
  * All no-allocation calls on one GPU share that array, whatever their handle or
  * stream, and it keeps the last call's contents (nothing in it has to start at zero:
  * every byte a run reads was written by the same run, or is masked): calls that
@@ -180,8 +180,7 @@ int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst,
  * Stage timing for profiling: the NEXT run on `h` records the IPK_NUM_STAGES + 1
  * caller-created HIP events events[0..3] (hipEvent_t, created with timing enabled)
  * on its stream: events[0..2] when the three stages start (the Q|K|V and position
- * projections, which also produce the rank-1 terms u.K_j, v.P_r and the V sums;
- * the attention core; the output projection), events[3] when the output projection
+ * projections; the attention core; the output projection), events[3] when the output projection
  * ends.  The events are carried by the kernel dispatches themselves, so recording
  * them adds no work to the stream.  The events are used once; later runs record
  * nothing until this is called again.  events = NULL clears a pending request.

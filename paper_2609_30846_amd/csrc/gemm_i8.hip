@@ -77,7 +77,6 @@ struct GemmArgs {
   int per_xcd;  // logical tiles dealt to each XCD
   int8_t *q, *k, *vt, *p, *y;
   int T_al, H, dk_shift, d, p_rows, p_base;  // d_k = 2^dk_shift
-  int32_t* vsum;  // sums of V over each 64-key chunk, produced by the epilogue
   // residual add of the MHSA module (row-major outputs only): y := clamp8(RS(m_z z1 +
   // m_y y, 1, shift_r)) with z1 laid out as y
   const int8_t* z1;
@@ -203,7 +202,6 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   constexpr int FROWS = NTH / 8;            // rows one pass of the fetch covers
   constexpr int KSL = BK / 32;              // 32-byte K slices per step
   static_assert(FN >= 1 && FM >= 1 && LX >= 1 && WTM % 32 == 0 && NTH >= TN && NWAVE % WN == 0, "tile shape");
-  constexpr int CPW = WTM >= KCHUNK ? WTM / KCHUNK : 1;  // 64-key chunks per wave (V sums)
   // two LDS buffers: the next K step is stored while the current one is multiplied
   __shared__ __align__(16) int8_t sx[2][TM * BK];
   __shared__ __align__(16) int sreq[2][TN];  // Eq. 7 constants of the tile's channels
@@ -364,14 +362,19 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   // its column, 16 bytes each.  A 32-channel sub-tile never straddles N, a head or the
   // Q/K/V boundary (N and d_k are multiples of 64), so its destination is uniform.
   //
-  // The same pass sums the int8 V values it stores over each 64-key chunk (a wave's
-  // WTM tokens are WTM / 64 whole chunks, two 32-token MFMA columns each; the two
-  // half-waves hold the two halves of a column).  V^T is written up to T_al, so the
-  // padded keys hold zeros, as the sums do.
+  // V^T is written up to T_al, so the padded keys hold zeros (a wave's WTM tokens are
+  // WTM / 64 whole 64-key blocks of V^T, two 32-token MFMA columns each).
   const int col = lane & 31;
   const int tw0 = t0 + wm * WTM;
-  const int dks = args.dk_shift, DK = 1 << dks, DKm = DK - 1;
-  const size_t head_bytes = (size_t)args.T_al << dks;  // one (utterance, head) block of Q, K or V^T
+  // the epilogue's arguments, loaded together (one wait, not one per first use)
+  int8_t *o_q = args.q, *o_k = args.k, *o_vt = args.vt, *o_p = args.p, *o_y = args.y;
+  const int8_t* o_z1 = args.z1;
+  int o_T_al = args.T_al, o_H = args.H, o_d = args.d, o_prows = args.p_rows, o_pbase = args.p_base, dks = args.dk_shift;
+  asm volatile(""
+               : "+s"(o_q), "+s"(o_k), "+s"(o_vt), "+s"(o_p), "+s"(o_y), "+s"(o_z1), "+s"(o_T_al), "+s"(o_H), "+s"(o_d),
+                 "+s"(o_prows), "+s"(o_pbase), "+s"(dks));
+  const int DK = 1 << dks, DKm = DK - 1;
+  const size_t head_bytes = (size_t)o_T_al << dks;  // one (utterance, head) block of Q, K or V^T
   // frag_index / vt_index with d_k = 2^dks
   auto frag_off = [&](int row, int kk) {
     return ((size_t)(row >> 4) << (dks + 4)) + (size_t)((kk >> 6) << 10) + (((((kk >> 4) & 3) << 4) + (row & 15)) << 4) +
@@ -380,11 +383,6 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
   auto vt_off = [&](int t, int kk) {
     return ((size_t)(t >> 6) << (dks + 6)) + (size_t)((kk >> 4) << 10) + (((((t >> 4) & 3) << 4) + (kk & 15)) << 4) +
            (t & 15);
-  };
-  // sum over both half-waves (lanes l and l ^ 32)
-  auto half_sum = [](int x) {
-    const auto s2 = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);
-    return (int)(s2[0] + s2[1]);
   };
 #pragma unroll
   for (int i = 0; i < FN; ++i) {
@@ -396,18 +394,18 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
     int kk = 0;  // channel of the sub-tile's first row inside its head
     int hd = 0;  // its head
     if (mode == OUT_QKV) {
-      const int which = (nb >= args.d) + (nb >= 2 * args.d);
-      const int c = nb - which * args.d;
+      const int which = (nb >= o_d) + (nb >= 2 * o_d);
+      const int c = nb - which * o_d;
       hd = c >> dks;
-      dst = (which == 0 ? args.q : which == 1 ? args.k : args.vt) + ((size_t)ub * args.H + hd) * head_bytes;
+      dst = (which == 0 ? o_q : which == 1 ? o_k : o_vt) + ((size_t)ub * o_H + hd) * head_bytes;
       kk = c & DKm;
     } else if (mode == OUT_POS) {
       hd = nb >> dks;
-      dst = args.p + ((size_t)hd * args.p_rows << dks);
+      dst = o_p + ((size_t)hd * o_prows << dks);
       kk = nb & DKm;
     } else {
-      dst = args.y + (size_t)ub * rows * N + nb;
-      zsrc = args.z1 + (size_t)ub * rows * N + nb;
+      dst = o_y + (size_t)ub * rows * N + nb;
+      zsrc = o_z1 + (size_t)ub * rows * N + nb;
     }
     // the tile-local channel of element e: with rows as tokens (V^T) the column, else
     // row g * 8 + half * 4 + e' of element e = 4g + e'
@@ -434,19 +432,15 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
     uint32_t off0;
     if (vwave) {
       tl = tw0 + half * 16;
-      tmax = args.T_al;
+      tmax = o_T_al;
       off0 = (uint32_t)vt_off(tl, kk + col);
     } else {
       tl = tw0 + col;
       tmax = rows;
       off0 = mode == OUT_ROWMAJOR ? (uint32_t)(tl * N + half * 16)
-                                  : (uint32_t)frag_off((mode == OUT_POS ? args.p_base : 0) + tl, kk + half * 16);
+                                  : (uint32_t)frag_off((mode == OUT_POS ? o_pbase : 0) + tl, kk + half * 16);
     }
     const uint32_t jstep = mode == OUT_ROWMAJOR ? 32u * (uint32_t)N : 2u << (dks + 4);
-    // this lane's share of the V sum of channel kk + col over each of the wave's chunks
-    int vpart[CPW];
-#pragma unroll
-    for (int c = 0; c < CPW; ++c) vpart[c] = 0;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       int v[16];
@@ -472,21 +466,6 @@ __global__ __launch_bounds__(64 * NWAVE) void gemm_i8_requant(GemmArgs args) {
         if (EPI == EPI_RESID)
           out = residual16(out, *(const v4i*)(zsrc + (off0 + joff)), args.m_z, args.m_y, args.shift_r);
         *(v4i*)(dst + (off0 + joff)) = out;
-      }
-      if (vwave) {
-#pragma unroll
-        for (int wd = 0; wd < 4; ++wd) vpart[j / 2] = __builtin_amdgcn_sdot4(out[wd], 0x01010101, vpart[j / 2], false);
-      }
-    }
-    if (vwave) {
-      // sums of V over the 64-key chunks tw0 / 64 + c, channel kk + col: [chunk][n % 16][n / 16]
-      const int n = kk + col, nch = args.T_al >> 6;
-#pragma unroll
-      for (int c = 0; c < CPW; ++c) {
-        const int tot = half_sum(vpart[c]);
-        const int tc = tw0 + c * KCHUNK;
-        if (half == 0 && tc < args.T_al)
-          args.vsum[((((size_t)ub * args.H + hd) * nch + (tc >> 6)) * 16 + (n & 15)) * (DK >> 4) + (n >> 4)] = tot;
       }
     }
   }
@@ -537,7 +516,6 @@ static void fill_dest(GemmArgs& a, const RunShape& rs, const Workspace& ws, int8
   a.d = rs.d;
   a.p_rows = rs.p_rows;
   a.p_base = rs.p_base;
-  a.vsum = ws.vsum;
 }
 
 template <int TN, int TM, int NWAVE, int WN, int EPI = EPI_PLAIN, int TPF = 1>
@@ -578,7 +556,7 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
   const int TMr = pick_tile_rows(256, 128, tiles_of);
   auto go = [&](auto tm_tag) {
     constexpr int TM = decltype(tm_tag)::value;
-    // the epilogue's V sums: a wave's tokens are whole 64-key chunks
+    // V^T's 64-key blocks: a wave's tokens are whole blocks
     static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
     GemmArgs a{};
     fill_dest(a, rs, ws, nullptr);

@@ -251,7 +251,6 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   chk(dev_alloc(h, &h->ws.vt, Bm * H * DK * T_al));
   chk(dev_alloc(h, &h->ws.p, H * PR * DK));
   chk(dev_alloc(h, &h->ws.ctx, Bm * (size_t)h->max_T * d));
-  chk(dev_alloc(h, &h->ws.vsum, Bm * H * (T_al / KCHUNK) * DK));
   if (e != hipSuccess) {
     free_handle(h);
     (void)hipGetLastError();
@@ -354,7 +353,6 @@ static int enqueue_run(ipk_relpos_attn* h, RunShape rs, const Lengths& lens, Wor
     x = ws.xln;
     ev[0] = LaunchEv{};
   }
-  // the projections also produce the V sums the core reads
   if (e == hipSuccess) e = launch_projections(rs, h->w, ws, x, pos_table, st, ev[0]);
   if (e == hipSuccess) e = launch_attention(rs, h->w, h->sc, ws, lens, st, ev[1]);
   if (e == hipSuccess) e = launch_out_projection(rs, h->w, ws, y, st, ev[2], z1 ? &h->res : nullptr, z1);
@@ -398,7 +396,6 @@ static size_t carve_workspace(const RunShape& rs, bool own_p, uint8_t* base, Wor
   ws->vt = (int8_t*)take(B * H * DK * T_al);
   ws->p = own_p ? (int8_t*)take(H * (size_t)rs.p_rows * DK) : nullptr;
   ws->ctx = (int8_t*)take(B * (size_t)rs.T * rs.d);
-  ws->vsum = (int32_t*)take(B * H * (T_al / KCHUNK) * DK * sizeof(int32_t));
   ws->xln = nullptr;
   return off;
 }

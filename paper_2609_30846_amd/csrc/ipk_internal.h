@@ -21,9 +21,6 @@
 //                chosen per run so that the table row j-i+T-1 of every 16-query by
 //                16-key tile starts a 16-row block.  The rows around the table keep
 //                every padded tile in bounds (their contents are never used).
-//   vsum   int32 [B][H][T_al/64][16][DK/16] sums of V over each 64-key chunk; channel n
-//                                   at [n % 16][n / 16] (written by the projection
-//                                   GEMM's epilogue)
 //   ctx    int8  [B][T][d]          attention output, heads concatenated
 #pragma once
 
@@ -67,7 +64,6 @@ __host__ __device__ inline size_t vt_index(int t, int kk, int DK) {
 
 struct Workspace {
   int8_t *q, *k, *vt, *p, *ctx;
-  int32_t* vsum;
   int8_t* xln;  // LayerNorm output [B][T][d] of the MHSA module's runs
 };
 
