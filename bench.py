@@ -47,17 +47,24 @@ def algorithmic_macs(B, T, d, H, dk, lengths):
     return proj, pos, attn
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(csrc: str = None) -> str:
     """Hash of the kernel sources (the HIP files and their shared header; the C-ABI
-    glue in ipk_api.cpp does not change what a kernel reads or writes)."""
+    glue in ipk_api.cpp does not change what a kernel reads or writes), with comments
+    and whitespace left out: only a change to the code itself invalidates a
+    measurement taken on it."""
     import glob
     import hashlib
+    import re
 
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_30846_amd", "csrc")
+    csrc = csrc or os.path.join(ROOT, "paper_2609_30846_amd", "csrc")
     for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+        with open(f, encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        code = " ".join(text.split())
+        h.update(os.path.basename(f).encode() + b"\0" + code.encode())
     return h.hexdigest()[:16]
 
 

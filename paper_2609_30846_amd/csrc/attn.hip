@@ -24,11 +24,11 @@
 //              integers.  Scores are kept as biased codes s + 128 in [1, 255].
 //  * each score byte is stored straight into its row's block (one address add per
 //    step: the tile and row offsets are instruction immediates).
-// Phase 2 (row sums): row max over the key splits (LDS); every lane then reads 16
-// scores of one row (16 bytes), forms the four distances d = M - s of each dword with
-// one subtraction (every s <= M, so no byte borrows), and looks up the I-BERT integer
-// exp of each d in a table with one copy per LDS bank; the address of one lookup is
-// a single v_dot4 (base + 128 d).
+// Phase 2 (row sums): row max over a row's 16 key lanes (DPP) and over the key splits
+// (LDS); every lane then reads 16 scores of one row (16 bytes), forms the four
+// distances d = M - s of each dword with one subtraction (every s <= M, so no byte
+// borrows), and looks up the I-BERT integer exp of each d in a table with one copy per
+// LDS bank; the address of one lookup is a single v_dot4 (base + 128 d).
 // Conversion: F = floor(2^32 / sum) per row (integer long division), per-row tables of
 // the softmax code a - 128 = min(floor(e F / 2^24), 255) - 128, and every score byte of
 // the workgroup replaced in place by its code.  Keys past the utterance take distance
