@@ -74,7 +74,7 @@ def _check_block(ipk, blk, label):
     assert _first_mismatch(g["y"], y) is None, (label, "y", _first_mismatch(g["y"], y))
 
 
-@pytest.mark.parametrize("regime", ["literal", "calibrated"])
+@pytest.mark.parametrize("regime", ["literal", "calibrated", "minmax"])
 @pytest.mark.parametrize("name", ["tiny", "parakeet"])
 def test_small_configs(gpu_lib, name, regime, score_path):
     blk = make_workload(name, regime).blocks[0]
@@ -119,13 +119,13 @@ def test_ragged_shapes(gpu_lib, T, d, H, B, lengths, regime, score_path):
     _check_block(gpu_lib, blk, f"T{T}-d{d}-H{H}-B{B}/{regime}")
 
 
-@pytest.mark.parametrize("regime", ["literal", "calibrated"])
+@pytest.mark.parametrize("regime", ["literal", "calibrated", "minmax"])
 def test_batched_masked(gpu_lib, regime, score_path):
     blk = make_workload("batched", regime).blocks[0]
     _check_block(gpu_lib, blk, f"batched/{regime}")
 
 
-@pytest.mark.parametrize("regime", ["literal", "calibrated"])
+@pytest.mark.parametrize("regime", ["literal", "calibrated", "minmax"])
 def test_longform(gpu_lib, regime, score_path):
     blk = make_workload("longform", regime).blocks[0]
     print(f"[parity] longform/{regime}", flush=True)

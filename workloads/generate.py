@@ -13,12 +13,17 @@ them with inputs of the same shapes, value ranges and length mix:
   positions (Sec. 3.1), quantized with S_pe = 1/127;
 * fixed-point multipliers use n = 16 (Eq. 7).
 
-Two scale regimes exist.  ``literal`` draws every per-tensor scale (and every
+Three scale regimes exist.  ``literal`` draws every per-tensor scale (and every
 per-channel weight scale) uniformly from [2^-8, 2^-4].  ``calibrated`` gives the
 real-valued activations unit variance and the weights Xavier scale, and then sets
 each grid to cover +-4 standard deviations of the tensor it quantizes, estimated
 from the known input distributions (no data pass); this gives non-saturated
-integer ranges.  Draw order is fixed: x, W_q, W_k, W_v, W_pos, W_out, u, v,
+integer ranges.  ``minmax`` draws everything as ``literal`` does (the same integer
+inputs, S_x and weight scales) and takes the block's seven output grids (S_Q, S_K,
+S_V, S_P, S_s, S_O, S_y) from a min-max calibration of the floating-point block on
+that same input (Eq. 6: S = max|.| / 127), stored in ``tests/golden/minmax_scales.json``
+by a script of the test oracle (``python -m oracle.calibrate``); this module only
+reads the numbers.  Draw order is fixed: x, W_q, W_k, W_v, W_pos, W_out, u, v,
 scales, lengths.
 
 The conversion of real scales to integers (the multiplier m of Eq. 7, m_c and
@@ -29,7 +34,9 @@ with exact decimal arithmetic: the block itself only ever sees the integers.
 from __future__ import annotations
 
 import dataclasses
+import json
 import math
+import os
 from decimal import Decimal, ROUND_FLOOR, getcontext
 from typing import Dict, List, Optional
 
@@ -240,9 +247,29 @@ def _consts_from_scales(sc, shape: ConfigShape):
     return c
 
 
+MINMAX_GRIDS = ("S_Q", "S_K", "S_V", "S_P", "S_s", "S_O", "S_y")
+MINMAX_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "tests", "golden",
+                           "minmax_scales.json")
+
+
+def minmax_key(name: str, B: int, T: int, seed: int) -> str:
+    return f"{name}:B={B}:T={T}:seed={seed}"
+
+
+def load_minmax_grids(name: str, B: int, T: int, seed: int) -> List[Dict[str, float]]:
+    """The stored min-max grids of one workload, one dict per layer."""
+    with open(MINMAX_PATH) as fh:
+        table = json.load(fh)
+    key = minmax_key(name, B, T, seed)
+    if key not in table["workloads"]:
+        raise KeyError(f"no min-max grids stored for {key}; python -m oracle.calibrate writes them")
+    return table["workloads"][key]
+
+
 def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str = "literal",
                with_x: bool = True, S_x: Optional[float] = None, lengths=None,
-               logit_gain: float = 1.0, w_scale: Optional[float] = None) -> Block:
+               logit_gain: float = 1.0, w_scale: Optional[float] = None,
+               grids: Optional[Dict[str, float]] = None, with_consts: bool = True) -> Block:
     d, H, dk = shape.d_model, shape.n_heads, shape.d_k
     x = _draw_x(rng, shape, T) if with_x else None
     ws = [_uniform_i8(rng, (d, d)) for _ in range(5)]
@@ -252,6 +279,13 @@ def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str
         sc = _scales_literal(rng, shape, S_x)
     elif regime == "calibrated":
         sc = _scales_calibrated(rng, shape, S_x, logit_gain, w_scale)
+    elif regime == "minmax":
+        # the literal draws (the random stream stays the same), then the calibrated grids
+        sc = _scales_literal(rng, shape, S_x)
+        if grids is None and with_consts:
+            raise ValueError("the minmax regime needs the block's calibrated grids")
+        for k in MINMAX_GRIDS if grids is not None else ():
+            sc[k] = float(grids[k])
     else:
         raise ValueError(regime)
     sc["S_pe"], sc["S_A"] = S_PE, S_A
@@ -263,7 +297,7 @@ def make_block(shape: ConfigShape, T: int, rng: np.random.Generator, regime: str
     lengths = np.asarray(lengths, dtype=np.int32)
     return Block(shape=shape, T=T, x=x, w_q=ws[0], w_k=ws[1], w_v=ws[2], w_pos=ws[3], w_out=ws[4],
                  pos_bias_u=u, pos_bias_v=v, pos_table=sinusoid_table(T, d), lengths=lengths,
-                 scales=sc, consts=_consts_from_scales(sc, shape))
+                 scales=sc, consts=_consts_from_scales(sc, shape) if with_consts else {})
 
 
 def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = None,
@@ -283,13 +317,16 @@ def make_workload(name_or_idx, regime: str = "literal", seed: Optional[int] = No
     if shape.len_lo is not None and T < shape.len_lo:
         shape = dataclasses.replace(shape, len_lo=max(1, T // 2))
     nl = shape.layers if layers is None else layers
+    grids = load_minmax_grids(shape.name, shape.B, T, seed)[:nl] if regime == "minmax" else [None] * nl
+    if len(grids) < nl:
+        raise KeyError(f"min-max grids stored for {len(grids)} of {nl} layers")
     blocks: List[Block] = []
     S_x = None
     lengths = None
     for layer in range(nl):
         rng = np.random.default_rng(seed + layer)
         blk = make_block(shape, T, rng, regime, with_x=(layer == 0), S_x=S_x, lengths=lengths,
-                         logit_gain=logit_gain, w_scale=w_scale)
+                         logit_gain=logit_gain, w_scale=w_scale, grids=grids[layer])
         blocks.append(blk)
         S_x = blk.scales["S_y"]
         lengths = blk.lengths
