@@ -213,6 +213,18 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, unsigned char* sme
   const int q0 = wg_q0 + ROWS * qset;  // first query of this wave's set
   const int L = a.lens.len[b];
   const int T = a.T, T_al = a.T_al;
+  if (wg_q0 >= L) {
+    // no valid query in this workgroup (a ragged batch): its context rows are zeros,
+    // and nothing else of it is needed
+    const int tid0 = threadIdx.x;
+    constexpr int PIECES = DK / 16;  // 16-byte pieces of one row's head slice
+    for (int idx = tid0; idx < WGQ * PIECES; idx += 64 * ATTN_WAVES) {
+      const int qi = wg_q0 + idx / PIECES;
+      if (qi < T)
+        *(v4i*)(a.ctx + ((size_t)b * T + qi) * a.d + (size_t)h * DK + (idx % PIECES) * 16) = (v4i){0, 0, 0, 0};
+    }
+    return;
+  }
   const int nkc = (L + KCHUNK - 1) / KCHUNK;
   int c_begin, c_end;
   split(nkc, P2_OLDER, &c_begin, &c_end);
@@ -838,8 +850,16 @@ static bool fits(const AttnCfg& c, int DK, int T_al) { return attn_lds_bytes(DK,
 // Time of one workgroup, modelled per key of a wave's share as 125 cycles for the K, P
 // and V streams (the same for any number of query tiles) plus 29 per 16-query tile
 // (score post-processing, exp sums, code lookups, combine), as measured on the
-// long-form workload.
-static double wg_cost(const AttnCfg& c, int T) { return ((double)T / c.ksplit) * (125.0 + 29.0 * c.ntl); }
+// long-form workload, plus a fixed ~16 K cycles that do not scale with T (operand
+// loads before the first step, the exp and code tables, F, the barriers and the
+// combine): at T = 500 a 48-query workgroup lives ~25 K cycles.  Without the fixed
+// part, short utterances in large batches took 48-query workgroups in more rounds where
+// 64-query ones in fewer finish first (T = 375 x 16 and 500 x 8: 13 - 17 % less time in
+// the core, measured).  At T = 2500 the fixed part does not change the plan.
+constexpr double kWgFixedCost = 16000.0;
+static double wg_cost(const AttnCfg& c, int T) {
+  return kWgFixedCost + ((double)T / c.ksplit) * (125.0 + 29.0 * c.ntl);
+}
 
 // Finishing time of groups of workgroups (count[g] of cost[g] each) started in order on
 // the CUs, one workgroup per CU (eight waves of more than 128 VGPRs), each CU taking the
