@@ -540,6 +540,13 @@ static int pick_tile_rows(int big, int small, F tiles_of) {
   return cost(small) < cost(big) ? small : big;
 }
 
+// A tile shape of the projection launch (channels, tokens, waves, waves along channels,
+// token-tile prefetch depth).
+template <int TN_, int TM_, int NWAVE_, int WN_, int TPF_>
+struct ProjShape {
+  static constexpr int tn = TN_, tm = TM_, nwave = NWAVE_, wn = WN_, tpf = TPF_;
+};
+
 hipError_t launch_projections(const RunShape& rs, const Weights& w, const Workspace& ws, const int8_t* x,
                               const int8_t* pos_table, hipStream_t st, const LaunchEv& ev) {
   // 256-channel tiles of eight waves in a 4 x 2 grid (64 channels x TM/2 tokens each):
@@ -554,21 +561,27 @@ hipError_t launch_projections(const RunShape& rs, const Weights& w, const Worksp
     return t;
   };
   const int TMr = pick_tile_rows(256, 128, tiles_of);
-  auto go = [&](auto tm_tag) {
-    constexpr int TM = decltype(tm_tag)::value;
+  auto go = [&](auto shape_tag) {
+    using S = decltype(shape_tag);
+    constexpr int TNs = S::tn, TMs = S::tm, NW = S::nwave, WNs = S::wn, TPFs = S::tpf;
     // V^T's 64-key blocks: a wave's tokens are whole blocks
-    static_assert((TM / (NWAVE / WN)) % KCHUNK == 0 && (TN / WN) % 32 == 0, "projection tile shape");
+    static_assert((TMs / (NW / WNs)) % KCHUNK == 0 && (TNs / WNs) % 32 == 0, "projection tile shape");
     GemmArgs a{};
     fill_dest(a, rs, ws, nullptr);
-    int tiles = add_problem(a, 0, x, w.w_qkv, w.rq_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TN, TM);
+    int tiles = add_problem(a, 0, x, w.w_qkv, w.rq_qkv, rs.B, rs.T, 3 * rs.d, rs.d, OUT_QKV, 0, TNs, TMs);
     a.nprob = 1;
     if (pos_table) {
-      tiles += add_problem(a, 1, pos_table, w.w_pos, w.rq_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TN, TM);
+      tiles += add_problem(a, 1, pos_table, w.w_pos, w.rq_pos, 1, 2 * rs.T - 1, rs.d, rs.d, OUT_POS, tiles, TNs, TMs);
       a.nprob = 2;
     }
-    return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, ev);
+    return launch_gemm<TNs, TMs, NW, WNs, EPI_PLAIN, TPFs>(a, tiles, st, ev);
   };
-  return TMr == 128 ? go(std::integral_constant<int, 128>{}) : go(std::integral_constant<int, 256>{});
+  // a short call (few frames): where the 256-channel tiles would leave more than half of
+  // the CUs idle, 128-channel x 64-token tiles of four waves (32 channels x 64 tokens
+  // each, the token tile fetched two steps ahead) spread it over several times as many
+  // workgroups
+  if (tiles_of(TMr) < kGemmCUs / 2) return go(ProjShape<128, 64, 4, 4, 2>{});
+  return TMr == 128 ? go(ProjShape<TN, 128, NWAVE, WN, 1>{}) : go(ProjShape<TN, 256, NWAVE, WN, 1>{});
 }
 
 hipError_t launch_pos_projection(const RunShape& rs, const Weights& w, int8_t* p, const int8_t* pos_table,
