@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define IPK_ABI_VERSION 4
+#define IPK_ABI_VERSION 5
 
 /* Status codes. */
 typedef enum ipk_status {
@@ -188,6 +188,23 @@ int ipk_relpos_attn_intermediate(ipk_relpos_attn_t* h, int32_t which, void* dst,
  */
 enum { IPK_NUM_STAGES = 3 };
 int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* events);
+
+/*
+ * Kernel timing for profiling: enqueues the attention core of the last run on `h`
+ * (Eq. 8-11, the integer softmax and A.V: the middle stage above) `count` more times,
+ * back to back on `stream`, with that run's shapes, lengths and score path.  It reads
+ * the projections the last run left in the handle's workspace (or the kept position
+ * projection, as it is now) and rewrites the context there with the same bytes; nothing
+ * outside the handle is touched, so two events around the call time the kernel alone,
+ * with no event between its launches.  The last run must have used the handle's own
+ * workspace (ipk_relpos_attn_run or ipk_mhsa_residual_run, not the no-allocation run,
+ * whose array other calls share), on the current device.
+ * Errors: IPK_ERR_INVALID_ARG (null handle, no run yet, the last run was the
+ * no-allocation one, count outside [1, IPK_MAX_REPEAT], another current device),
+ * IPK_ERR_HIP (launch failure).
+ */
+#define IPK_MAX_REPEAT 100000
+int ipk_relpos_attn_repeat_core(ipk_relpos_attn_t* h, int32_t count, void* stream);
 
 /*
  * How the attention core evaluates the fused score of Eq. 11.  Both paths are exact

@@ -34,6 +34,9 @@ struct ipk_relpos_attn {
   bool has_run;
   bool last_was_residual;
   Workspace last_ws;  // the last run's buffers (ws, the kept table, or the no-allocation array)
+  Lengths last_lens;  // the last run's lengths and score constants, for ipk_relpos_attn_repeat_core
+  Scalars last_sc;
+  bool last_noalloc;  // the last run's workspace was the shared no-allocation array
   hipEvent_t stage_ev[IPK_NUM_STAGES + 1];
   bool stages_pending;
   // projected position table kept by ipk_relpos_attn_cache_positions
@@ -227,6 +230,7 @@ extern "C" int ipk_relpos_attn_create(const ipk_relpos_attn_desc* desc, ipk_relp
   h->has_run = false;
   h->last_was_residual = false;
   h->last_ws = Workspace{};
+  h->last_noalloc = false;
   h->stages_pending = false;
   h->pcache = nullptr;
   h->pcache_T = 0;
@@ -329,7 +333,7 @@ static int validate_run(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_t
 // module), projections, attention core, output projection (with the residual add when
 // z1 != NULL).  With pos_table NULL the kept projection replaces ws.p.
 static int enqueue_run(ipk_relpos_attn* h, RunShape rs, const Lengths& lens, Workspace ws, const int8_t* x,
-                       const int8_t* pos_table, int8_t* y, void* stream, const int8_t* z1) {
+                       const int8_t* pos_table, int8_t* y, void* stream, const int8_t* z1, bool noalloc) {
   if (!pos_table) {
     // table row r of this T is row r + T_table - T of the kept one, whose relative
     // position 0 sits at a 16-row boundary for every T
@@ -359,6 +363,9 @@ static int enqueue_run(ipk_relpos_attn* h, RunShape rs, const Lengths& lens, Wor
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   h->last = rs;
   h->last_ws = ws;
+  h->last_lens = lens;
+  h->last_sc = h->sc;
+  h->last_noalloc = noalloc;
   h->has_run = true;
   h->last_was_residual = z1 != nullptr;
   return IPK_OK;
@@ -370,7 +377,7 @@ static int run_on_handle(ipk_relpos_attn* h, const int8_t* x, const int8_t* pos_
   Lengths lens;
   const int st = validate_run(h, x, pos_table, lengths, B, T, y, &rs, &lens);
   if (st != IPK_OK) return st;
-  return enqueue_run(h, rs, lens, h->ws, x, pos_table, y, stream, z1);
+  return enqueue_run(h, rs, lens, h->ws, x, pos_table, y, stream, z1, false);
 }
 
 extern "C" int ipk_relpos_attn_run(ipk_relpos_attn_t* h, const int8_t* x, const int8_t* pos_table,
@@ -418,7 +425,7 @@ extern "C" int ipk_relpos_attn_run_noalloc(ipk_relpos_attn_t* h, const int8_t* x
   const hipError_t e = noalloc_scratch(&base, &cap);
   if (e != hipSuccess) return fail(IPK_ERR_HIP, "looking up the scratch array failed: %s", hipGetErrorString(e));
   carve_workspace(rs, pos_table != nullptr, base, &ws);
-  return enqueue_run(h, rs, lens, ws, x, pos_table, y, stream, nullptr);
+  return enqueue_run(h, rs, lens, ws, x, pos_table, y, stream, nullptr, true);
 }
 
 extern "C" int ipk_mhsa_residual_run(ipk_relpos_attn_t* h, const int8_t* z1, const int8_t* pos_table,
@@ -546,6 +553,23 @@ extern "C" int ipk_relpos_attn_record_stages(ipk_relpos_attn_t* h, void* const* 
     if (!events[i]) return fail(IPK_ERR_INVALID_ARG, "events[%d] is NULL", i);
   for (int i = 0; i < IPK_NUM_STAGES + 1; ++i) h->stage_ev[i] = (hipEvent_t)events[i];
   h->stages_pending = true;
+  return IPK_OK;
+}
+
+extern "C" int ipk_relpos_attn_repeat_core(ipk_relpos_attn_t* h, int32_t count, void* stream) {
+  if (!h) return fail(IPK_ERR_INVALID_ARG, "handle is NULL");
+  if (!h->has_run) return fail(IPK_ERR_INVALID_ARG, "no run yet");
+  if (h->last_noalloc)
+    return fail(IPK_ERR_INVALID_ARG, "the last run worked in the shared no-allocation array, not the handle's workspace");
+  if (count < 1 || count > IPK_MAX_REPEAT) return fail(IPK_ERR_INVALID_ARG, "count=%d outside [1, %d]", count, IPK_MAX_REPEAT);
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess || cur != h->device)
+    return fail(IPK_ERR_INVALID_ARG, "the current HIP device (%d) is not the handle's (%d)", cur, h->device);
+  for (int i = 0; i < count; ++i) {
+    const hipError_t e = launch_attention(h->last, h->w, h->last_sc, h->last_ws, h->last_lens, (hipStream_t)stream,
+                                          LaunchEv{});
+    if (e != hipSuccess) return fail(IPK_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  }
   return IPK_OK;
 }
 

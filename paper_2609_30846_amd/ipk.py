@@ -40,6 +40,7 @@ SIGNATURES = [
     ("ipk_relpos_attn_destroy", C.c_int, [_vp]),
     ("ipk_relpos_attn_intermediate", C.c_int, [_vp, C.c_int32, _vp, C.c_int64, _vp]),
     ("ipk_relpos_attn_record_stages", C.c_int, [_vp, _vp]),
+    ("ipk_relpos_attn_repeat_core", C.c_int, [_vp, C.c_int32, _vp]),
     ("ipk_relpos_attn_cache_positions", C.c_int, [_vp, _vp, C.c_int32, _vp]),
     ("ipk_relpos_attn_set_score_path", C.c_int, [_vp, C.c_int32]),
     ("ipk_relpos_attn_score_path", C.c_int, [_vp]),
@@ -296,6 +297,14 @@ def ipk_relpos_attn_record_stages(h: int, events) -> None:
     _check(load().ipk_relpos_attn_record_stages(h, arr))
 
 
+MAX_REPEAT = 100000
+
+
+def ipk_relpos_attn_repeat_core(h: int, count: int, stream=None) -> None:
+    """Enqueues the last run's attention core ``count`` more times on ``stream`` (timing)."""
+    _check(load().ipk_relpos_attn_repeat_core(h, int(count), _stream_ptr(stream)))
+
+
 class RelPosAttn:
     """Owns one handle: device copies of a block's weights, built from host arrays.
 
@@ -367,6 +376,11 @@ class RelPosAttn:
         B, T, lengths = self._check_run(x, pos_table, lengths, y)
         ipk_relpos_attn_run_noalloc(self.handle, x, pos_table, lengths, B, T, y, stream)
         return y
+
+    def repeat_core(self, count: int, stream=None):
+        """Launches the last run's attention core ``count`` more times, back to back on
+        ``stream``, on the handle's workspace (two events around it time the kernel)."""
+        ipk_relpos_attn_repeat_core(self.handle, count, stream)
 
     def cache_positions(self, pos_table, stream=None):
         """Projects ``pos_table`` ([2 T_table - 1][d] int8 on the device) once; later

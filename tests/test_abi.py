@@ -42,7 +42,7 @@ def test_noalloc_scratch_size_matches_header():
 
 
 def test_status_strings_and_version():
-    assert ipk.abi_version() == 4
+    assert ipk.abi_version() == 5
     assert ipk.status_name(0) == "IPK_OK"
     assert ipk.status_name(-1) == "IPK_ERR_INVALID_ARG"
     assert ipk.status_name(-2) == "IPK_ERR_UNSUPPORTED"
@@ -160,6 +160,7 @@ def test_null_arguments_rejected():
     assert lib.ipk_relpos_attn_run(None, None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_relpos_attn_run_noalloc(None, None, None, None, 1, 1, None, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_relpos_attn_intermediate(None, 0, None, 0, None) == ipk.IPK_ERR_INVALID_ARG
+    assert lib.ipk_relpos_attn_repeat_core(None, 1, None) == ipk.IPK_ERR_INVALID_ARG
     assert lib.ipk_relpos_attn_destroy(None) == ipk.IPK_OK
 
 
