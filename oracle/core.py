@@ -9,6 +9,7 @@ arrays.
 from __future__ import annotations
 
 import ctypes as C
+import os
 import threading
 from typing import Dict, Optional
 
@@ -72,7 +73,9 @@ def lib():
     global _lib
     with _lock:
         if _lib is None:
-            path = _build.build(force=False)
+            # IPK_ORACLE_LIB names another build of the oracle's C source: the mutation
+            # test runs the pins against copies with planted mistakes
+            path = os.environ.get("IPK_ORACLE_LIB") or _build.build(force=False)
             L = C.CDLL(path)
             L.ipk_oracle_num_threads.restype = C.c_int
             L.ipk_oracle_num_threads.argtypes = []

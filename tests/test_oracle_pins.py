@@ -170,6 +170,29 @@ def test_iexp_halves_exactly_per_ln2_step(S):
         assert core.iexp(d + q_ln2, q_ln2, q_b, q_c) == core.iexp(d, q_ln2, q_b, q_c) >> 1
 
 
+@pytest.mark.parametrize("S", [2.0 ** -4, 2.0 ** -6, 2.0 ** -8])
+def test_iexp_at_multiples_of_ln2_is_the_shifted_polynomial(S):
+    # at d = k q_ln2 the remainder is 0, so e = L(0) >> k with L(0) = q_b^2 + q_c; on its
+    # grid a S^2, L(0) is the polynomial at 0 (exp(0) = 1 within 5e-4) up to the floors
+    # of q_b = floor(b / S) and q_c = floor(c / (a S^2)): within a (2 b S + 2 S^2)
+    q_ln2, q_b, q_c = generate.softmax_constants(S)
+    L0 = q_b * q_b + q_c
+    for k in range(0, 254 // q_ln2 + 1):
+        assert core.iexp(k * q_ln2, q_ln2, q_b, q_c) == L0 >> k
+    a, b = generate.IEXP_A, generate.IEXP_B
+    assert abs(a * S * S * L0 - 1.0) <= 5e-4 + a * (2 * b * S + 2 * S * S)
+
+
+def test_softmax_clamps_its_one_value_of_256():
+    # with e(0) a power of two, 2^32 / e(0) is exact and a single key reaches
+    # floor(e0 (2^32 / e0) / 2^24) = 256, which the 8-bit grid holds as 255; two
+    # equal keys then give exactly 128 each
+    q_ln2, q_b, q_c = 11, 0, 1 << 20
+    assert core.iexp(0, q_ln2, q_b, q_c) == 1 << 20
+    assert core.softmax_row(np.array([5]), q_ln2, q_b, q_c).tolist() == [255]
+    assert core.softmax_row(np.array([5, 5]), q_ln2, q_b, q_c).tolist() == [128, 128]
+
+
 def test_softmax_closed_forms():
     q_ln2, q_b, q_c = generate.softmax_constants(2.0 ** -5)
     e0 = (q_b * q_b + q_c)
@@ -342,6 +365,65 @@ def test_padding_invariance(regime):
     y_short = core.relpos_attn(short)
     np.testing.assert_array_equal(y_pad[:, :L], y_short)
     assert np.all(y_pad[:, L:] == 0)
+    # padded query rows carry no context either (not only no output)
+    _, tr = core.relpos_attn(blk, trace=True)
+    assert np.all(tr["ctx"][:, L:] == 0)
+
+
+@pytest.mark.parametrize("branch", ["content", "position"])
+def test_scores_of_zero_queries_are_matrix_vector_products(branch):
+    # W_q = 0 makes every query 0, so Eq. 8 leaves u.K_j (content) and v.P_r (position).
+    # With the other branch's multiplier 0, each row's fused scores are Eq. 11 on one
+    # matrix-vector product: K u for every row, or P v read at r = j - i + T - 1 (relative
+    # position i - j) for row i; K and P come from numpy matmuls and big-integer Eq. 7
+    blk = make_workload("tiny", "calibrated", seed=13, T=24, B=1).blocks[0]
+    T, d = blk.T, blk.shape.d_model
+    H, dk = blk.shape.n_heads, blk.shape.d_k
+    blk.w_q = np.zeros_like(blk.w_q)
+    c = dict(blk.consts)
+    c["m_p" if branch == "content" else "m_c"] = 0
+    blk.consts = c
+
+    def eq7(rows, w, mult, n):
+        acc = rows.astype(np.int64) @ w.astype(np.int64).T
+        return np.array([[min(127, max(-127, _rs_bigint(int(a_), int(mult[j]), n))) for j, a_ in enumerate(r)]
+                         for r in acc], dtype=np.int64)
+
+    K = eq7(blk.x[0], blk.w_k, c["mult_k"], c["shift_k"])
+    P = eq7(blk.pos_table, blk.w_pos, c["mult_pos"], c["shift_pos"])
+    _, tr = core.relpos_attn(blk, trace_scores=True)
+    for h in range(H):
+        sl = slice(h * dk, (h + 1) * dk)
+        if branch == "content":
+            g = K[:, sl] @ blk.pos_bias_u[h].astype(np.int64)  # [T]
+            want = np.array([[g[j] for j in range(T)] for _ in range(T)]) * c["m_c"]
+        else:
+            g = P[:, sl] @ blk.pos_bias_v[h].astype(np.int64)  # [2T - 1]
+            want = np.array([[g[j - i + T - 1] for j in range(T)] for i in range(T)]) * c["m_p"]
+        want = np.vectorize(lambda v_: min(127, max(-127, _rs_bigint(int(v_), 1, c["shift_s"]))))(want)
+        assert np.array_equal(tr["s"][0, h].astype(np.int64), want), (branch, h)
+
+
+@pytest.mark.parametrize("regime", ["literal", "calibrated"])
+def test_uniform_attention_gives_the_requantized_sum_of_v(regime):
+    # with W_q = 0 and u = v = 0 every query is 0 and every score is RS(0) = 0, so a
+    # row over L valid keys takes the closed form of L equal keys, floor(e0 floor(2^32 /
+    # (L e0)) / 2^24), and every valid context row is Eq. 7 on that weight times the sum
+    # of V over the valid keys: the same row for every query; padded rows stay zero
+    blk = make_workload("tiny", regime, seed=11, T=40, B=2).blocks[0]
+    blk.lengths = np.array([40, 23], dtype=np.int32)
+    blk.w_q = np.zeros_like(blk.w_q)
+    blk.pos_bias_u = np.zeros_like(blk.pos_bias_u)
+    blk.pos_bias_v = np.zeros_like(blk.pos_bias_v)
+    _, tr = core.relpos_attn(blk, trace=True)
+    c = blk.consts
+    e0 = c["q_b"] * c["q_b"] + c["q_c"]
+    for b, L in enumerate(int(n) for n in blk.lengths):
+        a = min(255, (e0 * ((1 << 32) // (L * e0))) >> 24)
+        vsum = tr["v"][b, :L].astype(np.int64).sum(axis=0)
+        want = np.array([min(127, max(-127, _rs_bigint(a * int(s_), c["m_o"], c["shift_o"]))) for s_ in vsum])
+        assert np.all(tr["ctx"][b, :L] == want[None, :]), (regime, b)
+        assert np.all(tr["ctx"][b, L:] == 0)
 
 
 def test_block_close_to_fp64_relpos_attention_calibrated():
