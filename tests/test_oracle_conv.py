@@ -114,9 +114,25 @@ def test_conv_module_padding_equals_truncation():
     blk = make_workload("tiny", "calibrated", T=40, B=1).blocks[0]
     cv = make_conv(256, "calibrated", seed=22, S_z=blk.scales["S_x"])
     for L in (1, 5, 23, 39):
-        full = core.conv_module(cv, blk.x, lengths=[L])
+        full, tr = core.conv_module(cv, blk.x, lengths=[L], trace=True)
         cut = core.conv_module(cv, np.ascontiguousarray(blk.x[:, :L]))
         np.testing.assert_array_equal(full[:, :L], cut)
+        # the masking reading: the GLU output (the depthwise input) and the Swish output
+        # are zero on the padded frames
+        assert np.all(tr["g"][:, L:] == 0) and np.all(tr["o"][:, L:] == 0), L
+
+
+def test_batchnorm_grid_is_symmetric_int16():
+    # Eq. 6 with b = 16: the BatchNorm output saturates at +-32767 (never -32768); a
+    # huge depthwise multiplier drives most values to both ends
+    blk = make_workload("tiny", "literal", T=24, B=1).blocks[0]
+    cv = make_conv(256, "literal", seed=24, S_z=blk.scales["S_x"])
+    cv.mult_dw = np.full_like(cv.mult_dw, (1 << 23) - 1)
+    cv.shift_dw = 1
+    _, tr = core.conv_module(cv, blk.x, trace=True)
+    v = tr["v"].astype(np.int64)
+    assert v.min() == -32767 and v.max() == 32767
+    assert np.mean(np.abs(v) == 32767) > 0.5
 
 
 def test_conv_module_against_float64():

@@ -89,6 +89,25 @@ def test_ffn_module_matches_numpy(regime):
     np.testing.assert_array_equal(z2, ref)
 
 
+def test_ffn_swish_stage_beyond_the_clip_point():
+    # Eq. 12's tanh^ is +-1 beyond |x| >= c, so the Swish is the identity for h >= q_c
+    # and zero for h <= -q_c: on h's grid q_sw = -(|h| + h) q_1, i.e. -2 h q_1 or 0;
+    # the module's Swish output there is Eq. 7 on that value (the literal grids put
+    # q_c below 127, so the saturated h reach it)
+    blk = make_workload("tiny", "literal", T=40).blocks[0]
+    f = make_ffn(256, "literal", seed=13, S_z=blk.scales["S_x"])
+    assert f.sw_qc <= 127
+    _, tr = core.ffn_module(f, blk.x, trace=True)
+    h = tr["h"].astype(np.int64).ravel()
+    o = tr["o"].astype(np.int64).ravel()
+    sat = np.abs(h) >= f.sw_qc
+    assert np.sum(h >= f.sw_qc) > 100 and np.sum(h <= -f.sw_qc) > 100
+    for hv, ov in zip(h[sat], o[sat]):
+        q = -(abs(int(hv)) + int(hv)) * int(f.sw_q1)
+        want = max(-127, min(127, (q * int(f.m_sw) + (1 << (int(f.shift_sw) - 1))) // (1 << int(f.shift_sw))))
+        assert ov == want, (hv, ov, want)
+
+
 def test_ffn_module_rows_are_independent():
     blk = make_workload("tiny", "calibrated", T=48).blocks[0]
     f = make_ffn(256, "calibrated", seed=12, S_z=blk.scales["S_x"])

@@ -2,12 +2,14 @@
 
 Each case plants one mistake in a copy of the C oracle (a dropped term, a wrong sign,
 index or operand, an off-by-one shift, a missing clamp or mask), builds the copy with
-gcc and runs tests/test_oracle_pins.py against it in a child process
-(IPK_ORACLE_LIB points the oracle's loader at the copy).  Every copy must fail at least
-one pin other than the brute-force block, which restates the method's steps in numpy
-and so would share a misreading of the paper; the pins that do catch each mistake are
-closed forms, big-integer arithmetic, library routines, exp() and float-softmax
-bounds, the pad-reshape-slice relative shift, padding invariance and the FP64 block.
+gcc and runs the oracle's pin files against it in a child process (IPK_ORACLE_LIB
+points the oracle's loader at the copy).  Every copy must fail at least one pin other
+than the numpy evaluations of the block and of the two modules, which restate the
+method's steps and so would share a misreading of the paper; the pins that do catch
+each mistake are closed forms, big-integer arithmetic, library routines (numpy's
+matmul and correlate, Python's integer square root), exp(), float-softmax and
+polynomial bounds, the pad-reshape-slice relative shift, padding invariance and the
+float64 block and modules.
 """
 
 import concurrent.futures as cf
@@ -21,7 +23,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "ipk_oracle.c")
-RESTATEMENT = "test_block_matches_brute_force"
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_residual.py", "test_oracle_ffn.py", "test_oracle_conv.py"]
+RESTATEMENTS = {"test_block_matches_brute_force", "test_ffn_module_matches_numpy", "test_conv_module_matches_numpy"}
 
 # (name, [(text in the oracle, planted replacement), ...])
 MUTANTS = [
@@ -71,6 +74,55 @@ MUTANTS = [
          "ipk_oracle_linear(pos_table, R, d, D->w_k, d, D->mult_pos, D->shift_pos, P);")]),
     ("first padded query row computed", [
         ("if (i >= L) continue; /* padded query rows stay zero */", "if (i > L || i >= T) continue;")]),
+    # LayerNorm, the residual add and the two modules around the block
+    ("LayerNorm mean ties rounded down", [
+        ("const int64_t mu = floor_div(2 * s + d, 2 * (int64_t)d);",
+         "const int64_t mu = floor_div(2 * s + d - 1, 2 * (int64_t)d);")]),
+    ("LayerNorm sigma one too large", [
+        ("int64_t sigma = ipk_oracle_isqrt(v);", "int64_t sigma = ipk_oracle_isqrt(v) + 1;")]),
+    ("integer square root one step late", [
+        ("if (nx >= x) return x;", "if (nx >= x) return nx;")]),
+    ("LayerNorm F = 2^30 / sigma", [
+        ("const int64_t F = ((int64_t)1 << 31) / sigma;", "const int64_t F = ((int64_t)1 << 30) / sigma;")]),
+    ("LayerNorm u = y F / 4", [
+        ("const int64_t u = floor_div_pow2((z[k] - mu) * F, 1);",
+         "const int64_t u = floor_div_pow2((z[k] - mu) * F, 2);")]),
+    ("LayerNorm without beta", [
+        ("x[k] = (int8_t)ipk_oracle_clamp8(floor_div_pow2(u * g[k] + c[k] + half, shift));",
+         "x[k] = (int8_t)ipk_oracle_clamp8(floor_div_pow2(u * g[k] + half, shift));")]),
+    ("MHSA residual multipliers swapped", [
+        ("z2[i] = (int8_t)ipk_oracle_residual(z1[i], y[i], m_z, m_y, shift_r);",
+         "z2[i] = (int8_t)ipk_oracle_residual(z1[i], y[i], m_y, m_z, shift_r);")]),
+    ("residual ties rounded down", [
+        ("return ipk_oracle_clamp8(floor_div_pow2(m_z * z1 + m_y * y + ((int64_t)1 << (shift - 1)), shift));",
+         "return ipk_oracle_clamp8(floor_div_pow2(m_z * z1 + m_y * y + ((int64_t)1 << (shift - 1)) - 1, shift));")]),
+    ("Swish with the wrong sign of the odd term", [
+        ("return -(aq * L + q * q_1);", "return -(aq * L - q * q_1);")]),
+    ("Swish clips with max instead of min", [
+        ("const int64_t t = (aq < q_c ? aq : q_c) - q_c;\n  const int64_t L = t * t + q_1;\n  return -(aq",
+         "const int64_t t = (aq > q_c ? aq : q_c) - q_c;\n  const int64_t L = t * t + q_1;\n  return -(aq")]),
+    ("sigmoid with the wrong sign", [
+        ("const int64_t sg = q > 0 ? 1 : (q < 0 ? -1 : 0);", "const int64_t sg = q > 0 ? -1 : (q < 0 ? 1 : 0);")]),
+    ("GLU gates with the wrong half", [
+        ("ipk_oracle_int_sigmoid(u[r * 2 * d + d + c], D->glu_qc, D->glu_q1);",
+         "ipk_oracle_int_sigmoid(u[r * 2 * d + c], D->glu_qc, D->glu_q1);")]),
+    ("depthwise taps off centre", [
+        ("const int32_t ts = t + k - 4;", "const int32_t ts = t + k - 3;")]),
+    ("depthwise without the folded BatchNorm bias", [
+        ("int64_t acc = D->bias_dw[c];", "int64_t acc = 0;")]),
+    ("int16 grid down to -32768", [
+        ("return v < -32767 ? -32767 : (v > 32767 ? 32767 : v);",
+         "return v < -32768 ? -32768 : (v > 32767 ? 32767 : v);")]),
+    ("GLU output not masked", [
+        ("        int64_t gv = 0;\n        if (t < L) {", "        int64_t gv = 0;\n        if (t < T) {")]),
+    ("Swish output not masked", [
+        ("if (t < L) ov = ipk_oracle_clamp8", "if (t < T) ov = ipk_oracle_clamp8")]),
+    ("feed-forward Swish constants swapped", [
+        ("ipk_oracle_rs(ipk_oracle_int_swish(h[i], D->sw_qc, D->sw_q1), D->m_sw, D->shift_sw)",
+         "ipk_oracle_rs(ipk_oracle_int_swish(h[i], D->sw_q1, D->sw_qc), D->m_sw, D->shift_sw)")]),
+    ("feed-forward residual multipliers swapped", [
+        ("z_out[i] = (int8_t)ipk_oracle_residual(z[i], y[i], D->m_z, D->m_y, D->shift_r);\n  if (x_out) memcpy(x_out, x, (size_t)(rows * d));\n  if (h_out)",
+         "z_out[i] = (int8_t)ipk_oracle_residual(z[i], y[i], D->m_y, D->m_z, D->shift_r);\n  if (x_out) memcpy(x_out, x, (size_t)(rows * d));\n  if (h_out)")]),
 ]
 
 
@@ -86,8 +138,8 @@ def _failed_pins(name, reps, work):
     subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-o", lib, c_file], check=True)
     report = os.path.join(work, tag + ".xml")
     env = dict(os.environ, IPK_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
-    res = subprocess.run([sys.executable, "-m", "pytest", os.path.join("tests", "test_oracle_pins.py"), "-q",
-                          "-p", "no:cacheprovider", f"--junitxml={report}"],
+    res = subprocess.run([sys.executable, "-m", "pytest"] + [os.path.join("tests", f) for f in PIN_FILES] +
+                         ["-q", "-p", "no:cacheprovider", f"--junitxml={report}"],
                          cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     failed = set()
     for case in ET.parse(report).getroot().iter("testcase"):
@@ -97,12 +149,12 @@ def _failed_pins(name, reps, work):
 
 
 def test_every_planted_mistake_fails_an_independent_pin(tmp_path):
-    with cf.ThreadPoolExecutor(4) as pool:
+    with cf.ThreadPoolExecutor(max(2, min(6, (os.cpu_count() or 4) - 2))) as pool:
         results = list(pool.map(lambda m: (m[0],) + _failed_pins(m[0], m[1], str(tmp_path)), MUTANTS))
     missed = []
     for name, rc, failed in results:
         print(f"[mutant] {name}: {rc=} caught by {failed}")
-        if rc == 0 or not set(failed) - {RESTATEMENT}:
+        if rc == 0 or not set(failed) - RESTATEMENTS:
             missed.append(name)
     assert not missed, f"planted mistakes no independent pin catches: {missed}"
 

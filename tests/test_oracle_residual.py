@@ -93,6 +93,53 @@ def test_layernorm_shift_invariance_and_constant_rows():
     assert np.array_equal(core.layernorm(z[:, perm], res_p), base[:, perm])
 
 
+def _unit_affine(d, shift):
+    # g = 1, c = 0: the output is u on the grid 2^-shift, rounded half up and clamped
+    from workloads.generate import Residual
+
+    return Residual(ln_mult=np.ones(d, np.int32), ln_bias=np.zeros(d, np.int64), ln_shift=shift, m_z=0, m_y=0,
+                    shift_r=1, scales={})
+
+
+def test_layernorm_mean_ties_round_up():
+    # the alternating 0/1 row has mean exactly 1/2, which rounds up to mu = 1: the ones
+    # sit at the mean (u = 0, output 0) and the zeros below it (with mu = 0 it would be
+    # the zeros at 0 and the ones above)
+    d = 256
+    z = np.tile(np.array([0, 1], np.int8), d // 2)[None, :]
+    x = core.layernorm(z, _unit_affine(d, 24))[0]
+    assert np.all(x[1::2] == 0)
+    assert np.all(x[0::2] < 0)
+
+
+def test_layernorm_of_a_plus_minus_one_row_is_exactly_unit():
+    # +-1 alternating over d = 256: mean 0, sum of squares 256, sigma = 16 exactly and
+    # F = 2^31 / 16 = 2^27, so u = +-2^26, i.e. (z - mean) / std = +-1 on the grid
+    # 2^30 / sqrt(d) of u; with g = 1, c = 0 and shift 20 the output is +-64 exactly
+    d = 256
+    z = np.tile(np.array([1, -1], np.int8), d // 2)[None, :]
+    x = core.layernorm(z, _unit_affine(d, 20))[0]
+    assert np.array_equal(x.astype(np.int64), 64 * z[0].astype(np.int64))
+
+
+def test_residual_rounds_ties_up():
+    # Eq. 2's add on Z2's grid is RS of m_z z1 + m_y y: against Python big integers on
+    # random values and on exact ties of both signs
+    rng = np.random.default_rng(19)
+    for _ in range(3000):
+        z1, y = (int(v) for v in rng.integers(-127, 128, size=2))
+        m_z, m_y = (int(v) for v in rng.integers(0, 1 << 22, size=2))
+        n = int(rng.integers(1, 30))
+        t = m_z * z1 + m_y * y
+        want = max(-127, min(127, (t + (1 << (n - 1))) // (1 << n)))
+        assert core.residual(z1, y, m_z, m_y, n) == want
+    for n in (1, 4, 12):
+        for z1 in (-7, -3, -1, 1, 3, 7):
+            # m_z z1 = z1 2^(n-1): an odd multiple of 2^(n-1) is an exact tie
+            got = core.residual(z1, 0, 1 << (n - 1), 0, n)
+            assert got == (z1 + 1) // 2, (n, z1)
+
+
 def test_residual_reduces_to_eq7_and_tracks_the_real_sum():
     rng = np.random.default_rng(9)
     for _ in range(2000):
