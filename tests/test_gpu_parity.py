@@ -223,6 +223,30 @@ def test_single_tile_workgroups(gpu_lib, T, lengths):
             assert _first_mismatch(g["y"], y) is None, (T, d // H, regime, _first_mismatch(g["y"], y))
 
 
+@pytest.mark.parametrize("T", [1, 20, 70])
+def test_largest_batch(gpu_lib, T):
+    """IPK_MAX_BATCH utterances in one call, ragged lengths from 1 to T (every
+    utterance's length travels in the launch arguments), both regimes, with the
+    intermediates compared too."""
+    import dataclasses
+
+    from workloads import generate
+
+    B = gpu_lib.IPK_MAX_BATCH
+    rng = np.random.default_rng(T)
+    lengths = [int(v) for v in rng.integers(1, T + 1, size=B)]
+    lengths[0], lengths[-1] = T, 1
+    shape = dataclasses.replace(generate.config_by_name("tiny"), B=B, name="tiny")
+    for regime in ("literal", "calibrated"):
+        blk = generate.make_block(shape, T, np.random.default_rng(7 * T + 1), regime, lengths=lengths)
+        print(f"[parity] largest batch B={B} T={T} {regime}", flush=True)
+        g = _run_gpu(gpu_lib, blk, inter=True)
+        y, tr = core.relpos_attn(blk, trace=True)
+        for k in ("q", "k", "v", "p", "ctx"):
+            assert _first_mismatch(g[k], tr[k]) is None, (T, regime, k, _first_mismatch(g[k], tr[k]))
+        assert _first_mismatch(g["y"], y) is None, (T, regime, _first_mismatch(g["y"], y))
+
+
 def test_longest_supported_T(gpu_lib):
     """The longest utterance the on-chip score rows allow (create rejects a longer
     max_T with IPK_ERR_UNSUPPORTED), d_k = 64 and 128."""
