@@ -690,6 +690,18 @@ hipError_t launch_linear(const int8_t* x, int rows, int K, int N, const int8_t* 
     a.nprob = 1;
     return launch_gemm<TN, TM, NWAVE, WN>(a, tiles, st, LaunchEv{});
   };
+  // 128-channel x 192-token tiles (eight waves of 32 x 96) when they leave the busiest
+  // CU less work than the 256-channel shape picked above (2500 rows, N = 2048: 224 tiles
+  // of 24.6 K outputs against 160 of 32.8 K)
+  const long t128 = (long)((rows + 191) / 192) * ((N + 127) / 128);
+  const long rounds_wide = (tiles_of(TMr) + kGemmCUs - 1) / kGemmCUs, rounds128 = (t128 + kGemmCUs - 1) / kGemmCUs;
+  if (rounds128 * 128 * 192 < rounds_wide * TN * TMr) {
+    GemmArgs a{};
+    a.y = y;
+    const int tiles = add_problem(a, 0, x, w, rq, 1, rows, N, K, OUT_ROWMAJOR, 0, 128, 192);
+    a.nprob = 1;
+    return launch_gemm<128, 192, 8, 4>(a, tiles, st, LaunchEv{});
+  }
   if (TMr == 128) return go(std::integral_constant<int, 128>{});
   if (TMr == 192) return go(std::integral_constant<int, 192>{});
   return go(std::integral_constant<int, 256>{});
