@@ -41,6 +41,12 @@ def test_noalloc_scratch_size_matches_header():
     assert m and int(m.group(1)) * 1024 * 1024 == ipk.IPK_NOALLOC_SCRATCH_BYTES
 
 
+def test_repeat_limit_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define IPK_MAX_REPEAT (\d+)", text)
+    assert m and int(m.group(1)) == ipk.MAX_REPEAT
+
+
 def test_status_strings_and_version():
     assert ipk.abi_version() == 5
     assert ipk.status_name(0) == "IPK_OK"
